@@ -1,0 +1,339 @@
+"""Seeded synthetic workloads for prefix-extend attention.
+
+This module only *generates inputs*: per-request (prefix_len, extend_len) pairs,
+the physical placement of every request's KV pages in the pool, fp8 scales and
+bf16 Q/K/V values.  It holds none of the attention arithmetic and none of the
+KV-store arithmetic, so both the CPU oracle (tests) and the HIP path draw their
+inputs from it without sharing any of the method's code.
+
+The workload shapes stand in for the agent traces of the paper (Section 4,
+Experimental setup), which are not available: a returning agent reuses a cached
+prefix and prefills only the uncached suffix (Section 1; Section 2, "Prefix
+caching for multi-turn agents"); a fully evicted agent recomputes its whole
+context (Section 3.1); round-robin tail eviction leaves partial prefixes whose
+lost tail chunks are recomputed (Section 3.2, Algorithm 1).
+
+Generation order (fixed, so every draw is reproducible):
+  * ``numpy.random.default_rng([config_id, 0, seed])`` draws the lengths, then
+    one permutation of the pool's pages, then the fp8 K scales and V scales.
+  * Each request's values come from torch generators seeded by
+    ``SeedSequence([config_id, 1, seed, kind, r])`` with kind 0 = Q, 1 = K, 2 = V.
+    Values are drawn as fp32 N(0, sigma^2) and rounded to bf16 (RNE); the bf16
+    values *are* the inputs.  The values depend on the device type the
+    generator runs on (torch's CPU and GPU generators differ), so a test always
+    hands the same tensors to both sides.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+PAGE_SIZE = 16
+
+KV_BF16 = 0
+KV_FP8_E4M3 = 1
+
+# Named synthetic configurations (prefix-extend batches of agent-shaped requests).
+CONFIG_IDS = {
+    "tiny": 1,          # 4 requests, 4/2 heads, head_dim 64
+    "llama8b": 2,       # 16 returning agents, Llama-3-8B-shaped layer
+    "tail_outlier": 3,  # one fully evicted 131072-token recompute + 31 partial hits
+    "rr_partial": 4,    # 64 agents that lost 1-4 tail chunks of 2048 tokens
+    "wide70b": 5,       # 48 requests, 64/8 heads, bf16 K/V pool
+    "wide70b_fp8": 5,   # same batch, fp8 e4m3 K/V pool with per-head scales
+}
+
+
+@dataclasses.dataclass
+class Workload:
+    """Shapes and page placement of one prefix-extend batch (host arrays)."""
+
+    name: str
+    config_id: int
+    seed: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    prefix_lens: np.ndarray           # int32 [R]
+    extend_lens: np.ndarray           # int32 [R]
+    num_pages: int                    # pool capacity in pages
+    page_indptr: np.ndarray           # int32 [R+1]: request r owns page_ids[indptr[r]:indptr[r+1]]
+    page_ids: np.ndarray              # int32: logical page j of request r -> physical page
+    kv_dtype: int = KV_BF16
+    k_scale: Optional[np.ndarray] = None  # float32 [Hkv] for the fp8 pool
+    v_scale: Optional[np.ndarray] = None
+    sigma: float = 1.0                # std of K and V values
+    q_sigma: float = 1.0              # std of Q values
+    page_size: int = PAGE_SIZE
+
+    @property
+    def num_reqs(self) -> int:
+        return int(self.prefix_lens.shape[0])
+
+    @property
+    def seq_lens(self) -> np.ndarray:
+        return (self.prefix_lens.astype(np.int64) + self.extend_lens).astype(np.int64)
+
+    @property
+    def qo_indptr(self) -> np.ndarray:
+        out = np.zeros(self.num_reqs + 1, dtype=np.int32)
+        np.cumsum(self.extend_lens, out=out[1:])
+        return out
+
+    @property
+    def total_extend(self) -> int:
+        return int(self.extend_lens.astype(np.int64).sum())
+
+    @property
+    def group(self) -> int:
+        return self.num_q_heads // self.num_kv_heads
+
+    @property
+    def sm_scale(self) -> float:
+        return 1.0 / math.sqrt(self.head_dim)
+
+    def pages_of(self, r: int) -> np.ndarray:
+        return self.page_ids[self.page_indptr[r]:self.page_indptr[r + 1]]
+
+    def visible_pairs(self) -> int:
+        """Number of (query row, key) pairs a causal prefix-extend pass visits, per q-head."""
+        p = self.prefix_lens.astype(np.int64)
+        e = self.extend_lens.astype(np.int64)
+        return int((e * p + e * (e + 1) // 2).sum())
+
+    def flops(self) -> float:
+        """Algorithmic FLOPs of one attention pass: 4*d*Hq per visible causal pair."""
+        return 4.0 * self.head_dim * self.num_q_heads * self.visible_pairs()
+
+    def subset(self, reqs: Sequence[int], compact_pages: bool = True) -> "Workload":
+        """Restrict to some requests.  With ``compact_pages`` their pages are renumbered
+        0..n-1 in order of appearance (a smaller pool with the same logical contents)."""
+        reqs = [int(r) for r in reqs]
+        pages = [self.pages_of(r) for r in reqs]
+        indptr = np.zeros(len(reqs) + 1, dtype=np.int32)
+        np.cumsum([len(p) for p in pages], out=indptr[1:])
+        ids = np.concatenate(pages).astype(np.int32) if pages else np.zeros(0, np.int32)
+        num_pages = self.num_pages
+        if compact_pages:
+            ids = np.arange(len(ids), dtype=np.int32)
+            num_pages = max(1, len(ids))
+        return dataclasses.replace(
+            self, prefix_lens=self.prefix_lens[reqs].copy(), extend_lens=self.extend_lens[reqs].copy(),
+            page_indptr=indptr, page_ids=ids, num_pages=num_pages)
+
+
+def _pages_needed(prefix_lens: np.ndarray, extend_lens: np.ndarray, page_size: int) -> np.ndarray:
+    total = prefix_lens.astype(np.int64) + extend_lens.astype(np.int64)
+    return (total + page_size - 1) // page_size
+
+
+def _round_to(x: np.ndarray, m: int) -> np.ndarray:
+    return (np.round(x / m) * m).astype(np.int64)
+
+
+def _place_pages(need: np.ndarray, num_pages: int, perm: np.ndarray):
+    indptr = np.zeros(len(need) + 1, dtype=np.int32)
+    np.cumsum(need, out=indptr[1:])
+    total = int(indptr[-1])
+    if total > num_pages:
+        raise ValueError(f"pool of {num_pages} pages cannot hold {total} pages")
+    return indptr, perm[:total].astype(np.int32)
+
+
+def make_custom(prefix_lens, extend_lens, num_q_heads, num_kv_heads, head_dim, *,
+                num_pages: Optional[int] = None, pool_factor: float = 1.5,
+                placement: str = "random", kv_dtype: int = KV_BF16,
+                k_scale=None, v_scale=None, sigma: float = 1.0, q_sigma: Optional[float] = None,
+                seed: int = 0, config_id: int = 99, name: str = "custom") -> Workload:
+    """A workload with explicit lengths.  ``placement`` is ``random`` (seeded shuffle of
+    the pool) or ``linear`` (pages 0, 1, 2, ... in request order)."""
+    p = np.asarray(prefix_lens, dtype=np.int32)
+    e = np.asarray(extend_lens, dtype=np.int32)
+    if p.shape != e.shape or (p < 0).any() or (e < 0).any():
+        raise ValueError("prefix_lens / extend_lens must be non-negative and equal length")
+    need = _pages_needed(p, e, PAGE_SIZE)
+    if num_pages is None:
+        num_pages = max(1, int(math.ceil(pool_factor * max(1, int(need.sum())))))
+    rng = np.random.default_rng([config_id, 0, seed])
+    if placement == "random":
+        perm = rng.permutation(num_pages)
+    elif placement == "linear":
+        perm = np.arange(num_pages)
+    else:
+        raise ValueError(placement)
+    indptr, ids = _place_pages(need, num_pages, perm)
+    if kv_dtype == KV_FP8_E4M3:
+        if k_scale is None:
+            k_scale = rng.uniform(0.01, 0.1, num_kv_heads)
+        if v_scale is None:
+            v_scale = rng.uniform(0.01, 0.1, num_kv_heads)
+        k_scale = np.asarray(k_scale, dtype=np.float32)
+        v_scale = np.asarray(v_scale, dtype=np.float32)
+    return Workload(name=name, config_id=config_id, seed=seed, num_q_heads=num_q_heads,
+                    num_kv_heads=num_kv_heads, head_dim=head_dim, prefix_lens=p, extend_lens=e,
+                    num_pages=int(num_pages), page_indptr=indptr, page_ids=ids, kv_dtype=kv_dtype,
+                    k_scale=k_scale, v_scale=v_scale, sigma=sigma,
+                    q_sigma=sigma if q_sigma is None else q_sigma)
+
+
+def make_workload(name: str, seed: int = 0) -> Workload:
+    """The five named agent-shaped batches (lengths and page placement only)."""
+    if name not in CONFIG_IDS:
+        raise KeyError(f"unknown workload {name!r}; known: {sorted(CONFIG_IDS)}")
+    cid = CONFIG_IDS[name]
+    rng = np.random.default_rng([cid, 0, seed])
+    kv_dtype = KV_BF16
+    sigma = 1.0
+    if name == "tiny":
+        hq, hkv, d = 4, 2, 64
+        p = np.array([0, 64, 208, 512])
+        e = np.array([32, 16, 100, 8])
+        num_pages = 256
+    elif name == "llama8b":
+        hq, hkv, d = 32, 8, 128
+        p = _round_to(rng.integers(4096, 32768 + 1, 16), PAGE_SIZE)
+        e = rng.integers(64, 2048 + 1, 16)
+        sigma = 0.5
+        num_pages = None
+    elif name == "tail_outlier":
+        hq, hkv, d = 32, 8, 128
+        p = np.concatenate([[0], _round_to(rng.integers(32768, 98304 + 1, 31), PAGE_SIZE)])
+        e = np.concatenate([[131072], rng.integers(256, 1024 + 1, 31)])
+        num_pages = None
+    elif name == "rr_partial":
+        hq, hkv, d = 32, 8, 128
+        ctx = np.exp(rng.uniform(math.log(8192), math.log(196608), 64))
+        ctx = (np.floor(ctx / PAGE_SIZE) * PAGE_SIZE).astype(np.int64)
+        k = rng.integers(1, 4 + 1, 64)
+        new = rng.integers(128, 4096 + 1, 64)
+        p = ctx - 2048 * k
+        e = 2048 * k + new
+        num_pages = None
+    else:  # wide70b, wide70b_fp8
+        hq, hkv, d = 64, 8, 128
+        p = _round_to(np.exp(rng.uniform(math.log(16384), math.log(262144), 48)), PAGE_SIZE)
+        e = rng.integers(512, 8192 + 1, 48)
+        num_pages = None
+        if name == "wide70b_fp8":
+            kv_dtype = KV_FP8_E4M3
+    p = p.astype(np.int32)
+    e = e.astype(np.int32)
+    need = _pages_needed(p, e, PAGE_SIZE)
+    if num_pages is None:
+        num_pages = int(math.ceil(1.5 * int(need.sum())))
+    perm = rng.permutation(num_pages)
+    indptr, ids = _place_pages(need, num_pages, perm)
+    k_scale = v_scale = None
+    if name.startswith("wide70b"):
+        # drawn for both wide70b runs so the two share lengths, pages and seeds
+        k_scale = rng.uniform(0.01, 0.1, hkv).astype(np.float32)
+        v_scale = rng.uniform(0.01, 0.1, hkv).astype(np.float32)
+        if kv_dtype == KV_BF16:
+            k_scale = v_scale = None
+    return Workload(name=name, config_id=cid, seed=seed, num_q_heads=hq, num_kv_heads=hkv,
+                    head_dim=d, prefix_lens=p, extend_lens=e, num_pages=num_pages,
+                    page_indptr=indptr, page_ids=ids, kv_dtype=kv_dtype, k_scale=k_scale,
+                    v_scale=v_scale, sigma=sigma, q_sigma=sigma)
+
+
+# ----------------------------------------------------------------------------- values
+
+def _torch_seed(*parts: int) -> int:
+    state = np.random.SeedSequence([int(x) for x in parts]).generate_state(2, dtype=np.uint32)
+    return int((int(state[0]) << 31) ^ int(state[1])) & ((1 << 62) - 1)
+
+
+def _randn_bf16(shape, sigma: float, seed: int, device) -> torch.Tensor:
+    dev = torch.device(device)
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    x = torch.randn(shape, generator=g, device=dev, dtype=torch.float32)
+    if sigma != 1.0:
+        x.mul_(sigma)
+    return x.to(torch.bfloat16)
+
+
+def request_q(w: Workload, r: int, device="cpu") -> torch.Tensor:
+    """Q rows of request r's uncached suffix: bf16 [E_r, Hq, d]."""
+    e = int(w.extend_lens[r])
+    return _randn_bf16((e, w.num_q_heads, w.head_dim), w.q_sigma,
+                       _torch_seed(w.config_id, 1, w.seed, 0, r), device)
+
+
+def request_kv(w: Workload, r: int, device="cpu"):
+    """The logical K and V sequences of request r (cached prefix then suffix): bf16 [L_r, Hkv, d]."""
+    n = int(w.prefix_lens[r]) + int(w.extend_lens[r])
+    shape = (n, w.num_kv_heads, w.head_dim)
+    k = _randn_bf16(shape, w.sigma, _torch_seed(w.config_id, 1, w.seed, 1, r), device)
+    v = _randn_bf16(shape, w.sigma, _torch_seed(w.config_id, 1, w.seed, 2, r), device)
+    return k, v
+
+
+def batch_tensors(w: Workload, device="cpu", reqs: Optional[Sequence[int]] = None):
+    """Concatenated inputs of one prefix-extend call.
+
+    Returns a dict with
+      ``q``        bf16 [T, Hq, d]    suffix queries (T = sum of extend_lens)
+      ``k_ext``    bf16 [T, Hkv, d]   suffix keys   (written by the KV store)
+      ``v_ext``    bf16 [T, Hkv, d]   suffix values
+      ``k_hist``   bf16 [sum P, Hkv, d] cached-prefix keys (written by an earlier turn)
+      ``v_hist``   bf16 [sum P, Hkv, d]
+    """
+    reqs = range(w.num_reqs) if reqs is None else reqs
+    qs, ke, ve, kh, vh = [], [], [], [], []
+    for r in reqs:
+        p = int(w.prefix_lens[r])
+        qs.append(request_q(w, r, device))
+        k, v = request_kv(w, r, device)
+        kh.append(k[:p])
+        vh.append(v[:p])
+        ke.append(k[p:])
+        ve.append(v[p:])
+        del k, v
+    def cat(xs, heads):
+        if xs:
+            return torch.cat(xs, 0)
+        return torch.zeros((0, heads, w.head_dim), dtype=torch.bfloat16, device=device)
+    return dict(q=cat(qs, w.num_q_heads), k_ext=cat(ke, w.num_kv_heads), v_ext=cat(ve, w.num_kv_heads),
+                k_hist=cat(kh, w.num_kv_heads), v_hist=cat(vh, w.num_kv_heads))
+
+
+def history_batch(w: Workload) -> Workload:
+    """The earlier turn that produced the cached prefixes: each request with prefix 0 and
+    extend = its cached prefix_len, on the same pages (the leading ceil(P/16) of them)."""
+    need = (w.prefix_lens.astype(np.int64) + w.page_size - 1) // w.page_size
+    indptr = np.zeros(w.num_reqs + 1, dtype=np.int32)
+    np.cumsum(need, out=indptr[1:])
+    ids = np.concatenate([w.pages_of(r)[:int(need[r])] for r in range(w.num_reqs)]
+                         ).astype(np.int32) if w.num_reqs else np.zeros(0, np.int32)
+    return dataclasses.replace(w, prefix_lens=np.zeros_like(w.prefix_lens),
+                               extend_lens=w.prefix_lens.copy(), page_indptr=indptr, page_ids=ids)
+
+
+def sample_rows(w: Workload, per_req: int, seed: int = 0, reqs: Optional[Sequence[int]] = None):
+    """Seeded rows (r, i) to check at full size: always the first and last suffix row and
+    a page-boundary row, plus random rows, ``per_req`` per request (fewer if E is small)."""
+    rng = np.random.default_rng([w.config_id, 2, seed])
+    reqs = range(w.num_reqs) if reqs is None else reqs
+    out = []
+    for r in reqs:
+        e = int(w.extend_lens[r])
+        p = int(w.prefix_lens[r])
+        if e == 0:
+            continue
+        chosen = {0, e - 1}
+        nb = (-p) % w.page_size  # first suffix row whose absolute position starts a page
+        if nb < e:
+            chosen.add(nb)
+        if e > 1 and nb + w.page_size - 1 < e:
+            chosen.add(nb + w.page_size - 1)
+        want = min(per_req, e)
+        while len(chosen) < want:
+            chosen.add(int(rng.integers(0, e)))
+        out.extend((r, i) for i in sorted(chosen))
+    return np.array(out, dtype=np.int32).reshape(-1, 2)

@@ -1,0 +1,94 @@
+"""Test helpers: an independent brute-force attention (numpy/scipy, no page table)
+and builders that run the oracle over a generated workload.
+
+The brute force is deliberately formulated differently from the oracle: it
+materialises the whole (suffix x context) score matrix of a request from the
+*logical* K/V sequence (never from a pool), expands KV heads to query heads with
+``numpy.repeat`` and applies softmax/logsumexp from scipy.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import scipy.special
+import torch
+
+import oracle
+from paper_2609_32278_amd import workloads as wl
+
+
+def to_f64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().to(torch.float64).numpy()
+
+
+def brute_force(q: np.ndarray, k: np.ndarray, v: np.ndarray, prefix_len: int, sm_scale: float):
+    """q [E, Hq, d], k/v [L, Hkv, d] float64 (the logical sequence), L = P + E.
+    Returns out [E, Hq, d] and lse [E, Hq] of bottom-right-aligned causal attention."""
+    e, hq, d = q.shape
+    n, hkv, _ = k.shape
+    assert n == prefix_len + e
+    g = hq // hkv
+    kx = np.repeat(k, g, axis=1)  # [L, Hq, d]: query head h reads kv head h // g
+    vx = np.repeat(v, g, axis=1)
+    s = np.einsum("ihc,jhc->hij", q, kx) * sm_scale  # [Hq, E, L]
+    rows = np.arange(e)[:, None] + prefix_len
+    cols = np.arange(n)[None, :]
+    s = np.where(cols <= rows, s, -np.inf)
+    p = scipy.special.softmax(s, axis=-1)
+    out = np.einsum("hij,jhc->ihc", p, vx)
+    lse = scipy.special.logsumexp(s, axis=-1).T  # [E, Hq]
+    return out, lse
+
+
+def oracle_pool_for(w: wl.Workload, t: dict, fill=None) -> oracle.OraclePool:
+    """An oracle pool holding the workload's cached prefixes (stored by an earlier
+    turn, the history batch) and then its suffix rows (this turn's KV store)."""
+    pool = oracle.OraclePool(w.num_pages, w.num_kv_heads, w.head_dim, w.kv_dtype, w.page_size,
+                             w.k_scale, w.v_scale, fill=fill)
+    h = wl.history_batch(w)
+    oracle.store_kv(pool, h.prefix_lens, h.extend_lens, h.page_indptr, h.page_ids,
+                    t["k_hist"], t["v_hist"])
+    oracle.store_kv(pool, w.prefix_lens, w.extend_lens, w.page_indptr, w.page_ids,
+                    t["k_ext"], t["v_ext"])
+    return pool
+
+
+def oracle_all_rows(w: wl.Workload, pool: oracle.OraclePool, q: torch.Tensor, mutant="none",
+                    want_lse=False, num_threads=0):
+    rr, rp = oracle.all_rows(w.extend_lens)
+    return oracle.extend_attention(pool, w.prefix_lens, w.extend_lens, w.page_indptr, w.page_ids,
+                                   q, rr, rp, w.num_q_heads, w.sm_scale, mutant=mutant,
+                                   want_lse=want_lse, num_threads=num_threads)
+
+
+def brute_force_all(w: wl.Workload, dequant=None):
+    """Brute-force outputs for every suffix row of every request, from the generator's
+    logical sequences.  ``dequant(k, v)`` maps the float64 logical K/V to what the pool
+    holds (identity for bf16)."""
+    outs, lses = [], []
+    for r in range(w.num_reqs):
+        q = to_f64(wl.request_q(w, r))
+        k, v = wl.request_kv(w, r)
+        k, v = to_f64(k), to_f64(v)
+        if dequant is not None:
+            k, v = dequant(k, v)
+        o, l = brute_force(q, k, v, int(w.prefix_lens[r]), w.sm_scale)
+        outs.append(o)
+        lses.append(l)
+    return np.concatenate(outs, 0), np.concatenate(lses, 0)
+
+
+def fp8_dequant_torch(w: wl.Workload):
+    """Dequantisation of the fp8 pool computed with torch's float8_e4m3fn cast of the
+    pre-clamped fp32 product (a library routine, independent of the oracle's codec)."""
+    ks = torch.from_numpy(np.asarray(w.k_scale, np.float32))
+    vs = torch.from_numpy(np.asarray(w.v_scale, np.float32))
+
+    def q8(x64: np.ndarray, scale: torch.Tensor) -> np.ndarray:
+        x = torch.from_numpy(x64).to(torch.float32)  # exact: values are bf16
+        inv = (1.0 / scale).to(torch.float32)  # fp32 reciprocal, as stored
+        y = (x * inv[None, :, None]).clamp(-448.0, 448.0)
+        code = y.to(torch.float8_e4m3fn)
+        return (code.to(torch.float64) * scale.to(torch.float64)[None, :, None]).numpy()
+
+    return lambda k, v: (q8(k, ks), q8(v, vs))
