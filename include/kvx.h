@@ -1,0 +1,206 @@
+/*
+ * kvx.h -- prefix-extend attention over a paged KV pool on AMD MI355X (gfx950).
+ *
+ * The operation.  An agent that returns for another turn reuses the KV tensors
+ * its cached prefix still holds and computes only the uncached suffix (paper,
+ * Section 1 and Section 2, "Prefix caching for multi-turn agents"): prefill
+ * materialises the suffix's K/V in the attention layer, and every suffix query
+ * attends causally over the cached prefix and the suffix before it.  The number
+ * of uncached tokens of a request is its prompt length minus its cached prefix
+ * length (Section 4, metrics).  The host keeps the prefix index and the eviction
+ * policy (Section 3.2, Algorithm 1); what reaches this library is, per request,
+ * a prefix length P, an extend length E and a page table.
+ *
+ * Conventions shared by every call
+ *   - Return value: KVX_OK (0) or a kvx_status code; kvx_last_error() then
+ *     describes the failure (thread-local string).  No exception crosses the ABI.
+ *   - Argument checks run synchronously on the host before anything is queued;
+ *     a call that fails them queues no work and leaves all buffers untouched.
+ *   - Device work is queued on `stream` (a hipStream_t; NULL = the null stream)
+ *     and is asynchronous: caller-owned buffers must stay alive until the
+ *     stream reaches the call.  Calls on one stream execute in order.
+ *   - "host" pointers are ordinary CPU memory read during the call;
+ *     "device" pointers are GPU memory (hipMalloc / torch CUDA tensors).
+ *   - bf16 means IEEE binary32 truncated to its upper 16 bits (2 bytes).
+ *   - Rows of Q, O, K_ext and V_ext are the suffix tokens of all requests,
+ *     request by request: request r owns rows [sum_{s<r} E_s, sum_{s<=r} E_s).
+ *   - Page ids outside [0, num_pages) are undefined behaviour unless the
+ *     environment variable KVX_VALIDATE=1 is set, in which case the page table
+ *     is copied to the host and checked (KVX_ERANGE), at the cost of a sync.
+ */
+#ifndef KVX_H
+#define KVX_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct kvx_pool kvx_pool; /* opaque; owned by the library */
+typedef void *kvx_stream_t;       /* a hipStream_t */
+
+enum kvx_status {
+    KVX_OK = 0,
+    KVX_EINVAL = 1,       /* bad argument (shape, length, null pointer, ...) */
+    KVX_ENOMEM = 2,       /* device or host allocation failed */
+    KVX_ERANGE = 3,       /* page id outside the pool (KVX_VALIDATE=1 only) */
+    KVX_EUNSUPPORTED = 4, /* valid but unsupported configuration */
+    KVX_EHIP = 5          /* a HIP runtime call failed */
+};
+
+enum kvx_kv_dtype {
+    KVX_KV_BF16 = 0,     /* K/V stored as bf16 */
+    KVX_KV_FP8_E4M3 = 1  /* K/V stored as OCP e4m3 (fp8, max 448, no inf) with per-head scales */
+};
+
+/* ------------------------------------------------------------------ the pool */
+
+/* Device layout of a pool, for tests and tools.  Element strides.  K is stored
+ * [page][kv_head][slot][dim]; V is stored transposed within a page,
+ * [page][kv_head][dim][slot], so that one page of one head is a contiguous
+ * block in both (4 KiB for bf16, head_dim 128). */
+typedef struct {
+    void *k_base;          /* device */
+    void *v_base;          /* device */
+    int64_t num_pages;
+    int32_t page_size;
+    int32_t num_kv_heads;
+    int32_t head_dim;
+    int32_t kv_dtype;      /* enum kvx_kv_dtype */
+    int32_t elem_bytes;    /* 2 (bf16) or 1 (fp8) */
+    int32_t reserved;
+    int64_t k_stride_page, k_stride_head, k_stride_slot, k_stride_dim;
+    int64_t v_stride_page, v_stride_head, v_stride_slot, v_stride_dim;
+    const float *k_scale;  /* device [num_kv_heads], NULL for bf16 */
+    const float *v_scale;  /* device [num_kv_heads], NULL for bf16 */
+} kvx_pool_layout;
+
+/*
+ * Allocate a KV pool of `num_pages` pages of `page_size` tokens (the shared
+ * cache pool of fixed-size pages, Section 2, "Modern serving systems manage
+ * reusable KV tensors in a shared cache pool").
+ *   page_size     must be 16.
+ *   num_kv_heads  >= 1.
+ *   head_dim      64 or 128.
+ *   kv_dtype      KVX_KV_BF16 or KVX_KV_FP8_E4M3.
+ *   k_scale, v_scale  host [num_kv_heads] positive finite dequantisation scales
+ *                 for the fp8 pool (stored value = code * scale); NULL for bf16.
+ *   out           receives the handle.
+ * The pool's contents are zero after creation.  Synchronous.  Errors: EINVAL,
+ * EUNSUPPORTED (page_size != 16, head_dim not 64/128), ENOMEM, EHIP.
+ */
+int kv_pool_create(int64_t num_pages, int32_t page_size, int32_t num_kv_heads, int32_t head_dim,
+                   int32_t kv_dtype, const float *k_scale, const float *v_scale, kvx_pool **out);
+
+/* Free a pool (waits for the device to go idle first).  NULL is a no-op. */
+int kv_pool_destroy(kvx_pool *pool);
+
+/* Fill *out with the pool's device layout.  Errors: EINVAL. */
+int kv_pool_layout(const kvx_pool *pool, kvx_pool_layout *out);
+
+/*
+ * Raw page upload / readback in the canonical order [n][kv_head][slot][dim]
+ * for both K and V, in the pool's element type (bf16 bits or fp8 codes); the
+ * library converts to and from its own V layout.  Neither call converts values.
+ *   page_ids   host [n] physical page ids (each in [0, num_pages); always checked)
+ *   k_*, v_*   device buffers of n * num_kv_heads * page_size * head_dim elements
+ * Asynchronous on `stream`.  Errors: EINVAL, ERANGE, ENOMEM, EHIP.
+ */
+int kv_pool_write_pages(kvx_pool *pool, const int32_t *page_ids, int64_t n, const void *k_src,
+                        const void *v_src, kvx_stream_t stream);
+int kv_pool_read_pages(const kvx_pool *pool, const int32_t *page_ids, int64_t n, void *k_dst,
+                       void *v_dst, kvx_stream_t stream);
+
+/* ---------------------------------------------------------------- the batch */
+
+/* One prefix-extend batch.  Request r has a cached prefix of P_r tokens already
+ * in the pool and an uncached suffix of E_r tokens; its logical pages
+ * j = 0 .. ceil((P_r+E_r)/16)-1 are page_ids[page_indptr[r] + j]. */
+typedef struct {
+    int32_t num_reqs;              /* R >= 0 */
+    const int32_t *prefix_lens;    /* host [R], P_r >= 0 */
+    const int32_t *extend_lens;    /* host [R], E_r >= 0 */
+    const int32_t *page_indptr;    /* host [R+1], non-decreasing, starts at 0; request r needs
+                                      page_indptr[r+1]-page_indptr[r] >= ceil((P_r+E_r)/16) */
+    const int32_t *page_ids;       /* device [page_indptr[R]] physical page ids */
+} kvx_batch;
+
+/*
+ * Write the suffix's K and V into the pool (prefill materialises KV in every
+ * attention layer, Section 2): for each request r, suffix token i and KV head h,
+ * the token at absolute position t = P_r + i goes to slot t % 16 of logical page
+ * t / 16.  bf16 pool: the bits are copied.  fp8 pool: each element is stored as
+ * e4m3(clamp(float(x) * float(1/scale_h), -448, 448)), rounded to nearest even.
+ * Slots not written by the batch keep their contents.
+ *   k_ext, v_ext  device bf16 [T, num_kv_heads, head_dim], T = sum E_r.
+ * Must precede extend_attention of the same batch on the same stream.
+ * Errors: EINVAL, ERANGE (validation mode), ENOMEM, EHIP.  R = 0 or T = 0: no-op.
+ */
+int store_kv(kvx_pool *pool, const kvx_batch *batch, const void *k_ext, const void *v_ext,
+             kvx_stream_t stream);
+
+/*
+ * Prefix-extend attention: for each request r, suffix row i and query head hq,
+ *   o = softmax_j(sm_scale * q . k_j) v_j  over keys j = 0 .. P_r + i
+ * of the request's logical sequence in the pool (cached prefix, then the suffix
+ * written by store_kv).  Query head hq reads KV head hq / (num_q_heads / num_kv_heads).
+ * The result equals attention over the whole context; only the suffix is computed
+ * (Section 1: reuse the cached prefix, compute the uncached suffix).
+ *   q            device bf16 [T, num_q_heads, head_dim]
+ *   num_q_heads  a multiple of the pool's num_kv_heads, with (num_q_heads /
+ *                num_kv_heads) dividing 128
+ *   sm_scale     softmax scale, finite and > 0 (usually 1/sqrt(head_dim))
+ *   out          device bf16 [T, num_q_heads, head_dim] (round to nearest even)
+ *   lse          device fp32 [T, num_q_heads] natural-log sum of exp of the scaled
+ *                scores, or NULL
+ * Uses a library-owned device workspace (grown with hipMalloc when a batch needs
+ * more than any earlier one).  Errors: EINVAL, EUNSUPPORTED, ERANGE (validation
+ * mode), ENOMEM, EHIP.  R = 0 or T = 0: no-op.
+ */
+int extend_attention(kvx_pool *pool, const kvx_batch *batch, const void *q, int32_t num_q_heads,
+                     float sm_scale, void *out, float *lse, kvx_stream_t stream);
+
+/* ---------------------------------------------------------- planning, tuning */
+
+/* One work item of extend_attention: a tile of suffix tokens of one request and
+ * one KV head (all of that head's query heads), over the key range [key_begin,
+ * key_end) of the request's logical sequence.  part >= 0 marks one part of a
+ * key range split across workgroups (merged afterwards by log-sum-exp). */
+typedef struct {
+    int32_t req;
+    int32_t kv_head;
+    int32_t tok_begin;   /* first suffix token of the tile */
+    int32_t tok_count;   /* suffix tokens in the tile */
+    int32_t key_begin;
+    int32_t key_end;
+    int32_t part;        /* -1: whole range; else index of the partial result */
+    int32_t xcd;         /* the XCD (L2 domain) the item is dispatched to */
+} kvx_work_item;
+
+/*
+ * The host-side work plan extend_attention would launch for a batch (host only,
+ * no device work): ragged (P, E) pairs cut into tiles, long key ranges split,
+ * items ordered longest first within each XCD.  Writes at most `cap` items to
+ * `items` (may be NULL) and the total count to *count.
+ *   num_kv_heads, num_q_heads, head_dim as for extend_attention.
+ * Errors: EINVAL, EUNSUPPORTED.
+ */
+int extend_attention_plan(const kvx_batch *batch, int32_t num_q_heads, int32_t num_kv_heads,
+                          int32_t head_dim, kvx_work_item *items, int64_t cap, int64_t *count);
+
+/*
+ * Key-range split length for extend_attention (tokens, a multiple of 64, or 0 =
+ * automatic, the default).  A non-zero value splits every key range longer
+ * than it; used to exercise the split path.  Process-wide.  Errors: EINVAL.
+ */
+int kvx_set_split_keys(int32_t keys);
+
+/* Message describing the last non-OK status on this thread ("" if none). */
+const char *kvx_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVX_H */

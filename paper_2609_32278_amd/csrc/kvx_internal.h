@@ -1,0 +1,107 @@
+// Internal declarations shared by the host code and the HIP kernels of libkvx.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "kvx.h"
+
+namespace kvx {
+
+constexpr int kPageSize = 16;
+constexpr int kTileRows = 128;  // query rows (token x query head of one KV head) per attention workgroup
+constexpr int kTileKeys = 64;   // keys per K/V tile staged in LDS
+constexpr int kAttnThreads = 256;
+constexpr int kNumXcd = 8;      // L2 domains of an MI355X; workgroup i runs on XCD i % 8
+
+// One attention workgroup: a tile of suffix tokens of one request and one KV head,
+// over keys [key_begin, key_end) of the request's logical sequence.
+struct AttnUnit {
+  int32_t qo_row0;    // global suffix row of the tile's first token
+  int32_t q_pos0;     // absolute position of that token (P + tok_begin)
+  int32_t page_base;  // offset of the request's page list in page_ids
+  int32_t key_begin;  // multiple of kTileKeys
+  int32_t key_end;    // exclusive; key_end <= key_begin marks a padding entry
+  int32_t head_ntok;  // (kv_head << 16) | tokens in the tile
+  int32_t part;       // -1: final result; else index of this part's partial result
+  int32_t req;
+};
+static_assert(sizeof(AttnUnit) == 32, "AttnUnit is 32 bytes");
+
+// Log-sum-exp merge of the parts of one split tile.
+struct MergeUnit {
+  int32_t qo_row0;
+  int32_t head_ntok;
+  int32_t part0;
+  int32_t nparts;
+};
+
+// One KV-store workgroup: the suffix slots [slot_begin, slot_end) of one page.
+struct StoreUnit {
+  int32_t row_slot0;  // suffix row that slot 0 of the page would hold (may be negative)
+  int32_t page_pos;   // index into page_ids
+  int32_t slot_begin;
+  int32_t slot_end;
+};
+
+struct AttnParams {
+  const uint16_t* q;      // bf16 [T, Hq, D]
+  uint16_t* out;          // bf16 [T, Hq, D]
+  float* lse;             // fp32 [T, Hq] or null
+  const void* k_pool;
+  const void* v_pool;
+  const int32_t* page_ids;
+  const AttnUnit* units;
+  float* o_part;          // fp32 [parts, kTileRows, D]
+  float* lse_part;        // fp32 [parts, kTileRows]
+  const float* k_scale;   // fp8 pool: device [Hkv]
+  const float* v_scale;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t group;          // Hq / Hkv
+  int32_t tile_tok;       // tokens per tile = kTileRows / group
+  float scale_log2;       // sm_scale * log2(e)
+};
+
+struct MergeParams {
+  const MergeUnit* merges;
+  const float* o_part;
+  const float* lse_part;
+  uint16_t* out;
+  float* lse;
+  int32_t num_q_heads;
+  int32_t group;
+};
+
+struct StoreParams {
+  const uint16_t* k_ext;  // bf16 [T, Hkv, D]
+  const uint16_t* v_ext;
+  void* k_pool;
+  void* v_pool;
+  const int32_t* page_ids;
+  const StoreUnit* units;
+  const float* k_inv_scale;  // fp8 pool: device [Hkv], fp32 1/scale
+  const float* v_inv_scale;
+  int32_t num_kv_heads;
+};
+
+struct PageIoParams {
+  const int32_t* page_ids;  // device [n]
+  void* k_pool;
+  void* v_pool;
+  void* k_lin;              // canonical [n][Hkv][16][D] buffers
+  void* v_lin;
+  int32_t num_kv_heads;
+  int32_t to_pool;          // 1: write pages into the pool, 0: read them out
+};
+
+hipError_t launch_extend_attention(const AttnParams& p, int64_t n_units, int head_dim, bool fp8,
+                                   hipStream_t stream);
+hipError_t launch_merge(const MergeParams& p, int64_t n_merges, int head_dim, hipStream_t stream);
+hipError_t launch_store_kv(const StoreParams& p, int64_t n_units, int head_dim, bool fp8,
+                           hipStream_t stream);
+hipError_t launch_page_io(const PageIoParams& p, int64_t n_pages, int head_dim, int elem_bytes,
+                          hipStream_t stream);
+
+}  // namespace kvx

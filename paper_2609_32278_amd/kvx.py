@@ -1,0 +1,207 @@
+"""Thin ctypes binding of libkvx (include/kvx.h): argument marshalling only.
+
+Every function keeps the C ABI's name.  Device buffers are torch CUDA tensors
+(PyTorch provides device memory and streams only; every step of the
+computation runs in libkvx's HIP kernels).  The library must have been built
+(``__graft_entry__.build()`` or ``python paper_2609_32278_amd/build.py``);
+loading raises ``KvxNotBuilt`` otherwise -- there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkvx.so")
+
+KVX_OK, KVX_EINVAL, KVX_ENOMEM, KVX_ERANGE, KVX_EUNSUPPORTED, KVX_EHIP = range(6)
+KVX_KV_BF16, KVX_KV_FP8_E4M3 = 0, 1
+STATUS_NAMES = {0: "KVX_OK", 1: "KVX_EINVAL", 2: "KVX_ENOMEM", 3: "KVX_ERANGE",
+                4: "KVX_EUNSUPPORTED", 5: "KVX_EHIP"}
+
+# Every symbol include/kvx.h declares.
+EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_layout", "kv_pool_write_pages",
+           "kv_pool_read_pages", "store_kv", "extend_attention", "extend_attention_plan",
+           "kvx_set_split_keys", "kvx_last_error"]
+
+
+class KvxNotBuilt(ImportError):
+    pass
+
+
+class KvxError(RuntimeError):
+    def __init__(self, status: int, func: str, message: str):
+        super().__init__(f"{func}: {STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class kvx_batch(ctypes.Structure):
+    _fields_ = [("num_reqs", ctypes.c_int32), ("prefix_lens", ctypes.c_void_p),
+                ("extend_lens", ctypes.c_void_p), ("page_indptr", ctypes.c_void_p),
+                ("page_ids", ctypes.c_void_p)]
+
+
+class kvx_pool_layout(ctypes.Structure):
+    _fields_ = [("k_base", ctypes.c_void_p), ("v_base", ctypes.c_void_p), ("num_pages", ctypes.c_int64),
+                ("page_size", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("kv_dtype", ctypes.c_int32), ("elem_bytes", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("k_stride_page", ctypes.c_int64), ("k_stride_head", ctypes.c_int64),
+                ("k_stride_slot", ctypes.c_int64), ("k_stride_dim", ctypes.c_int64),
+                ("v_stride_page", ctypes.c_int64), ("v_stride_head", ctypes.c_int64),
+                ("v_stride_slot", ctypes.c_int64), ("v_stride_dim", ctypes.c_int64),
+                ("k_scale", ctypes.c_void_p), ("v_scale", ctypes.c_void_p)]
+
+
+class kvx_work_item(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("req", "kv_head", "tok_begin", "tok_count", "key_begin", "key_end", "part", "xcd")]
+
+
+WORK_ITEM_DTYPE = np.dtype([(n, np.int32) for n, _ in kvx_work_item._fields_])
+
+_lib = None
+
+
+def lib():
+    """The loaded libkvx (raises KvxNotBuilt if the shared library is missing)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise KvxNotBuilt(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+        sig = {
+            "kv_pool_create": [i64, i32, i32, i32, i32, P, P, ctypes.POINTER(P)],
+            "kv_pool_destroy": [P],
+            "kv_pool_layout": [P, ctypes.POINTER(kvx_pool_layout)],
+            "kv_pool_write_pages": [P, P, i64, P, P, P],
+            "kv_pool_read_pages": [P, P, i64, P, P, P],
+            "store_kv": [P, ctypes.POINTER(kvx_batch), P, P, P],
+            "extend_attention": [P, ctypes.POINTER(kvx_batch), P, i32, f32, P, P, P],
+            "extend_attention_plan": [ctypes.POINTER(kvx_batch), i32, i32, i32, P, i64, ctypes.POINTER(i64)],
+            "kvx_set_split_keys": [i32],
+        }
+        for name, args in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_int
+        L.kvx_last_error.argtypes = []
+        L.kvx_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def kvx_last_error() -> str:
+    return lib().kvx_last_error().decode()
+
+
+def _check(status: int, func: str):
+    if status != KVX_OK:
+        raise KvxError(status, func, kvx_last_error())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        if torch.cuda.is_available() and torch.cuda.is_initialized():
+            return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        return None
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("expected a device (CUDA/HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+# ----------------------------------------------------------------------- batch
+
+class Batch:
+    """Host lengths and page_indptr plus the device page table, as a kvx_batch."""
+
+    def __init__(self, prefix_lens, extend_lens, page_indptr, page_ids_dev):
+        self.prefix_lens = np.ascontiguousarray(prefix_lens, dtype=np.int32)
+        self.extend_lens = np.ascontiguousarray(extend_lens, dtype=np.int32)
+        self.page_indptr = np.ascontiguousarray(page_indptr, dtype=np.int32)
+        self.page_ids = page_ids_dev  # device int32 tensor (or an int address)
+        self.c = kvx_batch(len(self.prefix_lens), self.prefix_lens.ctypes.data,
+                           self.extend_lens.ctypes.data, self.page_indptr.ctypes.data,
+                           _dptr(page_ids_dev) if page_ids_dev is not None else None)
+
+    @property
+    def total_extend(self) -> int:
+        return int(self.extend_lens.astype(np.int64).sum())
+
+
+# ------------------------------------------------------------------------ pool
+
+def kv_pool_create(num_pages: int, page_size: int, num_kv_heads: int, head_dim: int,
+                   kv_dtype: int = KVX_KV_BF16, k_scale=None, v_scale=None) -> ctypes.c_void_p:
+    ks = None if k_scale is None else np.ascontiguousarray(k_scale, dtype=np.float32)
+    vs = None if v_scale is None else np.ascontiguousarray(v_scale, dtype=np.float32)
+    out = ctypes.c_void_p()
+    _check(lib().kv_pool_create(int(num_pages), int(page_size), int(num_kv_heads), int(head_dim), int(kv_dtype),
+                                None if ks is None else ks.ctypes.data, None if vs is None else vs.ctypes.data,
+                                ctypes.byref(out)), "kv_pool_create")
+    return out
+
+
+def kv_pool_destroy(pool) -> None:
+    _check(lib().kv_pool_destroy(pool), "kv_pool_destroy")
+
+
+def kv_pool_layout(pool) -> dict:
+    lay = kvx_pool_layout()
+    _check(lib().kv_pool_layout(pool, ctypes.byref(lay)), "kv_pool_layout")
+    return {name: getattr(lay, name) for name, _ in kvx_pool_layout._fields_}
+
+
+def kv_pool_write_pages(pool, page_ids, k_src, v_src, stream=None) -> None:
+    ids = np.ascontiguousarray(page_ids, dtype=np.int32)
+    _check(lib().kv_pool_write_pages(pool, ids.ctypes.data, ids.size, _dptr(k_src), _dptr(v_src), _stream(stream)),
+           "kv_pool_write_pages")
+
+
+def kv_pool_read_pages(pool, page_ids, k_dst, v_dst, stream=None) -> None:
+    ids = np.ascontiguousarray(page_ids, dtype=np.int32)
+    _check(lib().kv_pool_read_pages(pool, ids.ctypes.data, ids.size, _dptr(k_dst), _dptr(v_dst), _stream(stream)),
+           "kv_pool_read_pages")
+
+
+# ----------------------------------------------------------------- hot path
+
+def store_kv(pool, batch: Batch, k_ext, v_ext, stream=None) -> None:
+    _check(lib().store_kv(pool, ctypes.byref(batch.c), _dptr(k_ext), _dptr(v_ext), _stream(stream)), "store_kv")
+
+
+def extend_attention(pool, batch: Batch, q, num_q_heads: int, sm_scale: float, out, lse=None, stream=None) -> None:
+    _check(lib().extend_attention(pool, ctypes.byref(batch.c), _dptr(q), int(num_q_heads), float(sm_scale),
+                                  _dptr(out), _dptr(lse), _stream(stream)), "extend_attention")
+
+
+def extend_attention_plan(batch: Batch, num_q_heads: int, num_kv_heads: int, head_dim: int) -> np.ndarray:
+    count = ctypes.c_int64()
+    _check(lib().extend_attention_plan(ctypes.byref(batch.c), num_q_heads, num_kv_heads, head_dim, None, 0,
+                                       ctypes.byref(count)), "extend_attention_plan")
+    items = np.zeros(count.value, dtype=WORK_ITEM_DTYPE)
+    _check(lib().extend_attention_plan(ctypes.byref(batch.c), num_q_heads, num_kv_heads, head_dim,
+                                       items.ctypes.data, count.value, ctypes.byref(count)),
+           "extend_attention_plan")
+    return items
+
+
+def kvx_set_split_keys(keys: int) -> None:
+    _check(lib().kvx_set_split_keys(int(keys)), "kvx_set_split_keys")

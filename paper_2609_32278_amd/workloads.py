@@ -70,6 +70,11 @@ class Workload:
     sigma: float = 1.0                # std of K and V values
     q_sigma: float = 1.0              # std of Q values
     page_size: int = PAGE_SIZE
+    orig_req: Optional[np.ndarray] = None  # request ids in the batch a subset was taken from
+
+    def value_id(self, r: int) -> int:
+        """The request id that seeds request r's values (stable under ``subset``)."""
+        return int(r if self.orig_req is None else self.orig_req[r])
 
     @property
     def num_reqs(self) -> int:
@@ -124,7 +129,8 @@ class Workload:
             num_pages = max(1, len(ids))
         return dataclasses.replace(
             self, prefix_lens=self.prefix_lens[reqs].copy(), extend_lens=self.extend_lens[reqs].copy(),
-            page_indptr=indptr, page_ids=ids, num_pages=num_pages)
+            page_indptr=indptr, page_ids=ids, num_pages=num_pages,
+            orig_req=np.array([self.value_id(r) for r in reqs], dtype=np.int64))
 
 
 def _pages_needed(prefix_lens: np.ndarray, extend_lens: np.ndarray, page_size: int) -> np.ndarray:
@@ -262,15 +268,15 @@ def request_q(w: Workload, r: int, device="cpu") -> torch.Tensor:
     """Q rows of request r's uncached suffix: bf16 [E_r, Hq, d]."""
     e = int(w.extend_lens[r])
     return _randn_bf16((e, w.num_q_heads, w.head_dim), w.q_sigma,
-                       _torch_seed(w.config_id, 1, w.seed, 0, r), device)
+                       _torch_seed(w.config_id, 1, w.seed, 0, w.value_id(r)), device)
 
 
 def request_kv(w: Workload, r: int, device="cpu"):
     """The logical K and V sequences of request r (cached prefix then suffix): bf16 [L_r, Hkv, d]."""
     n = int(w.prefix_lens[r]) + int(w.extend_lens[r])
     shape = (n, w.num_kv_heads, w.head_dim)
-    k = _randn_bf16(shape, w.sigma, _torch_seed(w.config_id, 1, w.seed, 1, r), device)
-    v = _randn_bf16(shape, w.sigma, _torch_seed(w.config_id, 1, w.seed, 2, r), device)
+    k = _randn_bf16(shape, w.sigma, _torch_seed(w.config_id, 1, w.seed, 1, w.value_id(r)), device)
+    v = _randn_bf16(shape, w.sigma, _torch_seed(w.config_id, 1, w.seed, 2, w.value_id(r)), device)
     return k, v
 
 

@@ -1,0 +1,148 @@
+"""GPU-side test harness: runs a generated workload through libkvx and checks it
+against the CPU oracle on the same seeded inputs.
+
+Values are generated on the GPU by the workload generator (torch's device RNG),
+copied to the host for the oracle, and never taken from the HIP path.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+from helpers import oracle_pool_for
+from paper_2609_32278_amd import kvx
+from paper_2609_32278_amd import workloads as wl
+
+DEV = "cuda"
+
+# parity gate on bf16 outputs, and a scale-free companion gate
+MAX_ABS, MEAN_ABS = 2e-2, 2e-3
+REL_RMS = 1e-2
+
+
+def fresh_batch(w: wl.Workload, page_ids: np.ndarray, prefix_lens, extend_lens, indptr):
+    ids_d = torch.from_numpy(np.ascontiguousarray(page_ids, np.int32)).to(DEV)
+    return kvx.Batch(prefix_lens, extend_lens, indptr, ids_d), ids_d
+
+
+class GpuRun:
+    """Pool + batch of one workload on the GPU; the cached prefixes are written by
+    store_kv of the history turn, request by request."""
+
+    def __init__(self, w: wl.Workload, fill_bits: int | None = None, overrides=None):
+        self.w = w
+        self.pool = kvx.kv_pool_create(w.num_pages, w.page_size, w.num_kv_heads, w.head_dim, w.kv_dtype,
+                                       w.k_scale, w.v_scale)
+        if fill_bits is not None:
+            self.fill_pool(fill_bits)
+        self.batch, self._ids = fresh_batch(w, w.page_ids, w.prefix_lens, w.extend_lens, w.page_indptr)
+        overrides = overrides or {}
+        qs, ke, ve = [], [], []
+        for r in range(w.num_reqs):
+            p = int(w.prefix_lens[r])
+            if "kv" in overrides:
+                k, v = overrides["kv"](r)
+            else:
+                k, v = wl.request_kv(w, r, DEV)
+            q = overrides["q"](r) if "q" in overrides else wl.request_q(w, r, DEV)
+            if p > 0:
+                n = (p + w.page_size - 1) // w.page_size
+                hb, ids = fresh_batch(w, w.pages_of(r)[:n], [0], [p], [0, n])
+                kvx.store_kv(self.pool, hb, k[:p].contiguous(), v[:p].contiguous())
+                torch.cuda.synchronize()
+                del ids
+            qs.append(q)
+            ke.append(k[p:])
+            ve.append(v[p:])
+        self.q = torch.cat(qs).contiguous()
+        self.k_ext = torch.cat(ke).contiguous()
+        self.v_ext = torch.cat(ve).contiguous()
+        self.qo = w.qo_indptr.astype(np.int64)
+
+    def fill_pool(self, bits: int, chunk: int = 4096):
+        w = self.w
+        dt = torch.int16 if w.kv_dtype == wl.KV_BF16 else torch.uint8
+        val = bits if w.kv_dtype != wl.KV_BF16 else (bits - 65536 if bits >= 32768 else bits)
+        for p0 in range(0, w.num_pages, chunk):
+            ids = np.arange(p0, min(w.num_pages, p0 + chunk), dtype=np.int32)
+            buf = torch.full((len(ids), w.num_kv_heads, w.page_size, w.head_dim), val, dtype=dt, device=DEV)
+            kvx.kv_pool_write_pages(self.pool, ids, buf, buf)
+        torch.cuda.synchronize()
+
+    def store(self):
+        kvx.store_kv(self.pool, self.batch, self.k_ext, self.v_ext)
+
+    def attend(self, want_lse=False):
+        w = self.w
+        out = torch.full((w.total_extend, w.num_q_heads, w.head_dim), float("nan"), dtype=torch.bfloat16,
+                         device=DEV)
+        lse = None
+        if want_lse:
+            lse = torch.full((w.total_extend, w.num_q_heads), float("nan"), dtype=torch.float32, device=DEV)
+        kvx.extend_attention(self.pool, self.batch, self.q, w.num_q_heads, w.sm_scale, out, lse)
+        torch.cuda.synchronize()
+        return (out, lse) if want_lse else out
+
+    def read_pages(self, page_ids):
+        w = self.w
+        dt = torch.int16 if w.kv_dtype == wl.KV_BF16 else torch.uint8
+        n = len(page_ids)
+        k = torch.empty((n, w.num_kv_heads, w.page_size, w.head_dim), dtype=dt, device=DEV)
+        v = torch.empty_like(k)
+        kvx.kv_pool_read_pages(self.pool, np.asarray(page_ids, np.int32), k, v)
+        torch.cuda.synchronize()
+        npdt = np.uint16 if w.kv_dtype == wl.KV_BF16 else np.uint8
+        return k.cpu().numpy().view(npdt), v.cpu().numpy().view(npdt)
+
+    def close(self):
+        if self.pool is not None:
+            kvx.kv_pool_destroy(self.pool)
+            self.pool = None
+
+
+def oracle_rows(w: wl.Workload, q_dev: torch.Tensor, rows: np.ndarray | None, fill=None, want_lse=False,
+                kv_override=None):
+    """Oracle outputs of the listed rows ((r, i) pairs; None = every row), built from
+    the generator's values for just the requests involved (compact pool)."""
+    if rows is None:
+        rr, rp = oracle.all_rows(w.extend_lens)
+        rows = np.stack([rr, rp], 1)
+    reqs = sorted(set(int(r) for r in rows[:, 0]))
+    sub = w.subset(reqs)
+    remap = {r: k for k, r in enumerate(reqs)}
+    t = {"q": [], "k_ext": [], "v_ext": [], "k_hist": [], "v_hist": []}
+    for k_i, r in enumerate(reqs):
+        if kv_override is not None:
+            kk, vv = kv_override(r)
+        else:
+            kk, vv = wl.request_kv(w, r, DEV)
+        p = int(w.prefix_lens[r])
+        t["k_hist"].append(kk[:p].cpu())
+        t["v_hist"].append(vv[:p].cpu())
+        t["k_ext"].append(kk[p:].cpu())
+        t["v_ext"].append(vv[p:].cpu())
+    t = {k: torch.cat(v) if v else None for k, v in t.items() if k != "q"}
+    pool = oracle_pool_for(sub, t, fill=fill)
+    qo = w.qo_indptr.astype(np.int64)
+    gidx = np.array([qo[r] + i for r, i in rows], dtype=np.int64)
+    q_rows = q_dev[torch.from_numpy(gidx).to(q_dev.device)].cpu()
+    rr = np.array([remap[int(r)] for r in rows[:, 0]], np.int32)
+    res = oracle.extend_attention(pool, sub.prefix_lens, sub.extend_lens, sub.page_indptr, sub.page_ids, q_rows,
+                                  rr, rows[:, 1].astype(np.int32), w.num_q_heads, w.sm_scale, want_lse=want_lse)
+    return res, gidx
+
+
+def compare(gpu_rows: np.ndarray, ref: np.ndarray, tag: str = ""):
+    """Parity gate on bf16 outputs: max |err| <= 2e-2, mean |err| <= 2e-3, plus
+    rms(err)/rms(ref) <= 1e-2."""
+    assert np.isfinite(gpu_rows).all(), f"{tag}: non-finite outputs"
+    err = np.abs(gpu_rows - ref)
+    mx, mean = float(err.max()), float(err.mean())
+    rel = float(np.sqrt((err ** 2).mean()) / max(np.sqrt((ref ** 2).mean()), 1e-30))
+    print(f"[parity] {tag}: max {mx:.3e} mean {mean:.3e} rel_rms {rel:.3e}", flush=True)
+    assert mx <= MAX_ABS, f"{tag}: max abs err {mx}"
+    assert mean <= MEAN_ABS, f"{tag}: mean abs err {mean}"
+    assert rel <= REL_RMS, f"{tag}: rel rms err {rel}"
+    return mx, mean, rel

@@ -1,0 +1,145 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol, rejects
+bad arguments before touching the device, and its work plan covers every visible
+(query row, key) pair exactly once."""
+
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_32278_amd import kvx
+from paper_2609_32278_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    if not os.path.exists(kvx.LIB_PATH):
+        from paper_2609_32278_amd import build
+        build.build()
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "kvx.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:int|const char\s*\*)\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared_functions()
+    assert set(names) == set(kvx.EXPORTS), names
+    lib = kvx.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _err(fn, *a):
+    with pytest.raises(kvx.KvxError) as e:
+        fn(*a)
+    assert kvx.kvx_last_error() != ""
+    return e.value.status
+
+
+def test_pool_argument_errors():
+    assert _err(kvx.kv_pool_create, 0, 16, 2, 64) == kvx.KVX_EINVAL
+    assert _err(kvx.kv_pool_create, 10, 8, 2, 64) == kvx.KVX_EUNSUPPORTED
+    assert _err(kvx.kv_pool_create, 10, 16, 2, 96) == kvx.KVX_EUNSUPPORTED
+    assert _err(kvx.kv_pool_create, 10, 16, 0, 64) == kvx.KVX_EINVAL
+    assert _err(kvx.kv_pool_create, 10, 16, 2, 64, kvx.KVX_KV_FP8_E4M3) == kvx.KVX_EUNSUPPORTED
+    assert _err(kvx.kv_pool_create, 10, 16, 2, 64, kvx.KVX_KV_FP8_E4M3, [1.0, 0.0], [1.0, 1.0]) == kvx.KVX_EINVAL
+    assert _err(kvx.kv_pool_create, 10, 16, 2, 64, 7) == kvx.KVX_EINVAL
+    assert _err(kvx.kvx_set_split_keys, 100) == kvx.KVX_EINVAL
+    assert _err(kvx.kv_pool_layout, None) == kvx.KVX_EINVAL
+
+
+def test_hot_path_argument_errors_before_any_device_work():
+    b = kvx.Batch([16], [4], [0, 2], 0x1000)
+    assert _err(kvx.store_kv, None, b, 1, 1) == kvx.KVX_EINVAL
+    assert _err(kvx.extend_attention, None, b, 1, 4, 0.125, 1) == kvx.KVX_EINVAL
+    # plan-level checks
+    assert _err(kvx.extend_attention_plan, b, 6, 4, 128) == kvx.KVX_EINVAL      # 6 % 4 != 0
+    assert _err(kvx.extend_attention_plan, b, 4, 2, 80) == kvx.KVX_EUNSUPPORTED  # head_dim
+    assert _err(kvx.extend_attention_plan, b, 512, 2, 128) == kvx.KVX_EUNSUPPORTED
+    short = kvx.Batch([16], [17], [0, 2], 0x1000)                                # 33 tokens need 3 pages
+    assert _err(kvx.extend_attention_plan, short, 4, 2, 128) == kvx.KVX_EINVAL
+    neg = kvx.Batch([-1], [4], [0, 1], 0x1000)
+    assert _err(kvx.extend_attention_plan, neg, 4, 2, 128) == kvx.KVX_EINVAL
+    bad0 = kvx.Batch([0], [4], [1, 2], 0x1000)
+    assert _err(kvx.extend_attention_plan, bad0, 4, 2, 128) == kvx.KVX_EINVAL
+
+
+def _check_plan(w, split=0):
+    kvx.kvx_set_split_keys(split)
+    try:
+        b = kvx.Batch(w.prefix_lens, w.extend_lens, w.page_indptr, 0)
+        items = kvx.extend_attention_plan(b, w.num_q_heads, w.num_kv_heads, w.head_dim)
+    finally:
+        kvx.kvx_set_split_keys(0)
+    g = w.group
+    tile_tok = 128 // g
+    real = items[items["req"] >= 0]
+    # dispatch position i runs on XCD i % 8
+    assert (items["xcd"] == np.arange(len(items)) % 8).all()
+    # every (request, kv head, suffix token) covered by exactly one tile; every tile's
+    # key range [0, P + last token] partitioned by its parts at multiples of 64
+    seen = {}
+    parts = set()
+    for it in real:
+        key = (int(it["req"]), int(it["kv_head"]), int(it["tok_begin"]))
+        seen.setdefault(key, []).append((int(it["key_begin"]), int(it["key_end"]), int(it["part"]),
+                                         int(it["tok_count"])))
+        if it["part"] >= 0:
+            assert it["part"] not in parts
+            parts.add(int(it["part"]))
+    if parts:
+        assert parts == set(range(len(parts)))
+    for r in range(w.num_reqs):
+        P, E = int(w.prefix_lens[r]), int(w.extend_lens[r])
+        for h in range(w.num_kv_heads):
+            covered = np.zeros(E, np.int32)
+            for t0 in range(0, E, tile_tok):
+                rng = sorted(seen.pop((r, h, t0)))
+                ntok = min(tile_tok, E - t0)
+                assert all(x[3] == ntok for x in rng)
+                covered[t0:t0 + ntok] += 1
+                assert rng[0][0] == 0 and rng[-1][1] == P + t0 + ntok
+                for (a, b_, pa, _), (c, _, pc, _) in zip(rng, rng[1:]):
+                    assert b_ == c and b_ % 64 == 0
+                    assert b_ <= P + t0  # earlier parts hold keys every row of the tile sees
+                assert (len(rng) == 1) == (rng[0][2] == -1)
+            assert (covered == 1).all()
+    assert not seen
+    # longest first within an XCD, by request then by tile
+    return items
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b", "tail_outlier", "rr_partial", "wide70b"])
+def test_plan_covers_every_visible_pair_once(name):
+    _check_plan(wl.make_workload(name))
+
+
+@pytest.mark.parametrize("split", [64, 1024])
+def test_plan_with_forced_splits(split):
+    w = wl.make_custom([3000, 129, 0, 77], [70, 200, 300, 1], 12, 2, 128)
+    items = _check_plan(w, split)
+    assert (items["part"] >= 0).any()
+
+
+def test_plan_splits_decode_like_batches_automatically():
+    w = wl.make_custom([32768], [64], 32, 8, 128)
+    items = _check_plan(w)
+    real = items[items["req"] >= 0]
+    assert len(real) >= 256 and (real["part"] >= 0).all()
+
+
+def test_plan_balances_xcds_for_eight_kv_heads():
+    w = wl.make_workload("rr_partial")
+    b = kvx.Batch(w.prefix_lens, w.extend_lens, w.page_indptr, 0)
+    items = kvx.extend_attention_plan(b, w.num_q_heads, w.num_kv_heads, w.head_dim)
+    real = items[items["req"] >= 0]
+    assert (real["xcd"] == real["kv_head"] % 8).all()
+    cost = np.zeros(8)
+    np.add.at(cost, real["xcd"], (real["key_end"] - real["key_begin"]).astype(np.float64))
+    assert cost.max() / cost.min() < 1.0001

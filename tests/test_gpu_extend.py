@@ -1,0 +1,226 @@
+"""extend_attention on the GPU against the CPU oracle: small cases run in full
+(several tiles and ragged tails), plus the invariances prefix reuse relies on."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_harness import DEV, GpuRun, compare, oracle_rows
+from paper_2609_32278_amd import kvx
+from paper_2609_32278_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def _run_and_compare(w, tag, want_lse=False, fill=None):
+    print(f"[extend] {tag}: R={w.num_reqs} T={w.total_extend} Hq={w.num_q_heads} Hkv={w.num_kv_heads} "
+          f"d={w.head_dim} fp8={w.kv_dtype}", flush=True)
+    run = GpuRun(w, fill_bits=fill)
+    try:
+        run.store()
+        res = run.attend(want_lse=want_lse)
+        out, lse = (res if want_lse else (res, None))
+        ref, gidx = oracle_rows(w, run.q, None, want_lse=want_lse)
+        if want_lse:
+            ref, ref_lse = ref
+        got = _f64(out)[gidx]
+        compare(got, ref, tag)
+        if want_lse:
+            lerr = np.abs(lse.cpu().numpy()[gidx] - ref_lse).max()
+            print(f"[parity] {tag}: lse max err {lerr:.3e}", flush=True)
+            assert lerr <= 2e-3 * max(1.0, float(np.abs(ref_lse).max()))
+        return out
+    finally:
+        run.close()
+
+
+def test_tiny_config_every_row():
+    _run_and_compare(wl.make_workload("tiny"), "tiny", want_lse=True)
+
+
+CASES = {
+    # unaligned prefixes, an empty suffix, single-token suffixes, ragged tails
+    "ragged_g4_d128": ([0, 5, 16, 37, 100, 3, 1000], [7, 0, 1, 29, 18, 40, 200], 8, 2, 128, wl.KV_BF16),
+    "g1_d64": ([0, 64, 129], [130, 17, 64], 4, 4, 64, wl.KV_BF16),
+    "g6_d128": ([33, 0], [45, 70], 12, 2, 128, wl.KV_BF16),
+    "g16_d64": ([80, 1], [19, 33], 32, 2, 64, wl.KV_BF16),
+    "g8_fp8_d128": ([300, 16, 0], [57, 129, 40], 16, 2, 128, wl.KV_FP8_E4M3),
+    "g2_fp8_d64": ([7, 200], [99, 3], 4, 2, 64, wl.KV_FP8_E4M3),
+    "decode_like": ([5000, 3001, 64], [1, 1, 1], 8, 1, 128, wl.KV_BF16),
+    "long_causal": ([0], [1000], 4, 1, 128, wl.KV_BF16),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_edge_cases_every_row(name):
+    p, e, hq, hkv, d, dt = CASES[name]
+    w = wl.make_custom(p, e, hq, hkv, d, kv_dtype=dt, seed=len(name))
+    _run_and_compare(w, name, want_lse=True)
+
+
+def test_sharpened_queries():
+    w = wl.make_custom([40, 300, 0], [90, 33, 77], 8, 2, 128, q_sigma=4.0, seed=9)
+    _run_and_compare(w, "sharpened")
+
+
+@pytest.mark.parametrize("split", [64, 128, 1024])
+def test_forced_key_split_matches_oracle(split):
+    w = wl.make_custom([3000, 129, 0], [70, 200, 300], 8, 2, 128, seed=10)
+    kvx.kvx_set_split_keys(split)
+    try:
+        _run_and_compare(w, f"split{split}", want_lse=True)
+    finally:
+        kvx.kvx_set_split_keys(0)
+
+
+def test_single_key_returns_value_bits():
+    for dt in (wl.KV_BF16, wl.KV_FP8_E4M3):
+        w = wl.make_custom([0], [1], 4, 2, 128, kv_dtype=dt, seed=2)
+        print(f"[extend] single key fp8={dt}", flush=True)
+        run = GpuRun(w)
+        try:
+            run.store()
+            out = run.attend().cpu()
+            v0 = run.v_ext[0].cpu()  # [Hkv, d]
+            if dt == wl.KV_FP8_E4M3:
+                s = torch.from_numpy(w.v_scale)
+                code = (v0.float() * (1.0 / s)[:, None]).clamp(-448, 448).to(torch.float8_e4m3fn)
+                v0 = (code.float() * s[:, None]).to(torch.bfloat16)
+            expect = v0.repeat_interleave(2, dim=0)
+            assert torch.equal(out[0].view(torch.int16), expect.view(torch.int16))
+        finally:
+            run.close()
+
+
+def test_page_permutation_gives_bitwise_identical_outputs():
+    outs = []
+    for seed in (1, 2, 3):
+        w = wl.make_custom([300, 17, 64], [100, 60, 5], 8, 2, 128, seed=seed, num_pages=128)
+        w.seed = 0  # same values, different placement
+        print(f"[extend] placement {seed}", flush=True)
+        run = GpuRun(w)
+        try:
+            run.store()
+            outs.append(run.attend().cpu())
+        finally:
+            run.close()
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+    assert torch.equal(outs[0].view(torch.int16), outs[2].view(torch.int16))
+
+
+def test_poisoned_unused_slots_do_not_change_outputs():
+    outs = []
+    for fill in (0x0000, 0x7FC0, 0x461C):  # zero, NaN, ~1e4
+        w = wl.make_custom([21, 130], [30, 9], 4, 1, 128, seed=6, num_pages=40)
+        print(f"[extend] poison {fill:#x}", flush=True)
+        run = GpuRun(w, fill_bits=fill)
+        try:
+            run.store()
+            outs.append(run.attend().cpu())
+        finally:
+            run.close()
+    assert not torch.isnan(outs[1].float()).any()
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+    assert torch.equal(outs[0].view(torch.int16), outs[2].view(torch.int16))
+
+
+def test_constant_values_give_the_constant():
+    c = 0.71875
+    w = wl.make_custom([100, 0], [40, 300], 8, 2, 128, seed=7)
+    shapes = {r: (int(w.prefix_lens[r] + w.extend_lens[r]), 2, 128) for r in range(w.num_reqs)}
+    run = GpuRun(w, overrides={"kv": lambda r: (wl.request_kv(w, r, DEV)[0],
+                                                  torch.full(shapes[r], c, dtype=torch.bfloat16, device=DEV))})
+    try:
+        run.store()
+        out = run.attend().float().cpu()
+        assert (out - c).abs().max().item() <= c * 2.0 ** -7
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("where", ["prefix", "page_boundary", "diagonal"])
+def test_needle_key_dominates(where):
+    P, E, d = 200, 50, 128
+    w = wl.make_custom([P], [E], 4, 1, d, seed=12, sigma=0.05)
+    i = E - 1
+    j = {"prefix": 7, "page_boundary": 192, "diagonal": P + i}[where]
+    q = wl.request_q(w, 0, DEV)
+    k, v = wl.request_kv(w, 0, DEV)
+    qv = q[i, 0].double()
+    needle = (qv * (60.0 * math.sqrt(d) / float(qv.norm()) ** 2)).to(torch.bfloat16)
+    k = k.clone()
+    v = v.clone()
+    k[j, 0] = needle
+    v[j, 0] = 3.0
+    run = GpuRun(w, overrides={"kv": lambda r: (k, v), "q": lambda r: q})
+    try:
+        run.store()
+        out = run.attend().float().cpu()
+        # query head 0 sees the needle with a logit margin of ~60: output = V_j
+        assert (out[i, 0] - 3.0).abs().max().item() <= 3.0 * 2.0 ** -7
+    finally:
+        run.close()
+
+
+def test_split_invariance_across_page_boundaries():
+    """One logical sequence, cut into cached prefix + suffix at several page
+    boundaries: the rows past the last cut agree with each other within the gate."""
+    total, hq, hkv, d = 700, 8, 2, 128
+    base = wl.make_custom([0], [total], hq, hkv, d, seed=13)
+    q_all = wl.request_q(base, 0, DEV)
+    k_all, v_all = wl.request_kv(base, 0, DEV)
+    cuts = [0, 16, 320, 640]
+    rows = []
+    for cut in cuts:
+        w = wl.make_custom([cut], [total - cut], hq, hkv, d, seed=13 + cut)
+        print(f"[extend] cut {cut}", flush=True)
+        run = GpuRun(w, overrides={"kv": lambda r: (k_all, v_all), "q": lambda r: q_all[cut:]})
+        try:
+            run.store()
+            out = run.attend()
+            rows.append(_f64(out)[cuts[-1] - cut:])
+        finally:
+            run.close()
+    for r in rows[1:]:
+        err = np.abs(r - rows[0])
+        assert err.max() <= 2e-2 and err.mean() <= 2e-3
+
+
+def test_empty_batches_are_no_ops():
+    pool = kvx.kv_pool_create(8, 16, 2, 64)
+    try:
+        out = torch.full((4, 4, 64), 7.0, dtype=torch.bfloat16, device=DEV)
+        ids = torch.zeros(1, dtype=torch.int32, device=DEV)
+        b0 = kvx.Batch([], [], [0], ids)
+        kvx.extend_attention(pool, b0, out, 4, 0.125, out)
+        b1 = kvx.Batch([16, 3], [0, 0], [0, 1, 2], ids)
+        kvx.store_kv(pool, b1, out, out)
+        kvx.extend_attention(pool, b1, out, 4, 0.125, out)
+        torch.cuda.synchronize()
+        assert (out.float() == 7.0).all()
+    finally:
+        kvx.kv_pool_destroy(pool)
+
+
+def test_validation_mode_rejects_out_of_range_pages(monkeypatch):
+    monkeypatch.setenv("KVX_VALIDATE", "1")
+    pool = kvx.kv_pool_create(8, 16, 1, 64)
+    try:
+        ids = torch.tensor([3, 8], dtype=torch.int32, device=DEV)  # 8 is outside the pool
+        b = kvx.Batch([16], [4], [0, 2], ids)
+        x = torch.zeros((4, 1, 64), dtype=torch.bfloat16, device=DEV)
+        with pytest.raises(kvx.KvxError) as e:
+            kvx.store_kv(pool, b, x, x)
+        assert e.value.status == kvx.KVX_ERANGE
+        q = torch.zeros((4, 2, 64), dtype=torch.bfloat16, device=DEV)
+        with pytest.raises(kvx.KvxError) as e:
+            kvx.extend_attention(pool, b, q, 2, 0.125, q)
+        assert e.value.status == kvx.KVX_ERANGE
+    finally:
+        kvx.kv_pool_destroy(pool)

@@ -84,6 +84,9 @@ def test_history_batch_and_subset():
     s = w.subset([3, 1])
     assert s.prefix_lens.tolist() == [512, 64]
     assert s.page_ids.tolist() == list(range(len(s.page_ids)))
+    # a subset regenerates the same values for the same requests
+    assert torch.equal(wl.request_q(s, 0), wl.request_q(w, 3))
+    assert torch.equal(wl.request_kv(s, 1)[1], wl.request_kv(w, 1)[1])
 
 
 def test_sample_rows_cover_ends_and_page_boundaries():
