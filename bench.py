@@ -1,0 +1,277 @@
+#!/usr/bin/env python3
+"""Prefix-extend attention benchmark on one MI355X.
+
+One step = one pass of the whole hot path over one batch: the host work plan,
+store_kv of the uncached suffix's K/V into the paged pool, and extend_attention
+of the suffix over its cached prefix and itself.  Inputs are synthetic, seeded,
+and resident in HBM before the timed region; the cached prefixes were written
+into the pool by an earlier (untimed) turn.
+
+Prints one JSON line: algorithmic TFLOP/s of the step (4*d*Hq per visible causal
+(query, key) pair), its fraction of the bf16 dense MFMA peak, uncached tokens/s,
+the attention kernel's roofline entry, and the CPU oracle timed on a bounded
+sample of the same workload.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config llama8b]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6  # 256 CUs x 2.4 GHz x 4096 dense bf16 flop/clk/CU
+PEAK_HBM_GBPS = 8000.0
+
+DESCRIPTIONS = {
+    "tiny": "4 requests, P {0,64,208,512}, E {32,16,100,8}, Hq 4 / Hkv 2, d 64, page 16, bf16 K/V",
+    "llama8b": "Llama-3-8B-shaped layer: 16 returning agents, P~U[4096,32768] (page-rounded), "
+               "E~U[64,2048], Hq 32 / Hkv 8, d 128, page 16, bf16 K/V, values N(0,0.25)",
+    "tail_outlier": "1 fully evicted agent (P 0, E 131072) + 31 agents P~U[32768,98304], E~U[256,1024], "
+                    "Hq 32 / Hkv 8, d 128, page 16, bf16 K/V",
+    "rr_partial": "64 agents, context~logU[8192,196608], k~U{1..4} lost 2048-token tail chunks, "
+                  "E = 2048k + U[128,4096], Hq 32 / Hkv 8, d 128, page 16, bf16 K/V",
+    "wide70b": "70B-shaped layer: 48 requests, P~logU[16384,262144], E~U[512,8192], Hq 64 / Hkv 8, d 128, "
+               "page 16, bf16 K/V",
+    "wide70b_fp8": "70B-shaped layer: 48 requests, P~logU[16384,262144], E~U[512,8192], Hq 64 / Hkv 8, d 128, "
+                   "page 16, fp8 e4m3 K/V with per-head scales U[0.01,0.1]",
+}
+
+
+def attn_source_hash() -> str:
+    path = os.path.join(ROOT, "paper_2609_32278_amd", "csrc", "kvx_attn.hip")
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def traffic_from_profiles(config: str):
+    """HBM bytes per attention launch from the committed rocprofv3 counter summary,
+    only if it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"extend_attn_{config}_hbm_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_hash = re.search(r"kernel source sha256\[:16\]:\s*`?([0-9a-f]{16})", text)
+    m_bytes = re.search(r"HBM bytes per launch \(scaled\):\s*`?([0-9.eE+]+)", text)
+    if not (m_hash and m_bytes) or m_hash.group(1) != attn_source_hash():
+        return None
+    return float(m_bytes.group(1))
+
+
+def setup(config: str, seed: int = 0):
+    import torch
+    from paper_2609_32278_amd import kvx
+    from paper_2609_32278_amd import workloads as wl
+
+    w = wl.make_workload(config, seed)
+    dev = "cuda"
+    pool = kvx.kv_pool_create(w.num_pages, w.page_size, w.num_kv_heads, w.head_dim, w.kv_dtype, w.k_scale, w.v_scale)
+    qs, ke, ve = [], [], []
+    for r in range(w.num_reqs):
+        k, v = wl.request_kv(w, r, dev)
+        p = int(w.prefix_lens[r])
+        if p > 0:  # the earlier turn that cached this prefix
+            n = (p + w.page_size - 1) // w.page_size
+            ids = torch.from_numpy(np.ascontiguousarray(w.pages_of(r)[:n])).to(dev)
+            hb = kvx.Batch([0], [p], [0, n], ids)
+            kvx.store_kv(pool, hb, k[:p].contiguous(), v[:p].contiguous())
+            torch.cuda.synchronize()
+        qs.append(wl.request_q(w, r, dev))
+        ke.append(k[p:].clone())
+        ve.append(v[p:].clone())
+        del k, v
+    q = torch.cat(qs).contiguous()
+    k_ext = torch.cat(ke).contiguous()
+    v_ext = torch.cat(ve).contiguous()
+    del qs, ke, ve
+    ids = torch.from_numpy(w.page_ids).to(dev)
+    batch = kvx.Batch(w.prefix_lens, w.extend_lens, w.page_indptr, ids)
+    out = torch.empty_like(q)
+    torch.cuda.synchronize()
+    return dict(w=w, pool=pool, batch=batch, ids=ids, q=q, k_ext=k_ext, v_ext=v_ext, out=out)
+
+
+def run_gpu(config: str, steps: int, warmup: int):
+    import torch
+    from paper_2609_32278_amd import kvx
+
+    s = setup(config)
+    w, pool, batch = s["w"], s["pool"], s["batch"]
+    q, k_ext, v_ext, out = s["q"], s["k_ext"], s["v_ext"], s["out"]
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        kvx.store_kv(pool, batch, k_ext, v_ext)
+        if ev is not None:
+            ev[1].record()
+        kvx.extend_attention(pool, batch, q, w.num_q_heads, w.sm_scale, out)
+        if ev is not None:
+            ev[2].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    store_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    ms_step = (t1 - t0) * 1e3 / steps
+    assert torch.isfinite(out.float()).all(), "non-finite attention output"
+    kvx.kv_pool_destroy(pool)
+    return w, ms_step, store_ms, attn_ms
+
+
+def run_cpu_baseline(config: str, rows_per_req: int, max_reqs: int):
+    """The oracle as it stands, on a bounded sample of the same workload."""
+    import torch
+    import oracle
+    from paper_2609_32278_amd import workloads as wl
+
+    w = wl.make_workload(config)
+    reqs = list(range(min(w.num_reqs, max_reqs)))
+    sub = w.subset(reqs)
+    t = wl.batch_tensors(sub, device="cuda")
+    t = {k: v.cpu() for k, v in t.items()}
+    # the oracle's own pool: cached prefixes (the earlier turn), then this turn's suffix
+    pool = oracle.OraclePool(sub.num_pages, sub.num_kv_heads, sub.head_dim, sub.kv_dtype, sub.page_size,
+                             sub.k_scale, sub.v_scale)
+    h = wl.history_batch(sub)
+    oracle.store_kv(pool, h.prefix_lens, h.extend_lens, h.page_indptr, h.page_ids, t["k_hist"], t["v_hist"])
+    oracle.store_kv(pool, sub.prefix_lens, sub.extend_lens, sub.page_indptr, sub.page_ids, t["k_ext"], t["v_ext"])
+    rows = wl.sample_rows(sub, rows_per_req)
+    qo = sub.qo_indptr.astype(np.int64)
+    q_rows = t["q"][torch.from_numpy(np.array([qo[r] + i for r, i in rows], dtype=np.int64))]
+    # the host's share of cores: the affinity mask, capped by OMP_NUM_THREADS when set
+    cores = len(os.sched_getaffinity(0))
+    if os.environ.get("OMP_NUM_THREADS", "").isdigit():
+        cores = min(cores, int(os.environ["OMP_NUM_THREADS"]))
+    t0 = time.perf_counter()
+    oracle.extend_attention(pool, sub.prefix_lens, sub.extend_lens, sub.page_indptr, sub.page_ids, q_rows,
+                            rows[:, 0], rows[:, 1], w.num_q_heads, w.sm_scale, num_threads=cores)
+    dt = time.perf_counter() - t0
+    used = oracle.max_threads()
+    visible = int(sum(int(sub.prefix_lens[r]) + int(i) + 1 for r, i in rows))
+    flops = 4.0 * w.head_dim * w.num_q_heads * visible
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": used,
+        "kind": "oracle",
+        "sample": f"{len(rows)} suffix rows x {w.num_q_heads} heads ({rows_per_req} per request: first, last, "
+                  f"page-boundary and seeded random rows) of the first {len(reqs)} requests; "
+                  f"{visible} visible (row, key) pairs per head, fp64, {dt:.1f} s",
+        "row_heads_per_s": len(rows) * w.num_q_heads / dt,
+        "seconds": dt,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="llama8b", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=16)
+    ap.add_argument("--cpu-reqs", type=int, default=16)
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="run only a plain 1 GiB device copy kernel (HBM counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); this build "
+              f"has no multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+
+    if args.calib_copy:
+        # a plain elementwise kernel that reads 1 GiB and writes 1 GiB, three launches
+        n = (1 << 30) // 4
+        x = torch.ones(n, dtype=torch.float32, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            torch.mul(x, 1.0, out=y)
+        torch.cuda.synchronize()
+        print(json.dumps({"calib_copy_bytes_read": 4 * n, "calib_copy_bytes_written": 4 * n, "launches": 3}))
+        return
+
+    w, ms_step, store_ms, attn_ms = run_gpu(args.config, args.steps, args.warmup)
+    flops = w.flops()
+    T = w.total_extend
+    tflops_step = flops / (ms_step * 1e-3) / 1e12
+    tflops_attn = flops / (attn_ms * 1e-3) / 1e12
+    eb = 2 if w.kv_dtype == 0 else 1
+    store_bytes = T * w.num_kv_heads * w.head_dim * 2 * (2 + eb)
+    ctx = int(w.seq_lens.sum())
+    attn_alg_bytes = (2 * T * w.num_q_heads * w.head_dim * 2 + 2 * eb * ctx * w.num_kv_heads * w.head_dim
+                      + 4 * int(np.ceil(w.seq_lens / 16).sum()))
+    traffic = traffic_from_profiles(args.config)
+    result = {
+        "metric": "prefix-extend attention TFLOP/s (% bf16 MFMA peak) + uncached tokens/s",
+        "value": round(tflops_step, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.config}: {DESCRIPTIONS[args.config]}",
+            "requests": w.num_reqs,
+            "uncached_tokens": T,
+            "context_tokens": ctx,
+            "algorithmic_flop": flops,
+            "kv_pool": "fp8_e4m3" if w.kv_dtype else "bf16",
+        },
+        "pct_bf16_peak": round(100.0 * tflops_step / PEAK_BF16_TFLOPS, 2),
+        "uncached_tokens_per_s": round(T / (ms_step * 1e-3), 1),
+        "attn_ms": round(attn_ms, 4),
+        "attn_tflops": round(tflops_attn, 2),
+        "uncached_tokens_per_s_attn_only": round(T / (attn_ms * 1e-3), 1),
+        "store_ms": round(store_ms, 4),
+        "store_GBps": round(store_bytes / (store_ms * 1e-3) / 1e9, 1),
+        "roofline": {
+            "kernel": "extend_attn_kernel",
+            "bound": "mfma",
+            "achieved": round(tflops_attn, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(tflops_attn / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes": attn_alg_bytes,
+            "kernel_source": attn_source_hash(),
+        },
+    }
+    if not args.no_cpu_baseline:
+        cb = run_cpu_baseline(args.config, args.cpu_rows, args.cpu_reqs)
+        result["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v) for k, v in cb.items()}
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
