@@ -187,7 +187,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="llama8b", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=16)
+    ap.add_argument("--cpu-rows", type=int, default=32)
     ap.add_argument("--cpu-reqs", type=int, default=16)
     ap.add_argument("--calib-copy", action="store_true",
                     help="run only a plain 1 GiB device copy kernel (HBM counter calibration)")
