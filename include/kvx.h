@@ -37,6 +37,10 @@
 extern "C" {
 #endif
 
+/* Query rows of one extend_attention work item: suffix tokens x the query heads
+ * that share one KV head (tokens per item = KVX_TILE_ROWS / (Hq / Hkv)). */
+#define KVX_TILE_ROWS 256
+
 typedef struct kvx_pool kvx_pool; /* opaque; owned by the library */
 typedef void *kvx_stream_t;       /* a hipStream_t */
 
@@ -148,8 +152,8 @@ int store_kv(kvx_pool *pool, const kvx_batch *batch, const void *k_ext, const vo
  * The result equals attention over the whole context; only the suffix is computed
  * (Section 1: reuse the cached prefix, compute the uncached suffix).
  *   q            device bf16 [T, num_q_heads, head_dim]
- *   num_q_heads  a multiple of the pool's num_kv_heads, with (num_q_heads /
- *                num_kv_heads) dividing 128
+ *   num_q_heads  a multiple of the pool's num_kv_heads, with at most
+ *                KVX_TILE_ROWS query heads per KV head
  *   sm_scale     softmax scale, finite and > 0 (usually 1/sqrt(head_dim))
  *   out          device bf16 [T, num_q_heads, head_dim] (round to nearest even)
  *   lse          device fp32 [T, num_q_heads] natural-log sum of exp of the scaled

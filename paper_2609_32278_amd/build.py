@@ -17,8 +17,11 @@ LIB = os.path.join(PKG, "libkvx.so")
 
 ARCH = "gfx950"
 # Packed fp32 VALU ops are disabled for all device code (-packed-fp32-ops).
+# MFMA results go to ordinary VGPRs (the attention kernel keeps its score tiles,
+# which the softmax works on, out of AGPRs that would need copies back).
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             "-mllvm", "-amdgpu-mfma-vgpr-form=true",
              "-I", INCLUDE, "-I", CSRC]
 
 

@@ -5,25 +5,30 @@
 // holds, then the suffix itself, causally (the computation prefix caching
 // reduces to the uncached suffix, paper Sections 1 and 2).
 //
-// Workgroup = 4 waves = one AttnUnit: 128 query rows (tile_tok suffix tokens x
-// the `group` query heads that share one KV head) against a range of keys.
-// Per 64-key tile:
-//   * K [64 keys][D] and V^T [D][64 keys] pages are gathered through the page
-//     table into LDS (double buffered; the next tile's global loads are issued
-//     before the current tile's math);
-//   * S^T = K * Q^T on v_mfma_f32_32x32x16_bf16: K rows are the A operand (read
-//     from LDS), the wave's 32 query rows are the B operand (held in registers
-//     for the whole unit).  In the result each lane owns one query row and 16
-//     keys of it, so softmax statistics are per lane plus one exchange with the
-//     other half of the wave (v_permlane32_swap);
-//   * online softmax in base 2 with the running maximum moved only when a row's
-//     maximum grows by more than 2^8 (values stay <= 2^8, the final division
-//     cancels the reference point);
-//   * O^T += V^T * P^T: V^T from LDS is the A operand, the probabilities stay in
-//     registers as the B operand, converted to bf16 pairs.
+// Workgroup = 8 waves = one AttnUnit: 256 query rows (tile_tok suffix tokens x
+// the `group` query heads that share one KV head) against a range of keys, one
+// workgroup per CU (two waves per SIMD).  Each wave owns 32 rows.
+//
+// Per 32-key tile t (two pages):
+//   * K(t) and V^T(t) pages are gathered from the pool straight into LDS
+//     (global_load_lds_dwordx4, no staging registers) through a 4-deep ring:
+//     iteration t issues K(t+3) and V(t+2), and waits only for the loads issued
+//     one iteration earlier.  Page ids are read with scalar loads.
+//   * S^T(t) = K(t) Q^T on v_mfma_f32_32x32x16_bf16: K rows are the A operand
+//     (LDS), the wave's query rows the B operand (registers for the whole unit).
+//     In the result each lane owns one query row and 16 keys of it, so softmax
+//     statistics are per lane plus one v_permlane32_swap;
+//   * online softmax in base 2: p = exp2(s * scale - m) (one FMA + one exp per
+//     score).  The running maximum m moves only when a row's maximum grows by
+//     more than 2^8, so O is rarely rescaled (the final division cancels the
+//     reference point);
+//   * O^T += V^T(t) P^T(t): V^T from LDS is the A operand, P stays in registers
+//     as bf16 pairs, and the row sums are taken over those bf16 values (v_dot2).
+// Software pipeline: the MFMAs of S(t+1) are issued among the exp / pack of tile
+// t, and the MFMAs of O += P(t) V(t) among the row maximum of tile t+1.
 // MFMA row m of the S^T product is assigned key perm(m) (bits 2 and 3 of m
 // swapped), which makes the keys a lane holds in the S^T accumulators exactly
-// the 8 consecutive keys its B operand slot needs in the P^T * V product.
+// the 8 consecutive keys its B operand slot needs in the V^T P^T product.
 
 #include "kvx_internal.h"
 
@@ -31,12 +36,21 @@ namespace kvx {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;  // scalar-loaded
 
-constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
+constexpr int kWaves = kAttnThreads / 64;
+constexpr int kBN = 32;  // keys per LDS tile (two pages); split boundaries are multiples of it
+static_assert(kWaves * 32 == kTileRows, "one 32-row MFMA block per wave");
+static_assert(kTileKeys % kBN == 0, "split boundaries must fall on tile boundaries");
+
+// compile-time flags passed to the pipelined iteration
+struct False { static constexpr bool value = false; };
+struct True { static constexpr bool value = true; };
 
 __device__ __forceinline__ float pair_max(float x) {
   // v_permlane32_swap(x, x): r[0] holds the low half's value, r[1] the high half's,
@@ -56,7 +70,6 @@ __device__ __forceinline__ int row_key(int m) {
 }
 
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   bf16x2 v;
   v[0] = (__bf16)a;
   v[1] = (__bf16)b;
@@ -77,134 +90,262 @@ __device__ __forceinline__ uint4 fp8x8_to_bf16x8(uint2 c) {
   return r;
 }
 
-template <int D, bool FP8>
-struct TileGeom {
-  static constexpr int BN = kTileKeys;
-  static constexpr int PAGES = BN / kPageSize;          // 4 pages per tile
-  static constexpr int K_LD = D + 8;                    // padded LDS row strides (elements)
-  static constexpr int V_LD = BN + 8;
-  static constexpr int K_TILE = BN * K_LD;
-  static constexpr int V_TILE = D * V_LD;
-  static constexpr int STAGE = K_TILE + V_TILE;         // one buffer, elements
-  static constexpr int CHUNKS = PAGES * 2 * D;          // 8-element chunks per tile, per K and per V
-  static constexpr int PER_THREAD = CHUNKS / kAttnThreads;
-  static_assert(CHUNKS % kAttnThreads == 0, "tile chunks must spread evenly");
+template <int D>
+struct Geom {
+  static constexpr int KSTEPS = D / 16;          // MFMA k-steps over head_dim
+  static constexpr int DB = D / 32;              // 32-wide head_dim blocks of O^T
+  static constexpr int CPR = D / 8;              // 16-byte chunks per bf16 K row
+  static constexpr int TILE_BYTES = kBN * D * 2; // bf16 K tile == bf16 V^T tile
+  static constexpr int INSTR = TILE_BYTES / 1024;        // 1 KiB direct loads per tile (K or V)
+  static constexpr int PER_WAVE = 2 * INSTR / kWaves;    // K and V loads of one wave per iteration
+  static constexpr int NSTAGE = 4;               // LDS ring depth for K and for V^T
+  static_assert((2 * INSTR) % kWaves == 0, "loads must spread evenly over waves");
 };
 
-// Global -> register prefetch of one K tile and one V^T tile.
-template <int D, bool FP8>
-struct TileRegs {
-  using G = TileGeom<D, FP8>;
-  uint4 k[G::PER_THREAD];
-  uint4 v[G::PER_THREAD];
+// LDS layouts (unpadded, XOR-swizzled so that the MFMA operand reads are free of
+// bank conflicts while every 1 KiB of a tile can be written by one wave-wide
+// direct load):
+//   K tile   [32 keys][D] bf16; 16-byte chunk c of key row r is stored at chunk
+//            c ^ (r % CPR) of that row.
+//   V^T tile [2 pages][D dims][16 slots] bf16; 16-byte chunk c (slots 8c..8c+7)
+//            of dim row d is stored at chunk c ^ ((d >> 3) & 1).
+// Load g = it * 8 + wave of a tile pair is K load j = g (g < INSTR) or V load
+// j = g - INSTR; lane l of load j writes bytes [1024 j + 16 l, +16) of its tile.
+//   K: row r = j * (64 / CPR) + l / CPR, stored chunk l % CPR.
+//   V: page j / (D/32), dim (j % (D/32)) * 32 + l / 2, stored chunk l % 2.
+// Each load falls inside one page.
+
+struct Ctx {
+  const_i32_ptr page_ids;
+  const void* k_pool;
+  const void* v_pool;
+  int num_kv_heads;
+  int page_base;
+  int key_end;
+  int kv_head;
 };
 
-template <int D, bool FP8>
-__device__ __forceinline__ void load_tile(TileRegs<D, FP8>& r, const AttnParams& p, const AttnUnit& u,
-                                          int kv_head, int k0) {
-  using G = TileGeom<D, FP8>;
-  constexpr int EB = FP8 ? 1 : 2;  // bytes per pool element
-  const int lp0 = k0 / kPageSize;
-  int pid[G::PAGES];
-#pragma unroll
-  for (int j = 0; j < G::PAGES; j++) {
-    const bool valid = (lp0 + j) * kPageSize < u.key_end;
-    pid[j] = valid ? __builtin_amdgcn_readfirstlane(p.page_ids[u.page_base + lp0 + j]) : -1;
-  }
-  const bool tail = k0 + G::BN > u.key_end;
-#pragma unroll
-  for (int it = 0; it < G::PER_THREAD; it++) {
-    const int c = threadIdx.x + it * kAttnThreads;
-    const int j = c / (2 * D);       // page within the tile
-    const int w = c % (2 * D);
-    const int page = pid[j];
-    // K chunk: slot w / (D/8), elements (w % (D/8)) * 8 .. +8
-    const int ks = w / (D / 8), kc = w % (D / 8);
-    // V^T chunk: dim row w / 2, slots (w % 2) * 8 .. +8
-    const int vd = w / 2, vh = w % 2;
-    uint4 kx = make_uint4(0, 0, 0, 0), vx = make_uint4(0, 0, 0, 0);
-    if (page >= 0) {
-      const size_t blk = ((size_t)page * p.num_kv_heads + kv_head) * (size_t)(kPageSize * D);
-      const char* kb = (const char*)p.k_pool + (blk + (size_t)ks * D + kc * 8) * EB;
-      const char* vb = (const char*)p.v_pool + (blk + (size_t)vd * kPageSize + vh * 8) * EB;
-      if constexpr (FP8) {
-        kx = fp8x8_to_bf16x8(*(const uint2*)kb);
-        vx = fp8x8_to_bf16x8(*(const uint2*)vb);
-      } else {
-        kx = *(const uint4*)kb;
-        vx = *(const uint4*)vb;
-      }
-      if (tail) {
-        // keys at or beyond key_end are never weighted; zero them so that slots
-        // never written (possibly NaN) cannot leak through 0 * NaN
-        const int key_k = k0 + j * kPageSize + ks;
-        if (key_k >= u.key_end) kx = make_uint4(0, 0, 0, 0);
-        const int key_v = k0 + j * kPageSize + vh * 8;
-        uint32_t* vw = (uint32_t*)&vx;
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-          const uint32_t lo = (key_v + 2 * e < u.key_end) ? 0xFFFFu : 0u;
-          const uint32_t hi = (key_v + 2 * e + 1 < u.key_end) ? 0xFFFF0000u : 0u;
-          vw[e] &= (lo | hi);
-        }
-      }
+// Physical page (uniform, scalar load) holding logical page lp of the unit's
+// request; pages at or past key_end fall back to the page holding key_end - 1, so
+// every address stays inside the pool (their keys are masked, and V is zeroed on
+// the register path).
+__device__ __forceinline__ int page_of(const Ctx& c, int lp) {
+  const int last = (c.key_end - 1) / kPageSize;
+  return c.page_ids[c.page_base + (lp < last ? lp : last)];
+}
+
+template <int D>
+struct LoadSlot {
+  bool is_v;     // this slot loads V^T (else K)
+  int j;         // load index within the tile
+  int off;       // per-lane byte offset inside the page block (bf16 elements x 2)
+  int page_sel;  // which page (0/1) of the tile
+  __device__ __forceinline__ void init(int g, int lane) {
+    using G = Geom<D>;
+    is_v = g >= G::INSTR;
+    j = is_v ? g - G::INSTR : g;
+    if (is_v) {
+      const int d = (j % (D / 32)) * 32 + lane / 2;
+      const int ch = (lane % 2) ^ ((d >> 3) & 1);
+      off = (d * kPageSize + ch * 8) * 2;
+      page_sel = j / (D / 32);
+    } else {
+      const int r = j * (64 / G::CPR) + lane / G::CPR;
+      const int ch = (lane % G::CPR) ^ (r % G::CPR);
+      off = ((r % kPageSize) * D + ch * 8) * 2;
+      page_sel = r / kPageSize;
     }
-    r.k[it] = kx;
-    r.v[it] = vx;
   }
+};
+
+template <int D>
+__device__ __forceinline__ const char* page_block(const Ctx& c, const LoadSlot<D>& s, int k0, int eb) {
+  const int page = page_of(c, k0 / kPageSize + s.page_sel);
+  return (const char*)(s.is_v ? c.v_pool : c.k_pool) +
+         ((size_t)page * c.num_kv_heads + c.kv_head) * (size_t)(kPageSize * D) * eb;
 }
 
+// Direct global -> LDS load of one 1 KiB piece of a bf16 tile (no registers):
+// lane l's 16 bytes at base + off land at LDS address lds + 16 l.  Issued as
+// inline assembly so that the compiler's wait-count tracking, which cannot tell
+// the ring slots apart and would drain every outstanding load before the next
+// one and before each barrier, stays out of the way; the kernel orders these
+// loads itself with explicit vmcnt waits and barriers.
+__device__ __forceinline__ void lds_dma_16(const char* sbase, int voff, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2"
+      :
+      : "s"(lds), "v"(voff), "s"(sbase)
+      : "memory", "m0");
+}
+
+template <int D>
+__device__ __forceinline__ void issue_direct(const LoadSlot<D>& s, const Ctx& c, int k0, uint8_t* tile) {
+  const char* base = page_block<D>(c, s, k0, 2);
+  const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)(tile + s.j * 1024);
+  lds_dma_16(base, s.off, lds);
+}
+
+// Register path for one piece: fp8 pools (converted to bf16 here) and V tiles
+// holding keys at or past key_end (zeroed here, so that unwritten, possibly NaN,
+// slots never meet a zero weight).  Same LDS layout as the direct loads.
 template <int D, bool FP8>
-__device__ __forceinline__ void store_tile(const TileRegs<D, FP8>& r, uint16_t* stage) {
-  using G = TileGeom<D, FP8>;
-  uint16_t* kt = stage;
-  uint16_t* vt = stage + G::K_TILE;
+__device__ __forceinline__ uint4 load_piece(const LoadSlot<D>& s, const Ctx& c, int k0) {
+  constexpr int EB = FP8 ? 1 : 2;
+  const char* src = page_block<D>(c, s, k0, EB) + s.off / 2 * EB;
+  uint4 x;
+  if constexpr (FP8) x = fp8x8_to_bf16x8(*(const uint2*)src);
+  else x = *(const uint4*)src;
+  if (k0 + kBN > c.key_end) {
+    const int elem = s.off / 2;  // element offset inside the page block
+    if (s.is_v) {
+      const int key = k0 + s.page_sel * kPageSize + (elem % kPageSize);
+      uint32_t* xw = (uint32_t*)&x;
 #pragma unroll
-  for (int it = 0; it < G::PER_THREAD; it++) {
-    const int c = threadIdx.x + it * kAttnThreads;
-    const int j = c / (2 * D);
-    const int w = c % (2 * D);
-    const int ks = w / (D / 8), kc = w % (D / 8);
-    const int vd = w / 2, vh = w % 2;
-    *(uint4*)(kt + (j * kPageSize + ks) * G::K_LD + kc * 8) = r.k[it];
-    *(uint4*)(vt + vd * G::V_LD + j * kPageSize + vh * 8) = r.v[it];
+      for (int e = 0; e < 4; e++) {
+        const uint32_t lo = (key + 2 * e < c.key_end) ? 0xFFFFu : 0u;
+        const uint32_t hi = (key + 2 * e + 1 < c.key_end) ? 0xFFFF0000u : 0u;
+        xw[e] &= (lo | hi);
+      }
+    } else {
+      const int key = k0 + s.page_sel * kPageSize + elem / D;
+      if (key >= c.key_end) x = make_uint4(0, 0, 0, 0);
+    }
+  }
+  return x;
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  // s_waitcnt with only the vector-memory counter limited (expcnt, lgkmcnt at max)
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// S^T of one tile for this wave's 32 rows.
+template <int D>
+__device__ __forceinline__ void qk_tile(f32x16& s, const uint8_t* kt, const int (&koff)[Geom<D>::KSTEPS],
+                                        const bf16x8 (&qf)[Geom<D>::KSTEPS]) {
+  using G = Geom<D>;
+  s = f32x16{};
+#pragma unroll
+  for (int st = 0; st < G::KSTEPS; st++) {
+    const bf16x8 a = *(const bf16x8*)(kt + koff[st]);
+    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], s, 0, 0, 0);
+  }
+}
+
+// Raw row maximum of a tile (optionally causally masked in place), combined over
+// both halves of the wave.  Accumulator i holds key k0 + 16*(i/8) + 8*h + i%8.
+template <bool MASK>
+__device__ __forceinline__ float row_max(f32x16& s, int k0, int qpos, int h) {
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 16; i++) {
+    float x = s[i];
+    if constexpr (MASK) {
+      const int key = k0 + 16 * (i / 8) + 8 * h + (i % 8);
+      x = key > qpos ? -INFINITY : x;
+      s[i] = x;
+    }
+    m = fmaxf(m, x);
+  }
+  return pair_max(m);
+}
+
+// p = exp2(s * scale - m) as bf16 pairs (the P^T B operands, one per page of the
+// tile); returns the row sum over those bf16 values added to l.
+__device__ __forceinline__ float exp_pack(const f32x16& s, bf16x8 (&pb)[2], float l, float m_run, float scale) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  const float neg = -m_run;
+#pragma unroll
+  for (int hf = 0; hf < 2; hf++) {
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; e++) {
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * hf + 2 * e], scale, neg));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * hf + 2 * e + 1], scale, neg));
+      w[e] = pack_bf16(p0, p1);
+      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, l, false);
+    }
+    pb[hf] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+  }
+  return l;
+}
+
+// O^T += V^T P^T: page hf of the tile against keys 16*hf .. 16*hf+15.
+template <int D>
+__device__ __forceinline__ void pv_tile(f32x16 (&o)[Geom<D>::DB], const uint8_t* vt, int vbase, const bf16x8 (&pb)[2]) {
+  using G = Geom<D>;
+#pragma unroll
+  for (int hf = 0; hf < 2; hf++) {
+#pragma unroll
+    for (int b = 0; b < G::DB; b++) {
+      const bf16x8 a = *(const bf16x8*)(vt + hf * (D * 32) + b * 1024 + vbase);
+      o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[hf], o[b], 0, 0, 0);
+    }
   }
 }
 
 template <int D, bool FP8>
-__global__ __launch_bounds__(kAttnThreads, 2) void extend_attn_kernel(AttnParams p) {
-  using G = TileGeom<D, FP8>;
-  constexpr int KSTEPS = D / 16;  // MFMA k-steps over head_dim
-  constexpr int DB = D / 32;      // 32-wide blocks of head_dim in O^T
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * G::STAGE];
+__global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams p) {
+  using G = Geom<D>;
+  __shared__ __attribute__((aligned(1024))) uint8_t k_lds[G::NSTAGE][G::TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_lds[G::NSTAGE][G::TILE_BYTES];
 
-  const AttnUnit u = p.units[blockIdx.x];
+  // the work item, read with scalar loads: every index derived from it stays uniform
+  AttnUnit u;
+  {
+    const const_i32_ptr w = (const_i32_ptr)(p.units + blockIdx.x);
+    u.qo_row0 = w[0];
+    u.q_pos0 = w[1];
+    u.page_base = w[2];
+    u.key_begin = w[3];
+    u.key_end = w[4];
+    u.head_ntok = w[5];
+    u.part = w[6];
+    u.req = w[7];
+  }
   if (u.key_end <= u.key_begin) return;  // padding entry: uniform exit
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int n = lane & 31;  // query row within the wave / MFMA row
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n = lane & 31;  // query row within the wave's block / MFMA row
   const int h = lane >> 5;  // half of the wave
   const int kv_head = u.head_ntok >> 16;
   const int ntok = u.head_ntok & 0xFFFF;
+  const Ctx c{(const_i32_ptr)p.page_ids, p.k_pool, p.v_pool, p.num_kv_heads, u.page_base, u.key_end, kv_head};
 
   // this lane's query row: row rho = token * group + head-in-group
   const int rho = wave * 32 + n;
   const int tok = rho / p.group;
   const int hq = kv_head * p.group + (rho - tok * p.group);
-  const bool row_valid = tok < ntok;
+  const bool valid = tok < ntok;
   const int qpos = u.q_pos0 + tok;
 
   // Q^T operand: k-slot (h, j) of k-step s holds dim h*D/2 + 8s + j
-  bf16x8 qf[KSTEPS];
+  bf16x8 qf[G::KSTEPS];
   {
     const uint4* src = (const uint4*)(p.q + ((size_t)(u.qo_row0 + tok) * p.num_q_heads + hq) * D + h * (D / 2));
 #pragma unroll
-    for (int s = 0; s < KSTEPS; s++) {
-      uint4 v = row_valid ? src[s] : make_uint4(0, 0, 0, 0);
-      qf[s] = __builtin_bit_cast(bf16x8, v);
-    }
+    for (int s = 0; s < G::KSTEPS; s++) qf[s] = __builtin_bit_cast(bf16x8, valid ? src[s] : make_uint4(0, 0, 0, 0));
   }
+
+  // LDS read offsets.  K: MFMA row n holds key row_key(n); k-step st reads dims
+  // h*D/2 + 8st .. +8, i.e. chunk h*CPR/2 + st, stored swizzled.  V^T: dim 32b + n,
+  // slots 8h..8h+7 of page hf.
+  int koff[G::KSTEPS];
+  {
+    const int r = row_key(n);
+#pragma unroll
+    for (int st = 0; st < G::KSTEPS; st++) koff[st] = r * (D * 2) + (((h * (G::CPR / 2) + st) ^ (r % G::CPR)) * 16);
+  }
+  const int vbase = n * 32 + ((h ^ ((n >> 3) & 1)) * 16);
+  LoadSlot<D> slot[G::PER_WAVE];
+#pragma unroll
+  for (int it = 0; it < G::PER_WAVE; it++) slot[it].init(it * kWaves + wave, lane);
 
   float scale = p.scale_log2;
   float vscale = 1.0f;
@@ -213,113 +354,149 @@ __global__ __launch_bounds__(kAttnThreads, 2) void extend_attn_kernel(AttnParams
     vscale = p.v_scale[kv_head];
   }
 
-  f32x16 o[DB];
+  f32x16 o[G::DB];
 #pragma unroll
-  for (int b = 0; b < DB; b++) o[b] = f32x16{};
-  float m_run = -1e30f;
-  float l_run = 0.0f;
+  for (int b = 0; b < G::DB; b++) o[b] = f32x16{};
+  float m_run = -1e30f, l_run = 0.0f, mx;
 
-  const int k_first = u.key_begin;
-  const int n_tiles = (u.key_end - k_first + G::BN - 1) / G::BN;
-  const int krow0 = row_key(n);
+  const int kb0 = u.key_begin;
+  const int n_tiles = (u.key_end - kb0 + kBN - 1) / kBN;
+  // tiles [0, n_full) hold keys every row of the unit sees; later ones need the causal mask
+  int n_full = (u.q_pos0 + 1 - kb0) / kBN;
+  n_full = n_full < 0 ? 0 : (n_full > n_tiles ? n_tiles : n_full);
+  const int last_whole = (u.key_end - kb0) / kBN;  // tiles [0, last_whole) lie inside [kb0, key_end)
 
-  TileRegs<D, FP8> regs;
-  load_tile<D, FP8>(regs, p, u, kv_head, k_first);
-  store_tile<D, FP8>(regs, lds);
+  // Issue this wave's pieces of K(tk) and V(tv) into the ring (tk / tv < 0: skip).
+  // bf16 pool: direct loads, except for a V tile reaching past key_end, which is
+  // loaded, zeroed and written synchronously (V pieces go first, so that wait only
+  // covers older loads).  Returns the direct loads issued.
+  // fp8 pool: every piece goes through registers (converted to bf16); finish()
+  // writes them to LDS after the compute block.  Tile indices are clamped so that
+  // the register loads are unconditional.
+  uint4 regs[G::PER_WAVE];
+  auto issue = [&](int tk, int tv) -> int {
+    int direct = 0;
+#pragma unroll
+    for (int it = G::PER_WAVE - 1; it >= 0; it--) {
+      const LoadSlot<D>& s = slot[it];
+      const int t = s.is_v ? tv : tk;
+      if constexpr (FP8) {
+        regs[it] = load_piece<D, true>(s, c, kb0 + (t < 0 ? 0 : t) * kBN);
+      } else {
+        if (t < 0) continue;
+        uint8_t* tile = s.is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
+        if (s.is_v && t >= last_whole) {
+          *(uint4*)(tile + s.j * 1024 + lane * 16) = load_piece<D, false>(s, c, kb0 + t * kBN);
+        } else {
+          issue_direct<D>(s, c, kb0 + t * kBN, tile);
+          direct++;
+        }
+      }
+    }
+    return direct;
+  };
+  auto finish = [&](int tk, int tv) {
+    if constexpr (FP8) {
+#pragma unroll
+      for (int it = 0; it < G::PER_WAVE; it++) {
+        const LoadSlot<D>& s = slot[it];
+        const int t = s.is_v ? tv : tk;
+        if (t < 0) continue;
+        uint8_t* tile = s.is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
+        *(uint4*)(tile + s.j * 1024 + lane * 16) = regs[it];
+      }
+    }
+  };
+
+  // ---- prologue: K(0..2), V(0..1) resident; S(0) and its row maximum
+  issue(0, 0);
+  finish(0, 0);
+  issue(n_tiles > 1 ? 1 : -1, n_tiles > 1 ? 1 : -1);
+  finish(1, 1);
+  issue(n_tiles > 2 ? 2 : -1, -1);
+  finish(2, -1);
+  wait_vmcnt<0>();
   __syncthreads();
 
-  for (int t = 0; t < n_tiles; t++) {
-    const int k0 = k_first + t * G::BN;
-    const bool more = t + 1 < n_tiles;
-    if (more) load_tile<D, FP8>(regs, p, u, kv_head, k0 + G::BN);
+  f32x16 sa, sb;
+  bf16x8 pb[2];
+  qk_tile<D>(sa, k_lds[0], koff, qf);
+  mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
 
-    const uint16_t* kt = lds + (t & 1) * G::STAGE;
-    const uint16_t* vt = kt + G::K_TILE;
+  // One pipelined iteration: consumes S(t) (scores in s_cur, maximum in mx), produces
+  // S(t+1) into s_nxt with its maximum, accumulates P(t) V(t).  Issues K(t+3) and
+  // V(t+2) into the ring and waits for K(t+2) and V(t+1), issued one iteration ago.
+  // In the unmasked variant tile t+1 exists and needs no mask, so the compute part
+  // is one branch-free block in which MFMA and the softmax VALU work interleave.
+  auto iteration = [&](f32x16& s_cur, f32x16& s_nxt, int t, auto masked) {
+    constexpr bool MASKED = decltype(masked)::value;
+    const int k0 = kb0 + t * kBN;
+    const bool has_next = MASKED ? t + 1 < n_tiles : true;
+    const int tk = t + 3 < n_tiles ? t + 3 : -1;
+    const int tv = t + 2 < n_tiles ? t + 2 : -1;
+    const int issued = issue(tk, tv);
 
-    // ---- S^T = K Q^T for two 32-key blocks
-    f32x16 s[2];
-#pragma unroll
-    for (int blk = 0; blk < 2; blk++) {
-      s[blk] = f32x16{};
-      const uint16_t* krow = kt + (blk * 32 + krow0) * G::K_LD + h * (D / 2);
-#pragma unroll
-      for (int st = 0; st < KSTEPS; st++) {
-        bf16x8 a = *(const bf16x8*)(krow + st * 8);
-        s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], s[blk], 0, 0, 0);
-      }
-    }
-
-    // ---- online softmax (base 2); accumulator i of block blk holds key
-    //      k0 + 32*blk + 16*(i/8) + 8*h + i%8 of this lane's query row
-    const bool masked = k0 + G::BN - 1 > u.q_pos0;
-    float mx = -INFINITY;
-#pragma unroll
-    for (int blk = 0; blk < 2; blk++) {
-#pragma unroll
-      for (int i = 0; i < 16; i++) {
-        float x = s[blk][i] * scale;
-        if (masked) {
-          const int key = k0 + blk * 32 + 16 * (i / 8) + 8 * h + (i % 8);
-          x = key > qpos ? -INFINITY : x;
-        }
-        s[blk][i] = x;
-        mx = fmaxf(mx, x);
-      }
-    }
-    mx = pair_max(mx);
-    if (__any(mx > m_run + kRescaleThreshold)) {
-      const float m_new = fmaxf(m_run, mx);
+    // lazy rescale: move the reference maximum only when a row outgrows it by 2^8
+    if (__any(mx * scale > m_run + kRescaleThreshold)) {
+      const float m_new = fmaxf(m_run, mx * scale);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
 #pragma unroll
-      for (int b = 0; b < DB; b++) o[b] *= alpha;
+      for (int b = 0; b < G::DB; b++) o[b] *= alpha;
       m_run = m_new;
     }
-    float rs = 0.0f;
-#pragma unroll
-    for (int blk = 0; blk < 2; blk++) {
-#pragma unroll
-      for (int i = 0; i < 16; i++) {
-        const float e = __builtin_amdgcn_exp2f(s[blk][i] - m_run);
-        s[blk][i] = e;
-        rs += e;
-      }
-    }
-    l_run += rs;
 
-    // ---- O^T += V^T P^T, 16 keys per MFMA
-#pragma unroll
-    for (int blk = 0; blk < 2; blk++) {
-#pragma unroll
-      for (int hf = 0; hf < 2; hf++) {
-        uint4 pw;
-        pw.x = pack_bf16(s[blk][8 * hf + 0], s[blk][8 * hf + 1]);
-        pw.y = pack_bf16(s[blk][8 * hf + 2], s[blk][8 * hf + 3]);
-        pw.z = pack_bf16(s[blk][8 * hf + 4], s[blk][8 * hf + 5]);
-        pw.w = pack_bf16(s[blk][8 * hf + 6], s[blk][8 * hf + 7]);
-        const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-        const uint16_t* vrow = vt + n * G::V_LD + blk * 32 + 16 * hf + 8 * h;
-#pragma unroll
-        for (int b = 0; b < DB; b++) {
-          bf16x8 a = *(const bf16x8*)(vrow + b * 32 * G::V_LD);
-          o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[b], 0, 0, 0);
-        }
-      }
+    if constexpr (MASKED) {
+      if (has_next) qk_tile<D>(s_nxt, k_lds[(t + 1) % G::NSTAGE], koff, qf);
+      l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
+      pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
+      if (has_next) mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
+    } else {
+      qk_tile<D>(s_nxt, k_lds[(t + 1) % G::NSTAGE], koff, qf);
+      l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
+      pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
+      mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     }
 
-    if (more) store_tile<D, FP8>(regs, lds + ((t + 1) & 1) * G::STAGE);
+    finish(tk, tv);
+    if constexpr (G::PER_WAVE == 2) {
+      if (issued == 2) wait_vmcnt<2>();
+      else if (issued == 1) wait_vmcnt<1>();
+      else wait_vmcnt<0>();
+    } else {
+      if (issued == 1) wait_vmcnt<1>();
+      else wait_vmcnt<0>();
+    }
     __syncthreads();
+  };
+
+  int t = 0;
+  // unmasked part: S(t+1) needs no mask while t + 1 < n_full
+  for (; t + 2 < n_full; t += 2) {
+    iteration(sa, sb, t, False{});
+    iteration(sb, sa, t + 1, False{});
   }
+  if (t + 1 < n_full) {
+    iteration(sa, sb, t, False{});
+    t++;
+    sa = sb;
+  }
+  for (; t < n_tiles; t += 2) {
+    iteration(sa, sb, t, True{});
+    if (t + 1 < n_tiles) iteration(sb, sa, t + 1, True{});
+  }
+
+  wait_vmcnt<0>();  // no load into this workgroup's LDS may outlive it
 
   // ---- epilogue: lane (n, h) holds dims 32*b + 8*(i/4) + 4*h + i%4 of its row
   const float l_tot = pair_sum(l_run);
   const float inv = l_tot > 0.0f ? vscale / l_tot : 0.0f;
   const float lse_val = l_tot > 0.0f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
   if (u.part < 0) {
-    if (row_valid) {
+    if (valid) {
       uint16_t* dst = p.out + ((size_t)(u.qo_row0 + tok) * p.num_q_heads + hq) * D;
 #pragma unroll
-      for (int b = 0; b < DB; b++) {
+      for (int b = 0; b < G::DB; b++) {
 #pragma unroll
         for (int g4 = 0; g4 < 4; g4++) {
           uint2 w;
@@ -333,7 +510,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void extend_attn_kernel(AttnParams
   } else {
     float* dst = p.o_part + ((size_t)u.part * kTileRows + rho) * D;
 #pragma unroll
-    for (int b = 0; b < DB; b++) {
+    for (int b = 0; b < G::DB; b++) {
 #pragma unroll
       for (int g4 = 0; g4 < 4; g4++) {
         f32x4 w;

@@ -128,7 +128,7 @@ struct Workspace {
   }
 };
 
-constexpr int kPlanSlots = 512;       // 256 CUs x 2 resident attention workgroups
+constexpr int kPlanSlots = 256;       // 256 CUs x 1 resident attention workgroup
 constexpr int64_t kMaxParts = 32768;  // bound on split partial results (2 GiB at head_dim 128)
 int32_t g_split_keys = 0;             // 0 = automatic
 

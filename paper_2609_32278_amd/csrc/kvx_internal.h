@@ -10,9 +10,9 @@
 namespace kvx {
 
 constexpr int kPageSize = 16;
-constexpr int kTileRows = 128;  // query rows (token x query head of one KV head) per attention workgroup
+constexpr int kTileRows = KVX_TILE_ROWS;  // query rows (token x query head of one KV head) per workgroup
 constexpr int kTileKeys = 64;   // keys per K/V tile staged in LDS
-constexpr int kAttnThreads = 256;
+constexpr int kAttnThreads = 512;  // 8 waves x 32 query rows
 constexpr int kNumXcd = 8;      // L2 domains of an MI355X; workgroup i runs on XCD i % 8
 
 // One attention workgroup: a tile of suffix tokens of one request and one KV head,

@@ -12,6 +12,7 @@ from paper_2609_32278_amd import kvx
 from paper_2609_32278_amd import workloads as wl
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+TILE_ROWS = int(re.search(r"#define KVX_TILE_ROWS (\d+)", open(os.path.join(ROOT, "include", "kvx.h")).read()).group(1))
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -61,7 +62,7 @@ def test_hot_path_argument_errors_before_any_device_work():
     # plan-level checks
     assert _err(kvx.extend_attention_plan, b, 6, 4, 128) == kvx.KVX_EINVAL      # 6 % 4 != 0
     assert _err(kvx.extend_attention_plan, b, 4, 2, 80) == kvx.KVX_EUNSUPPORTED  # head_dim
-    assert _err(kvx.extend_attention_plan, b, 512, 2, 128) == kvx.KVX_EUNSUPPORTED
+    assert _err(kvx.extend_attention_plan, b, 1024, 2, 128) == kvx.KVX_EUNSUPPORTED  # > 256 q heads per kv head
     short = kvx.Batch([16], [17], [0, 2], 0x1000)                                # 33 tokens need 3 pages
     assert _err(kvx.extend_attention_plan, short, 4, 2, 128) == kvx.KVX_EINVAL
     neg = kvx.Batch([-1], [4], [0, 1], 0x1000)
@@ -78,7 +79,7 @@ def _check_plan(w, split=0):
     finally:
         kvx.kvx_set_split_keys(0)
     g = w.group
-    tile_tok = 128 // g
+    tile_tok = TILE_ROWS // g
     real = items[items["req"] >= 0]
     # dispatch position i runs on XCD i % 8
     assert (items["xcd"] == np.arange(len(items)) % 8).all()
