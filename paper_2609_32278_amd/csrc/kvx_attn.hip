@@ -158,11 +158,9 @@ struct LoadSlot {
   }
 };
 
-template <int D>
-__device__ __forceinline__ const char* page_block(const Ctx& c, const LoadSlot<D>& s, int k0, int eb) {
-  const int page = page_of(c, k0 / kPageSize + s.page_sel);
-  return (const char*)(s.is_v ? c.v_pool : c.k_pool) +
-         ((size_t)page * c.num_kv_heads + c.kv_head) * (size_t)(kPageSize * D) * eb;
+// Byte address of (physical page, this unit's KV head) in the pool of the slot.
+__device__ __forceinline__ const char* page_block(const char* head_base, uint32_t page, uint32_t page_bytes) {
+  return head_base + (uint64_t)page * page_bytes;
 }
 
 // Direct global -> LDS load of one 1 KiB piece of a bf16 tile (no registers):
@@ -182,19 +180,18 @@ __device__ __forceinline__ void lds_dma_16(const char* sbase, int voff, uint32_t
 }
 
 template <int D>
-__device__ __forceinline__ void issue_direct(const LoadSlot<D>& s, const Ctx& c, int k0, uint8_t* tile) {
-  const char* base = page_block<D>(c, s, k0, 2);
+__device__ __forceinline__ void issue_direct(const LoadSlot<D>& s, const char* block, uint8_t* tile) {
   const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)(tile + s.j * 1024);
-  lds_dma_16(base, s.off, lds);
+  lds_dma_16(block, s.off, lds);
 }
 
 // Register path for one piece: fp8 pools (converted to bf16 here) and V tiles
 // holding keys at or past key_end (zeroed here, so that unwritten, possibly NaN,
 // slots never meet a zero weight).  Same LDS layout as the direct loads.
 template <int D, bool FP8>
-__device__ __forceinline__ uint4 load_piece(const LoadSlot<D>& s, const Ctx& c, int k0) {
+__device__ __forceinline__ uint4 load_piece(const LoadSlot<D>& s, const char* block, const Ctx& c, int k0) {
   constexpr int EB = FP8 ? 1 : 2;
-  const char* src = page_block<D>(c, s, k0, EB) + s.off / 2 * EB;
+  const char* src = block + s.off / 2 * EB;
   uint4 x;
   if constexpr (FP8) x = fp8x8_to_bf16x8(*(const uint2*)src);
   else x = *(const uint4*)src;
@@ -374,6 +371,18 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   // writes them to LDS after the compute block.  Tile indices are clamped so that
   // the register loads are unconditional.
   uint4 regs[G::PER_WAVE];
+  // per slot: the pool base of this KV head, and the page id of the tile the slot
+  // loads next (read one iteration ahead, so the scalar load is off the critical path)
+  constexpr int EBYTES = FP8 ? 1 : 2;
+  const uint32_t page_bytes = (uint32_t)p.num_kv_heads * (kPageSize * D * EBYTES);
+  const char* head_base[G::PER_WAVE];
+  uint32_t pid[G::PER_WAVE];
+#pragma unroll
+  for (int it = 0; it < G::PER_WAVE; it++)
+    head_base[it] = (const char*)(slot[it].is_v ? p.v_pool : p.k_pool) + (size_t)kv_head * (kPageSize * D * EBYTES);
+  auto page_for = [&](int it, int t) -> uint32_t {
+    return (uint32_t)page_of(c, (kb0 + t * kBN) / kPageSize + slot[it].page_sel);
+  };
   auto issue = [&](int tk, int tv) -> int {
     int direct = 0;
 #pragma unroll
@@ -381,16 +390,19 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       const LoadSlot<D>& s = slot[it];
       const int t = s.is_v ? tv : tk;
       if constexpr (FP8) {
-        regs[it] = load_piece<D, true>(s, c, kb0 + (t < 0 ? 0 : t) * kBN);
+        const int tt = t < 0 ? 0 : t;
+        regs[it] = load_piece<D, true>(s, page_block(head_base[it], page_for(it, tt), page_bytes), c, kb0 + tt * kBN);
       } else {
         if (t < 0) continue;
         uint8_t* tile = s.is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
+        const char* block = page_block(head_base[it], pid[it], page_bytes);
         if (s.is_v && t >= last_whole) {
-          *(uint4*)(tile + s.j * 1024 + lane * 16) = load_piece<D, false>(s, c, kb0 + t * kBN);
+          *(uint4*)(tile + s.j * 1024 + lane * 16) = load_piece<D, false>(s, block, c, kb0 + t * kBN);
         } else {
-          issue_direct<D>(s, c, kb0 + t * kBN, tile);
+          issue_direct<D>(s, block, tile);
           direct++;
         }
+        pid[it] = page_for(it, t + 1);  // next iteration's tile for this slot
       }
     }
     return direct;
@@ -409,13 +421,20 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   };
 
   // ---- prologue: K(0..2), V(0..1) resident; S(0) and its row maximum
+#pragma unroll
+  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 0);
   issue(0, 0);
   finish(0, 0);
   issue(n_tiles > 1 ? 1 : -1, n_tiles > 1 ? 1 : -1);
   finish(1, 1);
+#pragma unroll
+  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 2);
   issue(n_tiles > 2 ? 2 : -1, -1);
   finish(2, -1);
   wait_vmcnt<0>();
+  // page ids of the first loop iteration's tiles: K(3), V(2)
+#pragma unroll
+  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, slot[it].is_v ? 2 : 3);
   __syncthreads();
 
   f32x16 sa, sb;
@@ -452,10 +471,45 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
       if (has_next) mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
     } else {
-      qk_tile<D>(s_nxt, k_lds[(t + 1) % G::NSTAGE], koff, qf);
-      l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
-      pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
-      mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
+      // Written in issue order: every K fragment of tile t+1 and the first V^T
+      // fragments of tile t are read up front; each S(t+1) MFMA is followed by one
+      // pair of the exp / pack work of tile t; the row maximum of S(t+1) runs
+      // between the O MFMAs.
+      const uint8_t* kt = k_lds[(t + 1) % G::NSTAGE];
+      const uint8_t* vt = v_lds[t % G::NSTAGE];
+      constexpr int VPRE = G::DB;  // V^T fragments read ahead (one page)
+      bf16x8 kf[G::KSTEPS], vf[2 * G::DB];
+#pragma unroll
+      for (int st = 0; st < G::KSTEPS; st++) kf[st] = *(const bf16x8*)(kt + koff[st]);
+#pragma unroll
+      for (int i = 0; i < VPRE; i++) vf[i] = *(const bf16x8*)(vt + (i / G::DB) * (D * 32) + (i % G::DB) * 1024 + vbase);
+      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+      const float neg = -m_run;
+      uint32_t pw[8];
+      s_nxt = f32x16{};
+#pragma unroll
+      for (int st = 0; st < G::KSTEPS; st++) {
+        s_nxt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qf[st], s_nxt, 0, 0, 0);
+#pragma unroll
+        for (int e = st * 8 / G::KSTEPS; e < (st + 1) * 8 / G::KSTEPS; e++) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[2 * e], scale, neg));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[2 * e + 1], scale, neg));
+          pw[e] = pack_bf16(p0, p1);
+          l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw[e]), ones, l_run, false);
+        }
+      }
+      pb[0] = __builtin_bit_cast(bf16x8, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+      pb[1] = __builtin_bit_cast(bf16x8, make_uint4(pw[4], pw[5], pw[6], pw[7]));
+#pragma unroll
+      for (int i = VPRE; i < 2 * G::DB; i++) vf[i] = *(const bf16x8*)(vt + (i / G::DB) * (D * 32) + (i % G::DB) * 1024 + vbase);
+      float m = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 2 * G::DB; i++) {
+        o[i % G::DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pb[i / G::DB], o[i % G::DB], 0, 0, 0);
+#pragma unroll
+        for (int e = i * 16 / (2 * G::DB); e < (i + 1) * 16 / (2 * G::DB); e++) m = fmaxf(m, s_nxt[e]);
+      }
+      mx = pair_max(m);
     }
 
     finish(tk, tv);
