@@ -9,7 +9,7 @@
 // the `group` query heads that share one KV head) against a range of keys, one
 // workgroup per CU (two waves per SIMD).  Each wave owns 32 rows.
 //
-// Per 32-key tile t (two pages):
+// Per 64-key tile t (four pages):
 //   * K(t) and V^T(t) pages are gathered from the pool straight into LDS
 //     (global_load_lds_dwordx4, no staging registers) through a 4-deep ring:
 //     iteration t issues K(t+3) and V(t+2), and waits only for the loads issued
@@ -44,7 +44,8 @@ typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;  // scal
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
 constexpr int kWaves = kAttnThreads / 64;
-constexpr int kBN = 32;  // keys per LDS tile (two pages); split boundaries are multiples of it
+constexpr int kKB = 2;        // 32-key MFMA blocks per LDS tile
+constexpr int kBN = 32 * kKB; // keys per LDS tile; split boundaries are multiples of it
 static_assert(kWaves * 32 == kTileRows, "one 32-row MFMA block per wave");
 static_assert(kTileKeys % kBN == 0, "split boundaries must fall on tile boundaries");
 
@@ -105,10 +106,10 @@ struct Geom {
 // LDS layouts (unpadded, XOR-swizzled so that the MFMA operand reads are free of
 // bank conflicts while every 1 KiB of a tile can be written by one wave-wide
 // direct load):
-//   K tile   [32 keys][D] bf16; 16-byte chunk c of key row r is stored at chunk
+//   K tile   [kBN keys][D] bf16; 16-byte chunk c of key row r is stored at chunk
 //            c ^ (r % CPR) of that row.
-//   V^T tile [2 pages][D dims][16 slots] bf16; 16-byte chunk c (slots 8c..8c+7)
-//            of dim row d is stored at chunk c ^ ((d >> 3) & 1).
+//   V^T tile [kBN/16 pages][D dims][16 slots] bf16; 16-byte chunk c (slots
+//            8c..8c+7) of dim row d is stored at chunk c ^ ((d >> 3) & 1).
 // Load g = it * 8 + wave of a tile pair is K load j = g (g < INSTR) or V load
 // j = g - INSTR; lane l of load j writes bytes [1024 j + 16 l, +16) of its tile.
 //   K: row r = j * (64 / CPR) + l / CPR, stored chunk l % CPR.
@@ -221,67 +222,89 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// S^T of one tile for this wave's 32 rows.
+// Wait until at most `issued` (this iteration's) direct loads are outstanding.
+template <int MAX>
+__device__ __forceinline__ void wait_issued(int issued) {
+  if constexpr (MAX >= 4) { if (issued >= 4) { wait_vmcnt<4>(); return; } }
+  if constexpr (MAX >= 3) { if (issued == 3) { wait_vmcnt<3>(); return; } }
+  if constexpr (MAX >= 2) { if (issued == 2) { wait_vmcnt<2>(); return; } }
+  if (issued == 1) { wait_vmcnt<1>(); return; }
+  wait_vmcnt<0>();
+}
+
+// S^T of one tile for this wave's 32 rows: s[kb] holds keys 32 kb .. 32 kb + 31
+// (the swizzle of a key row depends on the row modulo 16 only, so block kb reads
+// at the same offsets shifted by 32 rows).
 template <int D>
-__device__ __forceinline__ void qk_tile(f32x16& s, const uint8_t* kt, const int (&koff)[Geom<D>::KSTEPS],
+__device__ __forceinline__ void qk_tile(f32x16 (&s)[kKB], const uint8_t* kt, const int (&koff)[Geom<D>::KSTEPS],
                                         const bf16x8 (&qf)[Geom<D>::KSTEPS]) {
   using G = Geom<D>;
-  s = f32x16{};
+#pragma unroll
+  for (int kb = 0; kb < kKB; kb++) s[kb] = f32x16{};
 #pragma unroll
   for (int st = 0; st < G::KSTEPS; st++) {
-    const bf16x8 a = *(const bf16x8*)(kt + koff[st]);
-    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], s, 0, 0, 0);
+#pragma unroll
+    for (int kb = 0; kb < kKB; kb++) {
+      const bf16x8 a = *(const bf16x8*)(kt + kb * 32 * D * 2 + koff[st]);
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], s[kb], 0, 0, 0);
+    }
   }
 }
 
 // Raw row maximum of a tile (optionally causally masked in place), combined over
-// both halves of the wave.  Accumulator i holds key k0 + 16*(i/8) + 8*h + i%8.
+// both halves of the wave.  Accumulator i of block kb holds key
+// k0 + 32 kb + 16 (i/8) + 8 h + i%8.
 template <bool MASK>
-__device__ __forceinline__ float row_max(f32x16& s, int k0, int qpos, int h) {
+__device__ __forceinline__ float row_max(f32x16 (&s)[kKB], int k0, int qpos, int h) {
   float m = -INFINITY;
 #pragma unroll
-  for (int i = 0; i < 16; i++) {
-    float x = s[i];
-    if constexpr (MASK) {
-      const int key = k0 + 16 * (i / 8) + 8 * h + (i % 8);
-      x = key > qpos ? -INFINITY : x;
-      s[i] = x;
+  for (int kb = 0; kb < kKB; kb++) {
+#pragma unroll
+    for (int i = 0; i < 16; i++) {
+      float x = s[kb][i];
+      if constexpr (MASK) {
+        const int key = k0 + 32 * kb + 16 * (i / 8) + 8 * h + (i % 8);
+        x = key > qpos ? -INFINITY : x;
+        s[kb][i] = x;
+      }
+      m = fmaxf(m, x);
     }
-    m = fmaxf(m, x);
   }
   return pair_max(m);
 }
 
 // p = exp2(s * scale - m) as bf16 pairs (the P^T B operands, one per page of the
 // tile); returns the row sum over those bf16 values added to l.
-__device__ __forceinline__ float exp_pack(const f32x16& s, bf16x8 (&pb)[2], float l, float m_run, float scale) {
+__device__ __forceinline__ float exp_pack(const f32x16 (&s)[kKB], bf16x8 (&pb)[2 * kKB], float l, float m_run,
+                                          float scale) {
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   const float neg = -m_run;
 #pragma unroll
-  for (int hf = 0; hf < 2; hf++) {
+  for (int pg = 0; pg < 2 * kKB; pg++) {
     uint32_t w[4];
 #pragma unroll
     for (int e = 0; e < 4; e++) {
-      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * hf + 2 * e], scale, neg));
-      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * hf + 2 * e + 1], scale, neg));
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[pg / 2][8 * (pg % 2) + 2 * e], scale, neg));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[pg / 2][8 * (pg % 2) + 2 * e + 1], scale, neg));
       w[e] = pack_bf16(p0, p1);
       l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, l, false);
     }
-    pb[hf] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+    pb[pg] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
   }
   return l;
 }
 
-// O^T += V^T P^T: page hf of the tile against keys 16*hf .. 16*hf+15.
+// O^T += V^T P^T: page pg of the tile against keys 16 pg .. 16 pg + 15.
 template <int D>
-__device__ __forceinline__ void pv_tile(f32x16 (&o)[Geom<D>::DB], const uint8_t* vt, int vbase, const bf16x8 (&pb)[2]) {
+__device__ __forceinline__ void pv_tile(f32x16 (&o)[Geom<D>::DB], const uint8_t* vt, int vbase,
+                                        const bf16x8 (&pb)[2 * kKB]) {
   using G = Geom<D>;
 #pragma unroll
-  for (int hf = 0; hf < 2; hf++) {
+  for (int pg = 0; pg < 2 * kKB; pg++) {
 #pragma unroll
     for (int b = 0; b < G::DB; b++) {
-      const bf16x8 a = *(const bf16x8*)(vt + hf * (D * 32) + b * 1024 + vbase);
-      o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[hf], o[b], 0, 0, 0);
+      const bf16x8 a = *(const bf16x8*)(vt + pg * (D * 32) + b * 1024 + vbase);
+      o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[pg], o[b], 0, 0, 0);
     }
   }
 }
@@ -437,8 +460,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, slot[it].is_v ? 2 : 3);
   __syncthreads();
 
-  f32x16 sa, sb;
-  bf16x8 pb[2];
+  f32x16 sa[kKB], sb[kKB];
+  bf16x8 pb[2 * kKB];
   qk_tile<D>(sa, k_lds[0], koff, qf);
   mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
 
@@ -447,7 +470,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   // V(t+2) into the ring and waits for K(t+2) and V(t+1), issued one iteration ago.
   // In the unmasked variant tile t+1 exists and needs no mask, so the compute part
   // is one branch-free block in which MFMA and the softmax VALU work interleave.
-  auto iteration = [&](f32x16& s_cur, f32x16& s_nxt, int t, auto masked) {
+  auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked) {
     constexpr bool MASKED = decltype(masked)::value;
     const int k0 = kb0 + t * kBN;
     const bool has_next = MASKED ? t + 1 < n_tiles : true;
@@ -471,56 +494,14 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
       if (has_next) mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
     } else {
-      // Written in issue order: every K fragment of tile t+1 and the first V^T
-      // fragments of tile t are read up front; each S(t+1) MFMA is followed by one
-      // pair of the exp / pack work of tile t; the row maximum of S(t+1) runs
-      // between the O MFMAs.
-      const uint8_t* kt = k_lds[(t + 1) % G::NSTAGE];
-      const uint8_t* vt = v_lds[t % G::NSTAGE];
-      constexpr int VPRE = G::DB;  // V^T fragments read ahead (one page)
-      bf16x8 kf[G::KSTEPS], vf[2 * G::DB];
-#pragma unroll
-      for (int st = 0; st < G::KSTEPS; st++) kf[st] = *(const bf16x8*)(kt + koff[st]);
-#pragma unroll
-      for (int i = 0; i < VPRE; i++) vf[i] = *(const bf16x8*)(vt + (i / G::DB) * (D * 32) + (i % G::DB) * 1024 + vbase);
-      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-      const float neg = -m_run;
-      uint32_t pw[8];
-      s_nxt = f32x16{};
-#pragma unroll
-      for (int st = 0; st < G::KSTEPS; st++) {
-        s_nxt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qf[st], s_nxt, 0, 0, 0);
-#pragma unroll
-        for (int e = st * 8 / G::KSTEPS; e < (st + 1) * 8 / G::KSTEPS; e++) {
-          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[2 * e], scale, neg));
-          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[2 * e + 1], scale, neg));
-          pw[e] = pack_bf16(p0, p1);
-          l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw[e]), ones, l_run, false);
-        }
-      }
-      pb[0] = __builtin_bit_cast(bf16x8, make_uint4(pw[0], pw[1], pw[2], pw[3]));
-      pb[1] = __builtin_bit_cast(bf16x8, make_uint4(pw[4], pw[5], pw[6], pw[7]));
-#pragma unroll
-      for (int i = VPRE; i < 2 * G::DB; i++) vf[i] = *(const bf16x8*)(vt + (i / G::DB) * (D * 32) + (i % G::DB) * 1024 + vbase);
-      float m = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < 2 * G::DB; i++) {
-        o[i % G::DB] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pb[i / G::DB], o[i % G::DB], 0, 0, 0);
-#pragma unroll
-        for (int e = i * 16 / (2 * G::DB); e < (i + 1) * 16 / (2 * G::DB); e++) m = fmaxf(m, s_nxt[e]);
-      }
-      mx = pair_max(m);
+      qk_tile<D>(s_nxt, k_lds[(t + 1) % G::NSTAGE], koff, qf);
+      l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
+      pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
+      mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     }
 
     finish(tk, tv);
-    if constexpr (G::PER_WAVE == 2) {
-      if (issued == 2) wait_vmcnt<2>();
-      else if (issued == 1) wait_vmcnt<1>();
-      else wait_vmcnt<0>();
-    } else {
-      if (issued == 1) wait_vmcnt<1>();
-      else wait_vmcnt<0>();
-    }
+    wait_issued<G::PER_WAVE>(issued);
     __syncthreads();
   };
 
@@ -533,7 +514,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   if (t + 1 < n_full) {
     iteration(sa, sb, t, False{});
     t++;
-    sa = sb;
+#pragma unroll
+    for (int kb = 0; kb < kKB; kb++) sa[kb] = sb[kb];
   }
   for (; t < n_tiles; t += 2) {
     iteration(sa, sb, t, True{});
