@@ -12,8 +12,9 @@
 // Per 64-key tile t (four pages):
 //   * K(t) and V^T(t) pages are gathered from the pool straight into LDS
 //     (global_load_lds_dwordx4, no staging registers) through a 4-deep ring:
-//     iteration t issues K(t+3) and V(t+2), and waits only for the loads issued
-//     one iteration earlier.  Page ids are read with scalar loads.
+//     iteration t issues K(t+4) and V(t+3) and waits only for the loads issued
+//     two iterations earlier, so each load has three iterations to arrive.
+//     Page ids are read with scalar loads, one iteration ahead.
 //   * S^T(t) = K(t) Q^T on v_mfma_f32_32x32x16_bf16: K rows are the A operand
 //     (LDS), the wave's query rows the B operand (registers for the whole unit).
 //     In the result each lane owns one query row and 16 keys of it, so softmax
@@ -222,14 +223,15 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// Wait until at most `issued` (this iteration's) direct loads are outstanding.
-template <int MAX>
-__device__ __forceinline__ void wait_issued(int issued) {
-  if constexpr (MAX >= 4) { if (issued >= 4) { wait_vmcnt<4>(); return; } }
-  if constexpr (MAX >= 3) { if (issued == 3) { wait_vmcnt<3>(); return; } }
-  if constexpr (MAX >= 2) { if (issued == 2) { wait_vmcnt<2>(); return; } }
-  if (issued == 1) { wait_vmcnt<1>(); return; }
-  wait_vmcnt<0>();
+// Wait until at most `n` direct loads (the most recent ones) are outstanding.
+template <int MAX, int N = MAX>
+__device__ __forceinline__ void wait_issued(int n) {
+  if constexpr (N == 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (n >= N) { wait_vmcnt<N>(); return; }
+    wait_issued<MAX, N - 1>(n);
+  }
 }
 
 // S^T of one tile for this wave's 32 rows: s[kb] holds keys 32 kb .. 32 kb + 31
@@ -443,27 +445,32 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
     }
   };
 
-  // ---- prologue: K(0..2), V(0..1) resident; S(0) and its row maximum
+  // ---- prologue: K(0), K(1), V(0) resident; K(2), V(1) and then K(3), V(2) in
+  // flight (they play the loads of iterations -2 and -1); S(0) and its maximum
+  auto tile_or_none = [&](int t) { return t < n_tiles ? t : -1; };
 #pragma unroll
   for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 0);
   issue(0, 0);
   finish(0, 0);
-  issue(n_tiles > 1 ? 1 : -1, n_tiles > 1 ? 1 : -1);
-  finish(1, 1);
 #pragma unroll
-  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 2);
-  issue(n_tiles > 2 ? 2 : -1, -1);
-  finish(2, -1);
+  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 1);
+  issue(tile_or_none(1), -1);
+  finish(tile_or_none(1), -1);
   wait_vmcnt<0>();
-  // page ids of the first loop iteration's tiles: K(3), V(2)
 #pragma unroll
-  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, slot[it].is_v ? 2 : 3);
+  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, slot[it].is_v ? 1 : 2);
+  int issued_prev2 = issue(tile_or_none(2), tile_or_none(1));
+  finish(tile_or_none(2), tile_or_none(1));
+  int issued_prev = issue(tile_or_none(3), tile_or_none(2));  // pid already advanced to K(3), V(2)
+  finish(tile_or_none(3), tile_or_none(2));
+  (void)issued_prev2;
   __syncthreads();
 
   f32x16 sa[kKB], sb[kKB];
   bf16x8 pb[2 * kKB];
   qk_tile<D>(sa, k_lds[0], koff, qf);
   mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
+  __syncthreads();  // every wave has read K(0) before iteration 0 refills its slot with K(4)
 
   // One pipelined iteration: consumes S(t) (scores in s_cur, maximum in mx), produces
   // S(t+1) into s_nxt with its maximum, accumulates P(t) V(t).  Issues K(t+3) and
@@ -474,8 +481,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
     constexpr bool MASKED = decltype(masked)::value;
     const int k0 = kb0 + t * kBN;
     const bool has_next = MASKED ? t + 1 < n_tiles : true;
-    const int tk = t + 3 < n_tiles ? t + 3 : -1;
-    const int tv = t + 2 < n_tiles ? t + 2 : -1;
+    const int tk = t + 4 < n_tiles ? t + 4 : -1;
+    const int tv = t + 3 < n_tiles ? t + 3 : -1;
     const int issued = issue(tk, tv);
 
     // lazy rescale: move the reference maximum only when a row outgrows it by 2^8
@@ -501,7 +508,9 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
     }
 
     finish(tk, tv);
-    wait_issued<G::PER_WAVE>(issued);
+    // K(t+2), V(t+1) (issued two iterations ago) must be in LDS before the barrier
+    wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
+    issued_prev = issued;
     __syncthreads();
   };
 
