@@ -405,8 +405,9 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
 #pragma unroll
   for (int it = 0; it < G::PER_WAVE; it++)
     head_base[it] = (const char*)(slot[it].is_v ? p.v_pool : p.k_pool) + (size_t)kv_head * (kPageSize * D * EBYTES);
+  const int lp0 = (int)((uint32_t)kb0 / kPageSize);
   auto page_for = [&](int it, int t) -> uint32_t {
-    return (uint32_t)page_of(c, (kb0 + t * kBN) / kPageSize + slot[it].page_sel);
+    return (uint32_t)page_of(c, lp0 + t * (kBN / kPageSize) + slot[it].page_sel);
   };
   auto issue = [&](int tk, int tv) -> int {
     int direct = 0;
@@ -431,6 +432,18 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       }
     }
     return direct;
+  };
+  // Steady state (bf16 pool, K(tk) and V(tv) both lie inside [kb0, key_end)): every
+  // piece is a direct load and nothing is conditional.
+  auto issue_whole = [&](int tk, int tv) {
+#pragma unroll
+    for (int it = G::PER_WAVE - 1; it >= 0; it--) {
+      const LoadSlot<D>& s = slot[it];
+      const int t = s.is_v ? tv : tk;
+      uint8_t* tile = s.is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
+      issue_direct<D>(s, page_block(head_base[it], pid[it], page_bytes), tile);
+      pid[it] = page_for(it, t + 1);
+    }
   };
   auto finish = [&](int tk, int tv) {
     if constexpr (FP8) {
@@ -477,13 +490,16 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   // V(t+2) into the ring and waits for K(t+2) and V(t+1), issued one iteration ago.
   // In the unmasked variant tile t+1 exists and needs no mask, so the compute part
   // is one branch-free block in which MFMA and the softmax VALU work interleave.
-  auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked) {
+  auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole) {
     constexpr bool MASKED = decltype(masked)::value;
+    constexpr bool WHOLE = !FP8 && decltype(whole)::value;
     const int k0 = kb0 + t * kBN;
     const bool has_next = MASKED ? t + 1 < n_tiles : true;
-    const int tk = t + 4 < n_tiles ? t + 4 : -1;
-    const int tv = t + 3 < n_tiles ? t + 3 : -1;
-    const int issued = issue(tk, tv);
+    const int tk = WHOLE || t + 4 < n_tiles ? t + 4 : -1;
+    const int tv = WHOLE || t + 3 < n_tiles ? t + 3 : -1;
+    int issued = G::PER_WAVE;
+    if constexpr (WHOLE) issue_whole(tk, tv);
+    else issued = issue(tk, tv);
 
     // lazy rescale: move the reference maximum only when a row outgrows it by 2^8
     if (__any(mx * scale > m_run + kRescaleThreshold)) {
@@ -509,26 +525,36 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
 
     finish(tk, tv);
     // K(t+2), V(t+1) (issued two iterations ago) must be in LDS before the barrier
-    wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
+    if constexpr (WHOLE) wait_vmcnt<2 * G::PER_WAVE>();
+    else wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
     issued_prev = issued;
     __syncthreads();
   };
 
   int t = 0;
-  // unmasked part: S(t+1) needs no mask while t + 1 < n_full
+  // unmasked part: S(t+1) needs no mask while t + 1 < n_full.  While the tiles an
+  // iteration issues (K(t+4), V(t+3)) are whole, the loads are unconditional; the
+  // prologue issued K(3) and V(2) in full whenever that holds for t = 0.
+  if (!FP8) {
+    const int whole_end = (last_whole - 3 < n_tiles - 4 ? last_whole - 3 : n_tiles - 4);
+    for (; t + 2 < n_full && t + 1 < whole_end; t += 2) {
+      iteration(sa, sb, t, False{}, True{});
+      iteration(sb, sa, t + 1, False{}, True{});
+    }
+  }
   for (; t + 2 < n_full; t += 2) {
-    iteration(sa, sb, t, False{});
-    iteration(sb, sa, t + 1, False{});
+    iteration(sa, sb, t, False{}, False{});
+    iteration(sb, sa, t + 1, False{}, False{});
   }
   if (t + 1 < n_full) {
-    iteration(sa, sb, t, False{});
+    iteration(sa, sb, t, False{}, False{});
     t++;
 #pragma unroll
     for (int kb = 0; kb < kKB; kb++) sa[kb] = sb[kb];
   }
   for (; t < n_tiles; t += 2) {
-    iteration(sa, sb, t, True{});
-    if (t + 1 < n_tiles) iteration(sb, sa, t + 1, True{});
+    iteration(sa, sb, t, True{}, False{});
+    if (t + 1 < n_tiles) iteration(sb, sa, t + 1, True{}, False{});
   }
 
   wait_vmcnt<0>();  // no load into this workgroup's LDS may outlive it
