@@ -78,17 +78,14 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-// 8 fp8 e4m3 codes -> 8 bf16 (exact: every e4m3 value is a bf16 value)
+// 8 fp8 e4m3 codes -> 8 bf16, two per instruction with a unit scale (exact: every
+// e4m3 value is a bf16 value)
 __device__ __forceinline__ uint4 fp8x8_to_bf16x8(uint2 c) {
   uint4 r;
-  auto f0 = __builtin_amdgcn_cvt_pk_f32_fp8(c.x, false);
-  auto f1 = __builtin_amdgcn_cvt_pk_f32_fp8(c.x, true);
-  auto f2 = __builtin_amdgcn_cvt_pk_f32_fp8(c.y, false);
-  auto f3 = __builtin_amdgcn_cvt_pk_f32_fp8(c.y, true);
-  r.x = pack_bf16(f0[0], f0[1]);
-  r.y = pack_bf16(f1[0], f1[1]);
-  r.z = pack_bf16(f2[0], f2[1]);
-  r.w = pack_bf16(f3[0], f3[1]);
+  r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c.x, 1.0f, false));
+  r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c.x, 1.0f, true));
+  r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c.y, 1.0f, false));
+  r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c.y, 1.0f, true));
   return r;
 }
 
@@ -100,6 +97,8 @@ struct Geom {
   static constexpr int TILE_BYTES = kBN * D * 2; // bf16 K tile == bf16 V^T tile
   static constexpr int INSTR = TILE_BYTES / 1024;        // 1 KiB direct loads per tile (K or V)
   static constexpr int PER_WAVE = 2 * INSTR / kWaves;    // K and V loads of one wave per iteration
+  static constexpr int K_SLOTS = INSTR / kWaves;         // slots [0, K_SLOTS) load K, the rest V^T
+  static_assert(INSTR % kWaves == 0, "K and V loads must each spread evenly over waves");
   static constexpr int NSTAGE = 4;               // LDS ring depth for K and for V^T
   static_assert((2 * INSTR) % kWaves == 0, "loads must spread evenly over waves");
 };
@@ -118,7 +117,7 @@ struct Geom {
 // Each load falls inside one page.
 
 struct Ctx {
-  const_i32_ptr page_ids;
+  const_i32_ptr page_ids;  // this request's page list
   const void* k_pool;
   const void* v_pool;
   int num_kv_heads;
@@ -133,7 +132,7 @@ struct Ctx {
 // the register path).
 __device__ __forceinline__ int page_of(const Ctx& c, int lp) {
   const int last = (c.key_end - 1) / kPageSize;
-  return c.page_ids[c.page_base + (lp < last ? lp : last)];
+  return c.page_ids[(uint32_t)(lp < last ? lp : last)];
 }
 
 template <int D>
@@ -187,31 +186,19 @@ __device__ __forceinline__ void issue_direct(const LoadSlot<D>& s, const char* b
   lds_dma_16(block, s.off, lds);
 }
 
-// Register path for one piece: fp8 pools (converted to bf16 here) and V tiles
-// holding keys at or past key_end (zeroed here, so that unwritten, possibly NaN,
-// slots never meet a zero weight).  Same LDS layout as the direct loads.
-template <int D, bool FP8>
-__device__ __forceinline__ uint4 load_piece(const LoadSlot<D>& s, const char* block, const Ctx& c, int k0) {
-  constexpr int EB = FP8 ? 1 : 2;
-  const char* src = block + s.off / 2 * EB;
-  uint4 x;
-  if constexpr (FP8) x = fp8x8_to_bf16x8(*(const uint2*)src);
-  else x = *(const uint4*)src;
-  if (k0 + kBN > c.key_end) {
-    const int elem = s.off / 2;  // element offset inside the page block
-    if (s.is_v) {
-      const int key = k0 + s.page_sel * kPageSize + (elem % kPageSize);
-      uint32_t* xw = (uint32_t*)&x;
+// Zero the bf16 V^T values of one piece whose keys lie at or past key_end (the
+// piece holds slots elem % 16 .. +7 of page page_sel of the tile at key k0), so
+// that unwritten, possibly NaN, slots never meet a zero weight.  Keys past key_end
+// in K need nothing: their scores are masked.
+template <int D>
+__device__ __forceinline__ uint4 mask_v_tail(uint4 x, const LoadSlot<D>& s, int k0, int key_end) {
+  const int key = k0 + s.page_sel * kPageSize + (s.off / 2) % kPageSize;
+  uint32_t* xw = (uint32_t*)&x;
 #pragma unroll
-      for (int e = 0; e < 4; e++) {
-        const uint32_t lo = (key + 2 * e < c.key_end) ? 0xFFFFu : 0u;
-        const uint32_t hi = (key + 2 * e + 1 < c.key_end) ? 0xFFFF0000u : 0u;
-        xw[e] &= (lo | hi);
-      }
-    } else {
-      const int key = k0 + s.page_sel * kPageSize + elem / D;
-      if (key >= c.key_end) x = make_uint4(0, 0, 0, 0);
-    }
+  for (int e = 0; e < 4; e++) {
+    const uint32_t lo = (key + 2 * e < key_end) ? 0xFFFFu : 0u;
+    const uint32_t hi = (key + 2 * e + 1 < key_end) ? 0xFFFF0000u : 0u;
+    xw[e] &= (lo | hi);
   }
   return x;
 }
@@ -338,7 +325,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   const int h = lane >> 5;  // half of the wave
   const int kv_head = u.head_ntok >> 16;
   const int ntok = u.head_ntok & 0xFFFF;
-  const Ctx c{(const_i32_ptr)p.page_ids, p.k_pool, p.v_pool, p.num_kv_heads, u.page_base, u.key_end, kv_head};
+  const Ctx c{(const_i32_ptr)p.page_ids + u.page_base, p.k_pool, p.v_pool, p.num_kv_heads, u.page_base, u.key_end,
+              kv_head};
 
   // this lane's query row: row rho = token * group + head-in-group
   const int rho = wave * 32 + n;
@@ -392,19 +380,22 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   // bf16 pool: direct loads, except for a V tile reaching past key_end, which is
   // loaded, zeroed and written synchronously (V pieces go first, so that wait only
   // covers older loads).  Returns the direct loads issued.
-  // fp8 pool: every piece goes through registers (converted to bf16); finish()
-  // writes them to LDS after the compute block.  Tile indices are clamped so that
-  // the register loads are unconditional.
-  uint4 regs[G::PER_WAVE];
-  // per slot: the pool base of this KV head, and the page id of the tile the slot
-  // loads next (read one iteration ahead, so the scalar load is off the critical path)
+  // fp8 pool: every piece is loaded as 8 raw codes into registers (`fresh`); they
+  // are converted to bf16 and written to the ring at the end of the next iteration
+  // (`held`), so each load has a whole iteration to arrive.
+  // Per slot: the pool base of this KV head, and the page id of the tile the slot
+  // loads next (read one iteration ahead, so the scalar load is off the critical path).
   constexpr int EBYTES = FP8 ? 1 : 2;
   const uint32_t page_bytes = (uint32_t)p.num_kv_heads * (kPageSize * D * EBYTES);
   const char* head_base[G::PER_WAVE];
   uint32_t pid[G::PER_WAVE];
+  uint2 fresh[G::PER_WAVE], held[G::PER_WAVE];
+  int held_tk = -1, held_tv = -1;
 #pragma unroll
-  for (int it = 0; it < G::PER_WAVE; it++)
-    head_base[it] = (const char*)(slot[it].is_v ? p.v_pool : p.k_pool) + (size_t)kv_head * (kPageSize * D * EBYTES);
+  for (int it = 0; it < G::PER_WAVE; it++) {
+    head_base[it] = (const char*)(it >= G::K_SLOTS ? p.v_pool : p.k_pool) + (size_t)kv_head * (kPageSize * D * EBYTES);
+    fresh[it] = held[it] = make_uint2(0, 0);
+  }
   const int lp0 = (int)((uint32_t)kb0 / kPageSize);
   auto page_for = [&](int it, int t) -> uint32_t {
     return (uint32_t)page_of(c, lp0 + t * (kBN / kPageSize) + slot[it].page_sel);
@@ -414,69 +405,98 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
 #pragma unroll
     for (int it = G::PER_WAVE - 1; it >= 0; it--) {
       const LoadSlot<D>& s = slot[it];
-      const int t = s.is_v ? tv : tk;
+      const bool is_v = it >= G::K_SLOTS;
+      const int t = is_v ? tv : tk;
+      if (t < 0) continue;
+      const char* block = page_block(head_base[it], pid[it], page_bytes);
       if constexpr (FP8) {
-        const int tt = t < 0 ? 0 : t;
-        regs[it] = load_piece<D, true>(s, page_block(head_base[it], page_for(it, tt), page_bytes), c, kb0 + tt * kBN);
+        fresh[it] = *(const uint2*)(block + s.off / 2);
       } else {
-        if (t < 0) continue;
-        uint8_t* tile = s.is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
-        const char* block = page_block(head_base[it], pid[it], page_bytes);
-        if (s.is_v && t >= last_whole) {
-          *(uint4*)(tile + s.j * 1024 + lane * 16) = load_piece<D, false>(s, block, c, kb0 + t * kBN);
+        uint8_t* tile = is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
+        if (is_v && t >= last_whole) {
+          *(uint4*)(tile + s.j * 1024 + lane * 16) = mask_v_tail<D>(*(const uint4*)(block + s.off), s, kb0 + t * kBN, u.key_end);
         } else {
           issue_direct<D>(s, block, tile);
           direct++;
         }
-        pid[it] = page_for(it, t + 1);  // next iteration's tile for this slot
       }
+      pid[it] = page_for(it, t + 1);  // next iteration's tile for this slot
     }
     return direct;
   };
-  // Steady state (bf16 pool, K(tk) and V(tv) both lie inside [kb0, key_end)): every
-  // piece is a direct load and nothing is conditional.
+  // Steady state (K(tk) and V(tv) both lie inside [kb0, key_end)): nothing is
+  // conditional.
   auto issue_whole = [&](int tk, int tv) {
 #pragma unroll
     for (int it = G::PER_WAVE - 1; it >= 0; it--) {
       const LoadSlot<D>& s = slot[it];
-      const int t = s.is_v ? tv : tk;
-      uint8_t* tile = s.is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
-      issue_direct<D>(s, page_block(head_base[it], pid[it], page_bytes), tile);
+      const bool is_v = it >= G::K_SLOTS;
+      const int t = is_v ? tv : tk;
+      const char* block = page_block(head_base[it], pid[it], page_bytes);
+      if constexpr (FP8) {
+        fresh[it] = *(const uint2*)(block + s.off / 2);
+      } else {
+        issue_direct<D>(s, block, is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE]);
+      }
       pid[it] = page_for(it, t + 1);
     }
   };
-  auto finish = [&](int tk, int tv) {
-    if constexpr (FP8) {
+  // fp8: convert the codes in `codes` for K(tk), V(tv) and write them to the ring.
+  auto store_codes = [&](const uint2 (&codes)[G::PER_WAVE], int tk, int tv, auto whole) {
+    constexpr bool WHOLE = decltype(whole)::value;
 #pragma unroll
-      for (int it = 0; it < G::PER_WAVE; it++) {
-        const LoadSlot<D>& s = slot[it];
-        const int t = s.is_v ? tv : tk;
-        if (t < 0) continue;
-        uint8_t* tile = s.is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
-        *(uint4*)(tile + s.j * 1024 + lane * 16) = regs[it];
-      }
+    for (int it = 0; it < G::PER_WAVE; it++) {
+      const bool is_v = it >= G::K_SLOTS;
+      const int t = is_v ? tv : tk;
+      if (!WHOLE && t < 0) continue;
+      uint4 x = fp8x8_to_bf16x8(codes[it]);
+      if (!WHOLE && is_v && t >= last_whole) x = mask_v_tail<D>(x, slot[it], kb0 + t * kBN, u.key_end);
+      uint8_t* tile = is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
+      *(uint4*)(tile + slot[it].j * 1024 + lane * 16) = x;
+    }
+  };
+  // end of an iteration that issued K(tk), V(tv): the fp8 codes held since the
+  // previous iteration go to the ring, this iteration's become the held ones
+  auto finish = [&](int tk, int tv, auto whole) {
+    if constexpr (FP8) {
+      store_codes(held, held_tk, held_tv, whole);
+#pragma unroll
+      for (int it = 0; it < G::PER_WAVE; it++) held[it] = fresh[it];
+      held_tk = tk;
+      held_tv = tv;
     }
   };
 
-  // ---- prologue: K(0), K(1), V(0) resident; K(2), V(1) and then K(3), V(2) in
-  // flight (they play the loads of iterations -2 and -1); S(0) and its maximum
+  // ---- prologue.  bf16: K(0), K(1), V(0) resident; K(2), V(1) and then K(3), V(2)
+  // in flight (they play the loads of iterations -2 and -1).  fp8: K(0..2), V(0..1)
+  // resident, the codes of K(3), V(2) held.
   auto tile_or_none = [&](int t) { return t < n_tiles ? t : -1; };
+  int issued_prev = 0;
 #pragma unroll
   for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 0);
-  issue(0, 0);
-  finish(0, 0);
+  if constexpr (FP8) {
+    issue(0, 0);
+    store_codes(fresh, 0, 0, False{});
+    issue(tile_or_none(1), tile_or_none(1));
+    store_codes(fresh, tile_or_none(1), tile_or_none(1), False{});
+    issue(tile_or_none(2), -1);
+    store_codes(fresh, tile_or_none(2), -1, False{});
+    issue(tile_or_none(3), tile_or_none(2));
+    held_tk = tile_or_none(3);
+    held_tv = tile_or_none(2);
 #pragma unroll
-  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 1);
-  issue(tile_or_none(1), -1);
-  finish(tile_or_none(1), -1);
-  wait_vmcnt<0>();
+    for (int it = 0; it < G::PER_WAVE; it++) held[it] = fresh[it];
+  } else {
+    issue(0, 0);
 #pragma unroll
-  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, slot[it].is_v ? 1 : 2);
-  int issued_prev2 = issue(tile_or_none(2), tile_or_none(1));
-  finish(tile_or_none(2), tile_or_none(1));
-  int issued_prev = issue(tile_or_none(3), tile_or_none(2));  // pid already advanced to K(3), V(2)
-  finish(tile_or_none(3), tile_or_none(2));
-  (void)issued_prev2;
+    for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 1);
+    issue(tile_or_none(1), -1);
+    wait_vmcnt<0>();
+#pragma unroll
+    for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, it >= G::K_SLOTS ? 1 : 2);
+    issue(tile_or_none(2), tile_or_none(1));
+    issued_prev = issue(tile_or_none(3), tile_or_none(2));  // pid already advanced to K(3), V(2)
+  }
   __syncthreads();
 
   f32x16 sa[kKB], sb[kKB];
@@ -492,7 +512,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   // is one branch-free block in which MFMA and the softmax VALU work interleave.
   auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole) {
     constexpr bool MASKED = decltype(masked)::value;
-    constexpr bool WHOLE = !FP8 && decltype(whole)::value;
+    constexpr bool WHOLE = decltype(whole)::value;
     const int k0 = kb0 + t * kBN;
     const bool has_next = MASKED ? t + 1 < n_tiles : true;
     const int tk = WHOLE || t + 4 < n_tiles ? t + 4 : -1;
@@ -523,11 +543,14 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     }
 
-    finish(tk, tv);
-    // K(t+2), V(t+1) (issued two iterations ago) must be in LDS before the barrier
-    if constexpr (WHOLE) wait_vmcnt<2 * G::PER_WAVE>();
-    else wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
-    issued_prev = issued;
+    if constexpr (FP8) {
+      finish(tk, tv, whole);
+    } else {
+      // K(t+2), V(t+1) (issued two iterations ago) must be in LDS before the barrier
+      if constexpr (WHOLE) wait_vmcnt<2 * G::PER_WAVE>();
+      else wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
+      issued_prev = issued;
+    }
     __syncthreads();
   };
 
@@ -535,7 +558,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   // unmasked part: S(t+1) needs no mask while t + 1 < n_full.  While the tiles an
   // iteration issues (K(t+4), V(t+3)) are whole, the loads are unconditional; the
   // prologue issued K(3) and V(2) in full whenever that holds for t = 0.
-  if (!FP8) {
+  {
     const int whole_end = (last_whole - 3 < n_tiles - 4 ? last_whole - 3 : n_tiles - 4);
     for (; t + 2 < n_full && t + 1 < whole_end; t += 2) {
       iteration(sa, sb, t, False{}, True{});
