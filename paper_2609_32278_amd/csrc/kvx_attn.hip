@@ -12,9 +12,13 @@
 // Per 64-key tile t (four pages):
 //   * K(t) and V^T(t) pages are gathered from the pool straight into LDS
 //     (global_load_lds_dwordx4, no staging registers) through a 4-deep ring:
-//     iteration t issues K(t+4) and V(t+3) and waits only for the loads issued
-//     two iterations earlier, so each load has three iterations to arrive.
-//     Page ids are read with scalar loads, one iteration ahead.
+//     iteration t issues K(t+4) and V(t+3) -- one load per wave after every
+//     quarter of the S(t+1) product, so the loads of a CU trickle into the
+//     address units instead of arriving as one burst -- and waits only for the
+//     loads issued two iterations earlier, so each load has three iterations to
+//     arrive.  Page ids are read with scalar loads one iteration ahead, after the
+//     iteration's last LDS operand read (an outstanding scalar load would make
+//     every LDS wait a full drain).
 //   * S^T(t) = K(t) Q^T on v_mfma_f32_32x32x16_bf16: K rows are the A operand
 //     (LDS), the wave's query rows the B operand (registers for the whole unit).
 //     In the result each lane owns one query row and 16 keys of it, so softmax
@@ -224,10 +228,13 @@ __device__ __forceinline__ void wait_issued(int n) {
 // S^T of one tile for this wave's 32 rows: s[kb] holds keys 32 kb .. 32 kb + 31
 // (the swizzle of a key row depends on the row modulo 16 only, so block kb reads
 // at the same offsets shifted by 32 rows).
-template <int D>
+// between(i) runs after k-step group i of the PER_WAVE groups (used to spread
+// this wave's loads of later tiles over the product).
+template <int D, typename F>
 __device__ __forceinline__ void qk_tile(f32x16 (&s)[kKB], const uint8_t* kt, const int (&koff)[Geom<D>::KSTEPS],
-                                        const bf16x8 (&qf)[Geom<D>::KSTEPS]) {
+                                        const bf16x8 (&qf)[Geom<D>::KSTEPS], F&& between) {
   using G = Geom<D>;
+  constexpr int STEP = G::KSTEPS / G::PER_WAVE;
 #pragma unroll
   for (int kb = 0; kb < kKB; kb++) s[kb] = f32x16{};
 #pragma unroll
@@ -237,7 +244,14 @@ __device__ __forceinline__ void qk_tile(f32x16 (&s)[kKB], const uint8_t* kt, con
       const bf16x8 a = *(const bf16x8*)(kt + kb * 32 * D * 2 + koff[st]);
       s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], s[kb], 0, 0, 0);
     }
+    if ((st + 1) % STEP == 0) between((st + 1) / STEP - 1);
   }
+}
+
+template <int D>
+__device__ __forceinline__ void qk_tile(f32x16 (&s)[kKB], const uint8_t* kt, const int (&koff)[Geom<D>::KSTEPS],
+                                        const bf16x8 (&qf)[Geom<D>::KSTEPS]) {
+  qk_tile<D>(s, kt, koff, qf, [](int) {});
 }
 
 // Raw row maximum of a tile (optionally causally masked in place), combined over
@@ -518,8 +532,16 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
     const int tk = WHOLE || t + 4 < n_tiles ? t + 4 : -1;
     const int tv = WHOLE || t + 3 < n_tiles ? t + 3 : -1;
     int issued = G::PER_WAVE;
-    if constexpr (WHOLE) issue_whole(tk, tv);
-    else issued = issue(tk, tv);
+    constexpr bool SPREAD = WHOLE && !FP8 && !MASKED;  // bf16 steady state
+    const char* blk[G::PER_WAVE];
+    if constexpr (SPREAD) {
+#pragma unroll
+      for (int it = 0; it < G::PER_WAVE; it++) blk[it] = page_block(head_base[it], pid[it], page_bytes);
+    } else if constexpr (WHOLE) {
+      issue_whole(tk, tv);
+    } else {
+      issued = issue(tk, tv);
+    }
 
     // lazy rescale: move the reference maximum only when a row outgrows it by 2^8
     if (__any(mx * scale > m_run + kRescaleThreshold)) {
@@ -536,6 +558,16 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
       pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
       if (has_next) mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
+    } else if constexpr (SPREAD) {
+      qk_tile<D>(s_nxt, k_lds[(t + 1) % G::NSTAGE], koff, qf, [&](int i) {
+        const int it = G::PER_WAVE - 1 - i;
+        const bool is_v = it >= G::K_SLOTS;
+        const int tt = is_v ? tv : tk;
+        issue_direct<D>(slot[it], blk[it], is_v ? v_lds[tt % G::NSTAGE] : k_lds[tt % G::NSTAGE]);
+      });
+      l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
+      pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
+      mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     } else {
       qk_tile<D>(s_nxt, k_lds[(t + 1) % G::NSTAGE], koff, qf);
       l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
@@ -543,6 +575,12 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     }
 
+    if constexpr (SPREAD) {
+      // next page ids, read after this iteration's last LDS operand read so that no
+      // operand wait has to cover an outstanding scalar load
+#pragma unroll
+      for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, (it >= G::K_SLOTS ? tv : tk) + 1);
+    }
     if constexpr (FP8) {
       finish(tk, tv, whole);
     } else {
