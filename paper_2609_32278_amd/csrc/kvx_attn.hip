@@ -524,6 +524,20 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   // V(t+2) into the ring and waits for K(t+2) and V(t+1), issued one iteration ago.
   // In the unmasked variant tile t+1 exists and needs no mask, so the compute part
   // is one branch-free block in which MFMA and the softmax VALU work interleave.
+  // lazy rescale before the scores of the tile whose maximum is mx are exponentiated:
+  // the reference maximum moves only when a row outgrows it by 2^8
+  auto rescale = [&]() {
+    if (__any(mx * scale > m_run + kRescaleThreshold)) {
+      const float m_new = fmaxf(m_run, mx * scale);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < G::DB; b++) o[b] *= alpha;
+      m_run = m_new;
+    }
+  };
+  if constexpr (FP8) rescale();
+
   auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole) {
     constexpr bool MASKED = decltype(masked)::value;
     constexpr bool WHOLE = decltype(whole)::value;
@@ -532,7 +546,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
     const int tk = WHOLE || t + 4 < n_tiles ? t + 4 : -1;
     const int tv = WHOLE || t + 3 < n_tiles ? t + 3 : -1;
     int issued = G::PER_WAVE;
-    constexpr bool SPREAD = WHOLE && !FP8 && !MASKED;  // bf16 steady state
+    constexpr bool SPREAD = WHOLE && !MASKED;  // steady state
     const char* blk[G::PER_WAVE];
     if constexpr (SPREAD) {
 #pragma unroll
@@ -543,15 +557,9 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       issued = issue(tk, tv);
     }
 
-    // lazy rescale: move the reference maximum only when a row outgrows it by 2^8
-    if (__any(mx * scale > m_run + kRescaleThreshold)) {
-      const float m_new = fmaxf(m_run, mx * scale);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int b = 0; b < G::DB; b++) o[b] *= alpha;
-      m_run = m_new;
-    }
+    // bf16 pool: the check for S(t) comes here; the fp8 kernel, tighter on
+    // registers, takes it at the end of the previous iteration instead
+    if constexpr (!FP8) rescale();
 
     if constexpr (MASKED) {
       if (has_next) qk_tile<D>(s_nxt, k_lds[(t + 1) % G::NSTAGE], koff, qf);
@@ -563,7 +571,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
         const int it = G::PER_WAVE - 1 - i;
         const bool is_v = it >= G::K_SLOTS;
         const int tt = is_v ? tv : tk;
-        issue_direct<D>(slot[it], blk[it], is_v ? v_lds[tt % G::NSTAGE] : k_lds[tt % G::NSTAGE]);
+        if constexpr (FP8) fresh[it] = *(const uint2*)(blk[it] + slot[it].off / 2);
+        else issue_direct<D>(slot[it], blk[it], is_v ? v_lds[tt % G::NSTAGE] : k_lds[tt % G::NSTAGE]);
       });
       l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
       pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
@@ -575,6 +584,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     }
 
+    if constexpr (FP8) rescale();  // for S(t+1), exponentiated in the next iteration
     if constexpr (SPREAD) {
       // next page ids, read after this iteration's last LDS operand read so that no
       // operand wait has to cover an outstanding scalar load
