@@ -1,0 +1,128 @@
+/*
+ * kvx_cache.h -- host-side prefix cache for multi-turn agents over the kvx page
+ * pool: per-agent cached histories, page allocation, and eviction by round-robin
+ * tail chunks (paper Section 3.2, Algorithm 1) or by least-recent leaf nodes (the
+ * LRU baseline of Sections 3.1 and 4).
+ *
+ * The model.  Every agent (trajectory) owns a private cached history: the first
+ * `cached` tokens of its context, held in whole pages of the pool (no sharing
+ * between agents, as in the analysis of Section 3.3).  Each finished turn adds one
+ * node to the agent's path: the full pages its prompt added to the cache.  A turn
+ * start and a turn end both stamp every node of the agent's path with the current
+ * logical time, so one agent's nodes always share one time stamp (the recency
+ * synchronization of Section 3.1).  While a turn runs the agent is active and its
+ * pages are pinned; between turns it is idle and its pages may be evicted.
+ *
+ * Eviction reclaims the pages a turn start needs beyond the free ones:
+ *   KVX_EVICT_LRU  repeatedly drops the whole leaf node with the oldest time stamp
+ *                  among idle agents (ties: smaller agent id); removing a leaf
+ *                  exposes its parent.
+ *   KVX_EVICT_RR   Algorithm 1: the idle agents holding pages form one queue in
+ *                  agent-id order, starting after the agent that lost the last
+ *                  chunk of any earlier reclamation (the round robin continues
+ *                  across reclamations).  The front agent loses one tail chunk:
+ *                  min(chunk, pages of its leaf node, pages still to reclaim)
+ *                  pages from the end of its leaf; it goes to the back of the
+ *                  queue while it holds pages.  Eligibility (idle, non-empty) is
+ *                  rechecked at every pop.
+ * Completion signals (Section 3.2, "Handling stale agent trajectories") are
+ * kvx_cache_complete: the agent's pages are freed at once.
+ *
+ * Conventions: every call is synchronous host code, returns KVX_OK or a
+ * kvx_status code from kvx.h (kvx_last_error() describes the failure), and is not
+ * thread-safe for one cache (callers serialize calls on a cache).  Page ids are
+ * indices into a kvx pool of the same num_pages; the cache never touches the pool's
+ * memory.  A cache is owned by the library until kvx_cache_destroy.
+ */
+#ifndef KVX_CACHE_H
+#define KVX_CACHE_H
+
+#include <stdint.h>
+
+#include "kvx.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct kvx_cache kvx_cache; /* opaque; owned by the library */
+
+enum kvx_evict_policy {
+    KVX_EVICT_LRU = 0, /* whole least-recent leaf nodes */
+    KVX_EVICT_RR = 1   /* round-robin tail chunks (Algorithm 1) */
+};
+
+typedef struct {
+    int64_t num_pages;      /* pool pages managed */
+    int64_t free_pages;     /* pages owned by nobody */
+    int64_t cached_pages;   /* pages of idle and active agents' cached histories */
+    int64_t turn_pages;     /* pages allocated to running turns beyond their cached prefix */
+    int64_t evicted_pages;  /* pages reclaimed by eviction since creation */
+    int64_t evictions;      /* eviction steps (LRU nodes or RR chunks) since creation */
+    int32_t agents;         /* agents known to the cache */
+    int32_t active_agents;  /* agents inside a turn */
+} kvx_cache_counters;
+
+/*
+ * Create a cache over `num_pages` pages of `page_size` tokens.
+ *   page_size     16 (the pool's page size).
+ *   chunk_tokens  RR tail-chunk size in tokens, a positive multiple of page_size
+ *                 (the paper evaluates 1024); ignored by LRU but still checked.
+ *   policy        KVX_EVICT_LRU or KVX_EVICT_RR.
+ * Errors: EINVAL (sizes, policy, out NULL), EUNSUPPORTED (page_size), ENOMEM.
+ */
+int kvx_cache_create(int64_t num_pages, int32_t page_size, int32_t chunk_tokens, int32_t policy,
+                     kvx_cache **out);
+
+/* Free a cache.  NULL is a no-op. */
+int kvx_cache_destroy(kvx_cache *cache);
+
+/*
+ * Start a turn of `agent` (any id; an unknown agent starts with nothing cached)
+ * whose prompt is `prompt_len` >= 1 tokens: its context so far, then the new
+ * input.  The reused prefix is the cached history capped at the last whole page
+ * before the prompt's final token (a turn always computes at least one token):
+ *   *prefix_len = min(cached, page_size * floor((prompt_len - 1) / page_size)).
+ * Cached pages past *prefix_len are dropped.  The pages for tokens
+ * [*prefix_len, prompt_len) are then allocated, evicting idle agents' pages per
+ * the policy when too few are free.  On success page_ids[0 .. n) with
+ * n = ceil(prompt_len / page_size) holds the turn's page table (logical page j ->
+ * physical page), ready for store_kv / extend_attention with P = *prefix_len and
+ * E = prompt_len - *prefix_len, and the agent is active.
+ *   page_ids, cap  host buffer of cap >= n entries (checked before any change).
+ * Errors: EINVAL (agent already active, prompt_len < 1, cap, NULL pointers),
+ * ENOMEM (not enough pages even after evicting every idle page: the pages
+ * evicted so far stay evicted, the agent stays idle with its prefix).
+ */
+int kvx_cache_begin_turn(kvx_cache *cache, int64_t agent, int32_t prompt_len, int32_t *prefix_len,
+                         int32_t *page_ids, int64_t cap);
+
+/*
+ * End the running turn of `agent`: the prompt's whole pages stay cached as the
+ * agent's history (a new node holding the pages this turn added), its partial
+ * last page is freed, and the agent becomes idle.  Errors: EINVAL (not active).
+ */
+int kvx_cache_end_turn(kvx_cache *cache, int64_t agent);
+
+/*
+ * Completion signal: free every page of an idle `agent` and forget it.
+ * Errors: EINVAL (unknown or active agent).
+ */
+int kvx_cache_complete(kvx_cache *cache, int64_t agent);
+
+/*
+ * Cached history of `agent` in tokens (0 for an unknown agent) and, if `page_ids`
+ * is non-NULL, its pages in logical order (at most `cap` written).  For tests and
+ * tools.  Errors: EINVAL.
+ */
+int kvx_cache_agent(const kvx_cache *cache, int64_t agent, int32_t *cached_tokens, int32_t *page_ids,
+                    int64_t cap);
+
+/* Counters of the cache.  Errors: EINVAL. */
+int kvx_cache_stats(const kvx_cache *cache, kvx_cache_counters *out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVX_CACHE_H */

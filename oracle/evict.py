@@ -1,0 +1,174 @@
+"""CPU oracle of the prefix cache's eviction policies -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/`` may import this module.  Plain Python, written from the paper,
+sharing no code with the library's cache (``kvx_cache.cpp``):
+
+* round-robin tail eviction follows Algorithm 1 (Section 3.2) step by step:
+  one queue of idle trajectories with evictable suffixes, pop the front,
+  recheck eligibility, evict one tail chunk (SelectTailChunk), push the
+  trajectory back while it still holds an evictable suffix, until enough is
+  freed or the queue is empty;
+* the LRU baseline (Section 3.1) drops the whole leaf node with the oldest
+  access time among idle trajectories, which exposes the parent as a new leaf;
+* completion signals (Section 3.2, stale trajectories) free an agent at once.
+
+Sizes are counted in pages; no physical page ids are tracked (which page a
+policy hands out is the library's choice, and tests check it separately).
+
+Readings where the paper leaves the backend open (the same ones the library
+takes; each is listed in the design doc):
+
+1. A trajectory is one agent's private history; nothing is shared between
+   agents (the analysis of Section 3.3 assumes no sharing).
+2. Each finished turn adds one node: the whole pages its prompt added.  Turn
+   start and turn end both stamp every node of the agent's path with the
+   current logical time (matching and inserting touch the whole path).
+3. A turn of P tokens reuses min(cached, 16 * floor((P - 1) / 16)) tokens: whole
+   pages, and at least one prompt token is computed.  Cached pages past that
+   are dropped; the prompt's partial last page is not kept after the turn.
+4. SelectTailChunk(tau, M - M_freed) = the last min(chunk, leaf pages,
+   M - M_freed) pages of tau's leaf node (a suffix of one leaf, never more than
+   is still needed).
+5. The queue of each reclamation lists idle agents in agent-id order, starting
+   after the agent that lost the previous chunk, so the rotation continues from
+   one reclamation to the next.
+6. LRU ties (equal stamps cannot happen with a strictly increasing clock) would
+   go to the smaller agent id.
+"""
+
+from __future__ import annotations
+
+from collections import deque
+
+
+class NoMemory(Exception):
+    """Active demand exceeds the capacity even after evicting every idle page."""
+
+
+class _Agent:
+    def __init__(self) -> None:
+        self.nodes: list[int] = []  # pages per node, root .. leaf
+        self.active = False
+        self.stamp = 0
+        self.prompt_len = 0
+        self.turn_pages = 0
+
+    @property
+    def pages(self) -> int:
+        return sum(self.nodes)
+
+
+class OracleCache:
+    LRU = 0
+    RR = 1
+
+    def __init__(self, num_pages: int, page_size: int, chunk_tokens: int, policy: int) -> None:
+        assert page_size == 16 and chunk_tokens % page_size == 0 and chunk_tokens > 0
+        self.num_pages = num_pages
+        self.page_size = page_size
+        self.chunk = chunk_tokens // page_size
+        self.policy = policy
+        self.free = num_pages
+        self.agents: dict[int, _Agent] = {}
+        self.clock = 0
+        self.rr_last = None
+        self.evicted_pages = 0
+        self.evictions = 0
+
+    # -- helpers -------------------------------------------------------------
+    def _drop_tail(self, a: _Agent, n: int) -> None:
+        while n > 0:
+            k = min(n, a.nodes[-1])
+            a.nodes[-1] -= k
+            if a.nodes[-1] == 0:
+                a.nodes.pop()
+            self.free += k
+            n -= k
+
+    def _evictable(self, agent_id: int) -> bool:
+        a = self.agents.get(agent_id)
+        return a is not None and not a.active and a.pages > 0
+
+    # -- Algorithm 1 ---------------------------------------------------------
+    def _reclaim_rr(self, M: int) -> None:
+        ids = sorted(i for i in self.agents if self._evictable(i))
+        if self.rr_last is None:
+            order = ids
+        else:
+            order = [i for i in ids if i > self.rr_last] + [i for i in ids if i <= self.rr_last]
+        Q = deque(order)
+        freed = 0
+        while freed < M and Q:
+            tau = Q.popleft()
+            if not self._evictable(tau):  # active, or no evictable suffix
+                continue
+            a = self.agents[tau]
+            c = min(self.chunk, a.nodes[-1], M - freed)  # SelectTailChunk(tau, M - M_freed)
+            self._drop_tail(a, c)  # Evict(c)
+            freed += c
+            self.evicted_pages += c
+            self.evictions += 1
+            self.rr_last = tau
+            if self._evictable(tau):
+                Q.append(tau)
+
+    # -- LRU baseline ----------------------------------------------------------
+    def _reclaim_lru(self, M: int) -> None:
+        freed = 0
+        while freed < M:
+            leaves = [(self.agents[i].stamp, i) for i in self.agents if self._evictable(i)]
+            if not leaves:
+                return
+            _, victim = min(leaves)
+            a = self.agents[victim]
+            n = a.nodes[-1]
+            self._drop_tail(a, n)
+            freed += n
+            self.evicted_pages += n
+            self.evictions += 1
+
+    # -- turns -----------------------------------------------------------------
+    def begin_turn(self, agent_id: int, prompt_len: int) -> int:
+        assert prompt_len >= 1
+        a = self.agents.setdefault(agent_id, _Agent())
+        assert not a.active
+        self.clock += 1
+        a.stamp = self.clock
+        reuse = min(a.pages, (prompt_len - 1) // self.page_size)
+        self._drop_tail(a, a.pages - reuse)
+        need = -(-prompt_len // self.page_size) - reuse
+        a.active = True
+        if self.free < need:
+            if self.policy == self.RR:
+                self._reclaim_rr(need - self.free)
+            else:
+                self._reclaim_lru(need - self.free)
+        if self.free < need:
+            a.active = False
+            raise NoMemory(agent_id)
+        self.free -= need
+        a.turn_pages = need
+        a.prompt_len = prompt_len
+        return reuse * self.page_size
+
+    def end_turn(self, agent_id: int) -> None:
+        a = self.agents[agent_id]
+        assert a.active
+        whole = a.prompt_len // self.page_size - a.pages
+        self.free += a.turn_pages - whole
+        if whole > 0:
+            a.nodes.append(whole)
+        a.turn_pages = 0
+        a.active = False
+        self.clock += 1
+        a.stamp = self.clock
+
+    def complete(self, agent_id: int) -> None:
+        a = self.agents[agent_id]
+        assert not a.active
+        self._drop_tail(a, a.pages)
+        del self.agents[agent_id]
+
+    def cached_tokens(self, agent_id: int) -> int:
+        a = self.agents.get(agent_id)
+        return 0 if a is None else a.pages * self.page_size

@@ -1,0 +1,213 @@
+"""Replay a synthetic multi-agent workload through the prefix cache and the hot path.
+
+Every scheduler tick, the agents whose idle time has run out start their next
+turn: the cache (include/kvx_cache.h) reuses what is left of each agent's history,
+evicts idle agents' pages by the chosen policy when the pool runs short, and
+returns the turn's page table.  The tick's starting turns form one prefix-extend
+batch: store_kv writes their uncached suffix K/V into the pool and
+extend_attention computes the suffix rows (paper Sections 1 and 2).  A turn then
+decodes for a few ticks (its pages pinned), ends, and the agent idles for its
+tool / user latency; an agent that finishes its last turn sends the completion
+signal (Section 3.2).
+
+The figures this produces are the paper's: uncached prompt tokens per returning
+turn (Section 4) and, with the GPU, the time of each batch's KV store + attention.
+
+    python -m paper_2609_32278_amd.agent_replay --policy both --agents 48 --turns 8
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import sys
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import kvx
+from . import workloads as wl
+
+POLICIES = {"lru": kvx.KVX_EVICT_LRU, "rr": kvx.KVX_EVICT_RR}
+
+
+@dataclass
+class TurnRecord:
+    agent: int
+    turn: int
+    tick: int
+    prompt: int        # tokens of the turn's prompt
+    prefix: int        # tokens reused from the cache
+    history: int       # tokens of context the agent had before this turn
+
+    @property
+    def uncached(self) -> int:
+        return self.prompt - self.prefix
+
+    @property
+    def recomputed_history(self) -> int:
+        """Old-prefix recomputation (the X of Section 3.3, in tokens)."""
+        return self.history - min(self.prefix, self.history)
+
+
+@dataclass
+class ReplayResult:
+    policy: str
+    turns: list = field(default_factory=list)
+    events: list = field(default_factory=list)   # ("begin", agent, prompt, prefix | None), ("end", a), ("complete", a)
+    batch_ms: list = field(default_factory=list)
+    stats: dict = field(default_factory=dict)
+
+    def summary(self) -> dict:
+        back = [t for t in self.turns if t.turn > 0]
+        u = np.array([t.uncached for t in back], dtype=np.float64)
+        x = np.array([t.recomputed_history / max(t.history, 1) for t in back], dtype=np.float64)
+        out = {
+            "policy": self.policy,
+            "turns": len(self.turns),
+            "returning_turns": len(back),
+            "uncached_tokens_total": int(sum(t.uncached for t in self.turns)),
+        }
+        if len(back):
+            out.update({
+                "uncached_p50": float(np.percentile(u, 50)),
+                "uncached_p90": float(np.percentile(u, 90)),
+                "uncached_p99": float(np.percentile(u, 99)),
+                "uncached_max": float(u.max()),
+                "uncached_mean": float(u.mean()),
+                "history_recomputed_mean": float(x.mean()),
+                "history_recomputed_p99": float(np.percentile(x, 99)),
+                "full_misses": int(sum(1 for t in back if t.prefix == 0)),
+            })
+        if self.batch_ms:
+            b = np.array(self.batch_ms)
+            out.update({"batches": len(b), "prefill_ms_total": float(b.sum()),
+                        "prefill_ms_p50": float(np.percentile(b, 50)), "prefill_ms_p99": float(np.percentile(b, 99))})
+        out["cache"] = self.stats
+        return out
+
+
+def replay(tr: wl.AgentTrace, policy: str, num_pages: int, *, chunk_tokens: int = 1024, decode_ticks: int = 2,
+           completion_signals: bool = True, gpu: bool = True, on_batch=None, max_ticks: int = 1_000_000) -> ReplayResult:
+    """Run the trace; `on_batch(requests, q, out)` sees each GPU batch (requests:
+    list of TurnRecord, q / out: the batch's [rows, Hq, d] tensors)."""
+    res = ReplayResult(policy)
+    cache = kvx.kvx_cache_create(num_pages, wl.PAGE_SIZE, chunk_tokens, POLICIES[policy])
+    pool = None
+    torch = None
+    if gpu:
+        import torch  # noqa: F811  (device memory and streams only)
+        pool = kvx.kv_pool_create(num_pages, wl.PAGE_SIZE, tr.num_kv_heads, tr.head_dim)
+    n = tr.num_agents
+    turns = len(tr.new[0])
+    ctx = [0] * n
+    turn = [0] * n
+    due = list(tr.start)          # tick at which the next turn may start
+    running_until = [-1] * n      # tick at which the running turn ends, -1 = idle
+    done = [False] * n
+    try:
+        tick = 0
+        while not all(done):
+            if tick > max_ticks:
+                raise RuntimeError("replay did not finish (capacity below the active demand?)")
+            for a in range(n):
+                if running_until[a] == tick:
+                    kvx.kvx_cache_end_turn(cache, a)
+                    res.events.append(("end", a))
+                    running_until[a] = -1
+                    ctx[a] += tr.reply[a][turn[a]]
+                    due[a] = tick + tr.idle[a][turn[a]]
+                    turn[a] += 1
+                    if turn[a] == turns:
+                        done[a] = True
+                        if completion_signals:
+                            kvx.kvx_cache_complete(cache, a)
+                            res.events.append(("complete", a))
+            batch = []
+            for a in range(n):
+                if done[a] or running_until[a] >= 0 or due[a] > tick:
+                    continue
+                prompt = ctx[a] + tr.new[a][turn[a]]
+                try:
+                    prefix, table = kvx.kvx_cache_begin_turn(cache, a, prompt)
+                except kvx.KvxError as e:
+                    if e.status != kvx.KVX_ENOMEM:
+                        raise
+                    res.events.append(("begin", a, prompt, None))
+                    continue  # waits for pages to free up
+                res.events.append(("begin", a, prompt, prefix))
+                rec = TurnRecord(a, turn[a], tick, prompt, prefix, ctx[a])
+                res.turns.append(rec)
+                batch.append((rec, table))
+                running_until[a] = tick + decode_ticks
+                ctx[a] = prompt
+            if batch and gpu:
+                res.batch_ms.append(_run_batch(tr, pool, batch, on_batch, torch))
+            tick += 1
+        res.stats = kvx.kvx_cache_stats(cache)
+    finally:
+        kvx.kvx_cache_destroy(cache)
+        if pool is not None:
+            kvx.kv_pool_destroy(pool)
+    return res
+
+
+def _run_batch(tr, pool, batch, on_batch, torch) -> float:
+    dev = "cuda"
+    P = np.array([r.prefix for r, _ in batch], np.int32)
+    E = np.array([r.uncached for r, _ in batch], np.int32)
+    indptr = np.zeros(len(batch) + 1, np.int32)
+    indptr[1:] = np.cumsum([len(t) for _, t in batch])
+    ids = torch.from_numpy(np.concatenate([t for _, t in batch]).astype(np.int32)).to(dev)
+    b = kvx.Batch(P, E, indptr, ids.data_ptr())
+    k_ext, v_ext, q = [], [], []
+    for r, _ in batch:
+        k, v = wl.agent_kv(tr, r.agent, r.prompt, dev)
+        k_ext.append(k[r.prefix:])
+        v_ext.append(v[r.prefix:])
+        q.append(wl.agent_q(tr, r.agent, r.turn, r.uncached, dev))
+    k_ext = torch.cat(k_ext).contiguous()
+    v_ext = torch.cat(v_ext).contiguous()
+    q = torch.cat(q).contiguous()
+    out = torch.empty_like(q)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    kvx.store_kv(pool, b, k_ext, v_ext)
+    kvx.extend_attention(pool, b, q, tr.num_q_heads, tr.sm_scale, out)
+    e1.record(stream)
+    e1.synchronize()
+    if on_batch is not None:
+        on_batch([r for r, _ in batch], q, out)
+    return e0.elapsed_time(e1)
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--policy", choices=["lru", "rr", "both"], default="both")
+    ap.add_argument("--agents", type=int, default=48)
+    ap.add_argument("--turns", type=int, default=8)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--capacity", type=float, default=0.5,
+                    help="pool size as a fraction of the summed final contexts of all agents")
+    ap.add_argument("--chunk-tokens", type=int, default=1024)
+    ap.add_argument("--decode-ticks", type=int, default=2)
+    ap.add_argument("--heads", default="32,8,128", help="Hq,Hkv,head_dim")
+    ap.add_argument("--no-gpu", action="store_true")
+    args = ap.parse_args(argv)
+    hq, hkv, d = (int(x) for x in args.heads.split(","))
+    tr = wl.make_agent_trace(args.agents, args.turns, seed=args.seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d)
+    total = sum(tr.max_context(i) for i in range(tr.num_agents))
+    num_pages = int(args.capacity * total) // wl.PAGE_SIZE
+    for pol in (["lru", "rr"] if args.policy == "both" else [args.policy]):
+        r = replay(tr, pol, num_pages, chunk_tokens=args.chunk_tokens, decode_ticks=args.decode_ticks,
+                   gpu=not args.no_gpu)
+        s = r.summary()
+        s.update({"agents": args.agents, "turns_per_agent": args.turns, "num_pages": num_pages,
+                  "context_tokens_total": total, "heads": [hq, hkv, d], "chunk_tokens": args.chunk_tokens})
+        print(json.dumps(s), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

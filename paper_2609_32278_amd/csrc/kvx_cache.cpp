@@ -1,0 +1,268 @@
+// Host-side prefix cache for multi-turn agents: page allocation over a kvx pool
+// and eviction of idle agents' histories, either by round-robin tail chunks
+// (paper Section 3.2, Algorithm 1) or by least-recent whole leaf nodes (the LRU
+// baseline, Section 3.1).  The C ABI and the model are declared in
+// include/kvx_cache.h.
+
+#include <algorithm>
+#include <deque>
+#include <limits>
+#include <map>
+#include <new>
+#include <vector>
+
+#include "kvx_cache.h"
+#include "kvx_internal.h"
+
+namespace {
+
+struct CacheNode {
+  std::vector<int32_t> pages;  // logical order
+};
+
+struct CacheAgent {
+  std::vector<CacheNode> nodes;  // root .. leaf; never empty nodes
+  int64_t pages = 0;             // cached pages (sum over nodes)
+  int64_t stamp = 0;             // time stamp shared by every node of the path
+  bool active = false;
+  int32_t prompt_len = 0;        // running turn
+  std::vector<int32_t> turn;     // pages allocated to the running turn
+};
+
+}  // namespace
+
+struct kvx_cache {
+  int64_t num_pages = 0;
+  int32_t page_size = 0;
+  int32_t chunk_pages = 0;
+  int32_t policy = 0;
+  std::vector<int32_t> free_pages;       // stack; the next page handed out is at the back
+  std::map<int64_t, CacheAgent> agents;  // ordered by id: the round-robin order
+  int64_t clock = 0;
+  bool rr_has_last = false;
+  int64_t rr_last = 0;  // agent that lost the last RR chunk
+  int64_t evicted_pages = 0;
+  int64_t evictions = 0;
+};
+
+namespace {
+
+using kvx::report;
+
+void release_pages(kvx_cache* c, const int32_t* p, size_t n) {
+  for (size_t i = n; i-- > 0;) c->free_pages.push_back(p[i]);
+}
+
+// Drop the last `n` cached pages of an agent (n <= agent pages), leaf first.
+void drop_tail(kvx_cache* c, CacheAgent& a, int64_t n) {
+  while (n > 0) {
+    CacheNode& leaf = a.nodes.back();
+    const int64_t k = std::min<int64_t>(n, (int64_t)leaf.pages.size());
+    const size_t keep = leaf.pages.size() - (size_t)k;
+    release_pages(c, leaf.pages.data() + keep, (size_t)k);
+    leaf.pages.resize(keep);
+    if (leaf.pages.empty()) a.nodes.pop_back();
+    a.pages -= k;
+    n -= k;
+  }
+}
+
+// LRU: whole leaf nodes, oldest time stamp first (ties: smaller id), idle agents only.
+int64_t evict_lru(kvx_cache* c, int64_t need) {
+  int64_t freed = 0;
+  while (freed < need) {
+    CacheAgent* best = nullptr;
+    for (auto& kv : c->agents) {
+      CacheAgent& a = kv.second;
+      if (a.active || a.nodes.empty()) continue;
+      if (best == nullptr || a.stamp < best->stamp) best = &a;  // map order breaks ties by id
+    }
+    if (best == nullptr) break;
+    const int64_t n = (int64_t)best->nodes.back().pages.size();
+    drop_tail(c, *best, n);
+    freed += n;
+    c->evicted_pages += n;
+    c->evictions++;
+  }
+  return freed;
+}
+
+// Algorithm 1: one queue of idle agents with evictable pages, in id order starting
+// after the agent that lost the previous chunk; one tail chunk per visit.
+int64_t evict_rr(kvx_cache* c, int64_t need) {
+  std::deque<int64_t> q;
+  auto start = c->rr_has_last ? c->agents.upper_bound(c->rr_last) : c->agents.begin();
+  for (auto it = start; it != c->agents.end(); ++it)
+    if (!it->second.active && it->second.pages > 0) q.push_back(it->first);
+  for (auto it = c->agents.begin(); it != start; ++it)
+    if (!it->second.active && it->second.pages > 0) q.push_back(it->first);
+  int64_t freed = 0;
+  while (freed < need && !q.empty()) {
+    const int64_t id = q.front();
+    q.pop_front();
+    auto it = c->agents.find(id);
+    if (it == c->agents.end()) continue;
+    CacheAgent& a = it->second;
+    if (a.active || a.pages == 0) continue;  // eligibility rechecked at every pop
+    // SelectTailChunk: a suffix of the leaf node, at most one chunk and at most
+    // what is still to be reclaimed
+    const int64_t n = std::min<int64_t>({(int64_t)c->chunk_pages, (int64_t)a.nodes.back().pages.size(),
+                                         need - freed});
+    drop_tail(c, a, n);
+    freed += n;
+    c->evicted_pages += n;
+    c->evictions++;
+    c->rr_has_last = true;
+    c->rr_last = id;
+    if (a.pages > 0) q.push_back(id);
+  }
+  return freed;
+}
+
+int64_t div_up(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+extern "C" {
+
+int kvx_cache_create(int64_t num_pages, int32_t page_size, int32_t chunk_tokens, int32_t policy,
+                     kvx_cache** out) {
+  if (out == nullptr) return report(KVX_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (num_pages <= 0 || num_pages > (int64_t)std::numeric_limits<int32_t>::max())
+    return report(KVX_EINVAL, "num_pages = %lld must be in [1, 2^31-1]", (long long)num_pages);
+  if (page_size != kvx::kPageSize) return report(KVX_EUNSUPPORTED, "page_size %d (supported: 16)", page_size);
+  if (chunk_tokens <= 0 || chunk_tokens % page_size != 0)
+    return report(KVX_EINVAL, "chunk_tokens = %d must be a positive multiple of %d", chunk_tokens, page_size);
+  if (policy != KVX_EVICT_LRU && policy != KVX_EVICT_RR) return report(KVX_EINVAL, "policy %d", policy);
+  kvx_cache* c = new (std::nothrow) kvx_cache();
+  if (c == nullptr) return report(KVX_ENOMEM, "cache allocation failed");
+  try {
+    c->free_pages.resize((size_t)num_pages);
+  } catch (...) {
+    delete c;
+    return report(KVX_ENOMEM, "free list of %lld pages", (long long)num_pages);
+  }
+  for (int64_t i = 0; i < num_pages; i++) c->free_pages[(size_t)i] = (int32_t)(num_pages - 1 - i);  // page 0 first
+  c->num_pages = num_pages;
+  c->page_size = page_size;
+  c->chunk_pages = chunk_tokens / page_size;
+  c->policy = policy;
+  *out = c;
+  return KVX_OK;
+}
+
+int kvx_cache_destroy(kvx_cache* c) {
+  delete c;
+  return KVX_OK;
+}
+
+int kvx_cache_begin_turn(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_t* prefix_len, int32_t* page_ids,
+                         int64_t cap) {
+  if (c == nullptr || prefix_len == nullptr || page_ids == nullptr)
+    return report(KVX_EINVAL, "cache, prefix_len and page_ids must be non-NULL");
+  if (prompt_len < 1) return report(KVX_EINVAL, "prompt_len = %d must be >= 1", prompt_len);
+  const int64_t S = c->page_size;
+  const int64_t n_total = div_up(prompt_len, S);
+  if (cap < n_total) return report(KVX_EINVAL, "page_ids holds %lld entries, the prompt needs %lld", (long long)cap,
+                                   (long long)n_total);
+  auto found = c->agents.find(agent);
+  if (found != c->agents.end() && found->second.active)
+    return report(KVX_EINVAL, "agent %lld is already inside a turn", (long long)agent);
+  CacheAgent& a = c->agents[agent];
+  a.stamp = ++c->clock;  // matching the prefix touches every node of the path
+  const int64_t reuse_pages = std::min<int64_t>(a.pages, (prompt_len - 1) / S);
+  if (a.pages > reuse_pages) drop_tail(c, a, a.pages - reuse_pages);
+  const int64_t need = n_total - reuse_pages;
+  a.active = true;  // pinned while this turn allocates
+  if ((int64_t)c->free_pages.size() < need) {
+    const int64_t want = need - (int64_t)c->free_pages.size();
+    if (c->policy == KVX_EVICT_RR) evict_rr(c, want);
+    else evict_lru(c, want);
+  }
+  if ((int64_t)c->free_pages.size() < need) {
+    a.active = false;
+    return report(KVX_ENOMEM, "agent %lld: %lld pages needed, %lld free after evicting every idle page",
+                  (long long)agent, (long long)need, (long long)c->free_pages.size());
+  }
+  a.turn.clear();
+  a.turn.reserve((size_t)need);
+  for (int64_t i = 0; i < need; i++) {
+    a.turn.push_back(c->free_pages.back());
+    c->free_pages.pop_back();
+  }
+  a.prompt_len = prompt_len;
+  int64_t j = 0;
+  for (const CacheNode& nd : a.nodes)
+    for (int32_t pg : nd.pages) page_ids[j++] = pg;
+  for (int32_t pg : a.turn) page_ids[j++] = pg;
+  *prefix_len = (int32_t)(reuse_pages * S);
+  return KVX_OK;
+}
+
+int kvx_cache_end_turn(kvx_cache* c, int64_t agent) {
+  if (c == nullptr) return report(KVX_EINVAL, "cache is NULL");
+  auto it = c->agents.find(agent);
+  if (it == c->agents.end() || !it->second.active)
+    return report(KVX_EINVAL, "agent %lld is not inside a turn", (long long)agent);
+  CacheAgent& a = it->second;
+  // whole pages of the prompt stay cached; a partial last page is freed
+  const int64_t full = a.prompt_len / c->page_size - a.pages;  // whole pages added by this turn
+  CacheNode nd;
+  nd.pages.assign(a.turn.begin(), a.turn.begin() + full);
+  if ((size_t)full < a.turn.size()) release_pages(c, a.turn.data() + full, a.turn.size() - (size_t)full);
+  if (!nd.pages.empty()) {
+    a.pages += (int64_t)nd.pages.size();
+    a.nodes.push_back(std::move(nd));
+  }
+  a.turn.clear();
+  a.active = false;
+  a.stamp = ++c->clock;  // inserting the turn's pages touches the whole path
+  return KVX_OK;
+}
+
+int kvx_cache_complete(kvx_cache* c, int64_t agent) {
+  if (c == nullptr) return report(KVX_EINVAL, "cache is NULL");
+  auto it = c->agents.find(agent);
+  if (it == c->agents.end()) return report(KVX_EINVAL, "agent %lld is unknown", (long long)agent);
+  if (it->second.active) return report(KVX_EINVAL, "agent %lld is inside a turn", (long long)agent);
+  drop_tail(c, it->second, it->second.pages);
+  c->agents.erase(it);
+  return KVX_OK;
+}
+
+int kvx_cache_agent(const kvx_cache* c, int64_t agent, int32_t* cached_tokens, int32_t* page_ids, int64_t cap) {
+  if (c == nullptr || cached_tokens == nullptr) return report(KVX_EINVAL, "cache and cached_tokens must be non-NULL");
+  auto it = c->agents.find(agent);
+  if (it == c->agents.end()) {
+    *cached_tokens = 0;
+    return KVX_OK;
+  }
+  *cached_tokens = (int32_t)(it->second.pages * c->page_size);
+  if (page_ids != nullptr) {
+    int64_t j = 0;
+    for (const CacheNode& nd : it->second.nodes)
+      for (int32_t pg : nd.pages)
+        if (j < cap) page_ids[j++] = pg;
+  }
+  return KVX_OK;
+}
+
+int kvx_cache_stats(const kvx_cache* c, kvx_cache_counters* out) {
+  if (c == nullptr || out == nullptr) return report(KVX_EINVAL, "cache and out must be non-NULL");
+  kvx_cache_counters s{};
+  s.num_pages = c->num_pages;
+  s.free_pages = (int64_t)c->free_pages.size();
+  for (const auto& kv : c->agents) {
+    s.cached_pages += kv.second.pages;
+    s.turn_pages += (int64_t)kv.second.turn.size();
+    if (kv.second.active) s.active_agents++;
+  }
+  s.agents = (int32_t)c->agents.size();
+  s.evicted_pages = c->evicted_pages;
+  s.evictions = c->evictions;
+  *out = s;
+  return KVX_OK;
+}
+
+}  // extern "C"

@@ -34,6 +34,20 @@ int fail(int code, const char* fmt, ...) {
   return code;
 }
 
+}  // namespace
+
+int kvx::report(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+namespace {
+
 int hip_fail(hipError_t e, const char* what) {
   return fail(e == hipErrorOutOfMemory ? KVX_ENOMEM : KVX_EHIP, "%s: %s", what, hipGetErrorString(e));
 }

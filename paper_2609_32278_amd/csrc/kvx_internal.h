@@ -96,6 +96,9 @@ struct PageIoParams {
   int32_t to_pool;          // 1: write pages into the pool, 0: read them out
 };
 
+// Record a failure for kvx_last_error() and return `code` (host code of any file).
+int report(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+
 hipError_t launch_extend_attention(const AttnParams& p, int64_t n_units, int head_dim, bool fp8,
                                    hipStream_t stream);
 hipError_t launch_merge(const MergeParams& p, int64_t n_merges, int head_dim, hipStream_t stream);

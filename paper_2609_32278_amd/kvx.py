@@ -23,10 +23,14 @@ KVX_KV_BF16, KVX_KV_FP8_E4M3 = 0, 1
 STATUS_NAMES = {0: "KVX_OK", 1: "KVX_EINVAL", 2: "KVX_ENOMEM", 3: "KVX_ERANGE",
                 4: "KVX_EUNSUPPORTED", 5: "KVX_EHIP"}
 
-# Every symbol include/kvx.h declares.
+KVX_EVICT_LRU, KVX_EVICT_RR = 0, 1
+
+# Every symbol include/kvx.h and include/kvx_cache.h declare.
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_layout", "kv_pool_write_pages",
            "kv_pool_read_pages", "store_kv", "extend_attention", "extend_attention_plan",
-           "kvx_set_split_keys", "kvx_last_error"]
+           "kvx_set_split_keys", "kvx_last_error",
+           "kvx_cache_create", "kvx_cache_destroy", "kvx_cache_begin_turn", "kvx_cache_end_turn",
+           "kvx_cache_complete", "kvx_cache_agent", "kvx_cache_stats"]
 
 
 class KvxNotBuilt(ImportError):
@@ -63,6 +67,12 @@ class kvx_work_item(ctypes.Structure):
 
 WORK_ITEM_DTYPE = np.dtype([(n, np.int32) for n, _ in kvx_work_item._fields_])
 
+
+class kvx_cache_stats_t(ctypes.Structure):
+    _fields_ = [("num_pages", ctypes.c_int64), ("free_pages", ctypes.c_int64), ("cached_pages", ctypes.c_int64),
+                ("turn_pages", ctypes.c_int64), ("evicted_pages", ctypes.c_int64), ("evictions", ctypes.c_int64),
+                ("agents", ctypes.c_int32), ("active_agents", ctypes.c_int32)]
+
 _lib = None
 
 
@@ -84,6 +94,13 @@ def lib():
             "extend_attention": [P, ctypes.POINTER(kvx_batch), P, i32, f32, P, P, P],
             "extend_attention_plan": [ctypes.POINTER(kvx_batch), i32, i32, i32, P, i64, ctypes.POINTER(i64)],
             "kvx_set_split_keys": [i32],
+            "kvx_cache_create": [i64, i32, i32, i32, ctypes.POINTER(P)],
+            "kvx_cache_destroy": [P],
+            "kvx_cache_begin_turn": [P, i64, i32, ctypes.POINTER(i32), P, i64],
+            "kvx_cache_end_turn": [P, i64],
+            "kvx_cache_complete": [P, i64],
+            "kvx_cache_agent": [P, i64, ctypes.POINTER(i32), P, i64],
+            "kvx_cache_stats": [P, ctypes.POINTER(kvx_cache_stats_t)],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -205,3 +222,48 @@ def extend_attention_plan(batch: Batch, num_q_heads: int, num_kv_heads: int, hea
 
 def kvx_set_split_keys(keys: int) -> None:
     _check(lib().kvx_set_split_keys(int(keys)), "kvx_set_split_keys")
+
+
+# ------------------------------------------------------------------ prefix cache (include/kvx_cache.h)
+
+def kvx_cache_create(num_pages: int, page_size: int = 16, chunk_tokens: int = 1024, policy: int = KVX_EVICT_RR):
+    out = ctypes.c_void_p()
+    _check(lib().kvx_cache_create(int(num_pages), page_size, chunk_tokens, policy, ctypes.byref(out)),
+           "kvx_cache_create")
+    return out
+
+
+def kvx_cache_destroy(cache) -> None:
+    _check(lib().kvx_cache_destroy(cache), "kvx_cache_destroy")
+
+
+def kvx_cache_begin_turn(cache, agent: int, prompt_len: int):
+    """Returns (prefix_len, page_ids int32 array of ceil(prompt_len / 16) entries)."""
+    ids = np.zeros(max(1, -(-int(prompt_len) // 16)), np.int32)
+    prefix = ctypes.c_int32()
+    _check(lib().kvx_cache_begin_turn(cache, int(agent), int(prompt_len), ctypes.byref(prefix), ids.ctypes.data,
+                                      ids.size), "kvx_cache_begin_turn")
+    return prefix.value, ids
+
+
+def kvx_cache_end_turn(cache, agent: int) -> None:
+    _check(lib().kvx_cache_end_turn(cache, int(agent)), "kvx_cache_end_turn")
+
+
+def kvx_cache_complete(cache, agent: int) -> None:
+    _check(lib().kvx_cache_complete(cache, int(agent)), "kvx_cache_complete")
+
+
+def kvx_cache_agent(cache, agent: int):
+    """Returns (cached_tokens, page_ids of the cached history)."""
+    tok = ctypes.c_int32()
+    _check(lib().kvx_cache_agent(cache, int(agent), ctypes.byref(tok), None, 0), "kvx_cache_agent")
+    ids = np.zeros(tok.value // 16, np.int32)
+    _check(lib().kvx_cache_agent(cache, int(agent), ctypes.byref(tok), ids.ctypes.data, ids.size), "kvx_cache_agent")
+    return tok.value, ids
+
+
+def kvx_cache_stats(cache) -> dict:
+    st = kvx_cache_stats_t()
+    _check(lib().kvx_cache_stats(cache, ctypes.byref(st)), "kvx_cache_stats")
+    return {n: getattr(st, n) for n, _ in st._fields_}

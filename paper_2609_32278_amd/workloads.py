@@ -343,3 +343,68 @@ def sample_rows(w: Workload, per_req: int, seed: int = 0, reqs: Optional[Sequenc
             chosen.add(int(rng.integers(0, e)))
         out.extend((r, i) for i in sorted(chosen))
     return np.array(out, dtype=np.int32).reshape(-1, 2)
+
+
+# ----------------------------------------------------------------------------- agents
+
+AGENT_CONFIG_ID = 7  # seed domain of the multi-agent traces below
+
+
+@dataclasses.dataclass
+class AgentTrace:
+    """A synthetic multi-turn agent workload (stand-in for replayed agent traces,
+    Section 4): agent i starts at tick start[i]; turn k appends new[i][k] tokens
+    (user input or tool output) to its context, its reply adds reply[i][k] tokens,
+    and it then waits idle[i][k] ticks (tool or user latency) before the next turn."""
+    seed: int
+    start: list
+    new: list
+    reply: list
+    idle: list
+    num_q_heads: int = 8
+    num_kv_heads: int = 2
+    head_dim: int = 64
+    sigma: float = 1.0
+
+    @property
+    def num_agents(self) -> int:
+        return len(self.start)
+
+    def max_context(self, i: int) -> int:
+        return int(sum(self.new[i]) + sum(self.reply[i]))
+
+    @property
+    def sm_scale(self) -> float:
+        return 1.0 / math.sqrt(self.head_dim)
+
+
+def make_agent_trace(num_agents: int, turns: int, *, seed: int = 0, first=(2048, 8192), new=(64, 1024),
+                     reply=(32, 256), idle=(1, 8), spread: int = 8, num_q_heads: int = 8, num_kv_heads: int = 2,
+                     head_dim: int = 64) -> AgentTrace:
+    """Lengths only: integer uniforms (inclusive) from default_rng([7, 0, seed])."""
+    rng = np.random.default_rng([AGENT_CONFIG_ID, 0, seed])
+    start = rng.integers(0, spread + 1, num_agents).tolist()
+    news, replies, idles = [], [], []
+    for _ in range(num_agents):
+        n = rng.integers(new[0], new[1] + 1, turns)
+        n[0] = rng.integers(first[0], first[1] + 1)  # the first prompt carries the task
+        news.append(n.tolist())
+        replies.append(rng.integers(reply[0], reply[1] + 1, turns).tolist())
+        idles.append(rng.integers(idle[0], idle[1] + 1, turns).tolist())
+    return AgentTrace(seed, start, news, replies, idles, num_q_heads, num_kv_heads, head_dim)
+
+
+def agent_kv(tr: AgentTrace, agent: int, length: int, device="cpu"):
+    """The logical K and V of an agent's context (positions 0 .. length-1): bf16
+    [length, Hkv, d].  A position's values never change between turns, so a
+    recomputed suffix writes the same K/V its evicted copy held."""
+    shape = (tr.max_context(agent), tr.num_kv_heads, tr.head_dim)
+    k = _randn_bf16(shape, tr.sigma, _torch_seed(AGENT_CONFIG_ID, 1, tr.seed, 1, agent), device)
+    v = _randn_bf16(shape, tr.sigma, _torch_seed(AGENT_CONFIG_ID, 1, tr.seed, 2, agent), device)
+    return k[:length], v[:length]
+
+
+def agent_q(tr: AgentTrace, agent: int, turn: int, rows: int, device="cpu") -> torch.Tensor:
+    """Queries of the uncached rows of one turn: bf16 [rows, Hq, d]."""
+    return _randn_bf16((rows, tr.num_q_heads, tr.head_dim), tr.sigma,
+                       _torch_seed(AGENT_CONFIG_ID, 1, tr.seed, 0, agent * 4096 + turn), device)

@@ -1,0 +1,211 @@
+"""The library's prefix cache (include/kvx_cache.h) against the eviction oracle on
+random multi-agent traces: identical reuse decisions, cached histories and
+counters after every call; page tables that are valid, disjoint and stable."""
+
+import os
+
+import numpy as np
+import pytest
+
+from oracle.evict import NoMemory, OracleCache
+from paper_2609_32278_amd import kvx
+
+PAGE = 16
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    if not os.path.exists(kvx.LIB_PATH):
+        from paper_2609_32278_amd import build
+        build.build()
+
+
+def _err(fn, *a):
+    with pytest.raises(kvx.KvxError) as e:
+        fn(*a)
+    return e.value.status
+
+
+def test_argument_errors():
+    assert _err(kvx.kvx_cache_create, 0, 16, 1024, kvx.KVX_EVICT_RR) == kvx.KVX_EINVAL
+    assert _err(kvx.kvx_cache_create, 64, 8, 1024, kvx.KVX_EVICT_RR) == kvx.KVX_EUNSUPPORTED
+    assert _err(kvx.kvx_cache_create, 64, 16, 24, kvx.KVX_EVICT_RR) == kvx.KVX_EINVAL
+    assert _err(kvx.kvx_cache_create, 64, 16, 1024, 5) == kvx.KVX_EINVAL
+    c = kvx.kvx_cache_create(64, 16, 64, kvx.KVX_EVICT_RR)
+    try:
+        assert _err(kvx.kvx_cache_begin_turn, c, 1, 0) == kvx.KVX_EINVAL
+        assert _err(kvx.kvx_cache_end_turn, c, 1) == kvx.KVX_EINVAL      # not inside a turn
+        assert _err(kvx.kvx_cache_complete, c, 1) == kvx.KVX_EINVAL      # unknown
+        kvx.kvx_cache_begin_turn(c, 1, 40)
+        assert _err(kvx.kvx_cache_begin_turn, c, 1, 50) == kvx.KVX_EINVAL  # already active
+        assert _err(kvx.kvx_cache_complete, c, 1) == kvx.KVX_EINVAL      # active
+        ids = np.zeros(2, np.int32)
+        prefix = kvx.ctypes.c_int32()
+        st = kvx.lib().kvx_cache_begin_turn(c, 2, 100, kvx.ctypes.byref(prefix), ids.ctypes.data, 2)
+        assert st == kvx.KVX_EINVAL                                       # page_ids too short
+        assert kvx.kvx_cache_stats(c)["agents"] == 1                      # checked before any change
+        assert _err(kvx.kvx_cache_begin_turn, c, 3, 65 * PAGE) == kvx.KVX_ENOMEM
+    finally:
+        kvx.kvx_cache_destroy(c)
+
+
+class _Pair:
+    """The library cache and the oracle, driven in lockstep."""
+
+    def __init__(self, num_pages, chunk_tokens, policy):
+        self.c = kvx.kvx_cache_create(num_pages, PAGE, chunk_tokens, policy)
+        self.o = OracleCache(num_pages, PAGE, chunk_tokens, OracleCache.RR if policy == kvx.KVX_EVICT_RR
+                             else OracleCache.LRU)
+        self.num_pages = num_pages
+        self.tables = {}  # active agent -> page table of its running turn
+
+    def close(self):
+        kvx.kvx_cache_destroy(self.c)
+
+    def begin(self, agent, prompt):
+        cached_before, pages_before = kvx.kvx_cache_agent(self.c, agent)
+        try:
+            want = self.o.begin_turn(agent, prompt)
+        except NoMemory:
+            want = None
+        if want is None:
+            with pytest.raises(kvx.KvxError) as e:
+                kvx.kvx_cache_begin_turn(self.c, agent, prompt)
+            assert e.value.status == kvx.KVX_ENOMEM
+            return None
+        prefix, table = kvx.kvx_cache_begin_turn(self.c, agent, prompt)
+        assert prefix == want
+        assert len(table) == -(-prompt // PAGE)
+        # the reused prefix keeps its physical pages
+        assert (table[: prefix // PAGE] == pages_before[: prefix // PAGE]).all()
+        self.tables[agent] = table
+        return prefix
+
+    def end(self, agent):
+        self.o.end_turn(agent)
+        kvx.kvx_cache_end_turn(self.c, agent)
+        table = self.tables.pop(agent)
+        cached, pages = kvx.kvx_cache_agent(self.c, agent)
+        assert (pages == table[: cached // PAGE]).all()  # the turn's whole pages stay, in order
+
+    def complete(self, agent):
+        self.o.complete(agent)
+        kvx.kvx_cache_complete(self.c, agent)
+
+    def check(self):
+        st = kvx.kvx_cache_stats(self.c)
+        assert st["free_pages"] == self.o.free
+        assert st["evicted_pages"] == self.o.evicted_pages
+        assert st["evictions"] == self.o.evictions
+        assert st["agents"] == len(self.o.agents)
+        owned = []
+        for a in self.o.agents:
+            cached, pages = kvx.kvx_cache_agent(self.c, a)
+            assert cached == self.o.cached_tokens(a)
+            owned.extend(pages.tolist())
+        for a, t in self.tables.items():
+            cached, _ = kvx.kvx_cache_agent(self.c, a)
+            owned.extend(t[cached // PAGE:].tolist())  # the running turn's fresh pages
+        assert len(owned) == len(set(owned)), "a page is owned twice"
+        assert all(0 <= p < self.num_pages for p in owned)
+        assert len(owned) + st["free_pages"] == self.num_pages
+
+
+def _trace(seed, policy, n_agents, num_pages, chunk_tokens, steps):
+    rng = np.random.default_rng(seed)
+    pair = _Pair(num_pages, chunk_tokens, policy)
+    ctx = {}
+    active = set()
+    try:
+        for _ in range(steps):
+            a = int(rng.integers(n_agents))
+            r = rng.random()
+            if a in active:
+                if r < 0.85:
+                    pair.end(a)
+                    active.discard(a)
+                    ctx[a] += int(rng.integers(0, 300))  # the model's reply joins the context
+            elif a in ctx and r < 0.05:
+                pair.complete(a)
+                del ctx[a]
+            else:
+                prompt = ctx.get(a, int(rng.integers(1, 400))) + int(rng.integers(1, 600))
+                if pair.begin(a, prompt) is not None:
+                    active.add(a)
+                    ctx[a] = prompt
+            pair.check()
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("policy", [kvx.KVX_EVICT_RR, kvx.KVX_EVICT_LRU])
+def test_random_traces_match_the_oracle(seed, policy):
+    _trace(seed, policy, n_agents=12, num_pages=700, chunk_tokens=64 * (1 + seed % 3), steps=600)
+
+
+@pytest.mark.parametrize("policy", [kvx.KVX_EVICT_RR, kvx.KVX_EVICT_LRU])
+def test_random_traces_under_heavy_pressure(policy):
+    """Capacity near the active demand: frequent evictions and failed turn starts."""
+    _trace(99, policy, n_agents=30, num_pages=260, chunk_tokens=16, steps=1500)
+
+
+@pytest.mark.parametrize("policy,expect", [(kvx.KVX_EVICT_RR, "even"), (kvx.KVX_EVICT_LRU, "whole")])
+def test_homogeneous_regime_closed_forms(policy, expect):
+    """Equations 2 and 3 on the library: n = 10, n a = 4, m = 7 prefixes of u pages."""
+    n, na, m = 10, 4, 7
+    ns = n - na
+    u = 8 * ns
+    c = kvx.kvx_cache_create(m * u, PAGE, PAGE, policy)
+    try:
+        for i in range(ns):
+            kvx.kvx_cache_begin_turn(c, i, u * PAGE + 1)
+            kvx.kvx_cache_end_turn(c, i)
+        for j in range(na):
+            kvx.kvx_cache_begin_turn(c, 1000 + j, u * PAGE)
+        kept = [kvx.kvx_cache_agent(c, i)[0] / (u * PAGE) for i in range(ns)]
+    finally:
+        kvx.kvx_cache_destroy(c)
+    h = (m - na) / ns
+    if expect == "even":
+        assert all(abs(k - h) < 1e-12 for k in kept)
+    else:
+        assert kept == [0.0] * (n - m) + [1.0] * (m - na)
+
+
+@pytest.mark.parametrize("policy", ["lru", "rr"])
+def test_replay_decisions_match_the_oracle(policy):
+    """The replay tool's cache calls, re-run through the oracle, give the same reuse."""
+    from paper_2609_32278_amd import agent_replay
+    from paper_2609_32278_amd import workloads as wl
+    tr = wl.make_agent_trace(24, 6, seed=5)
+    total = sum(tr.max_context(i) for i in range(tr.num_agents))
+    num_pages = int(0.5 * total) // PAGE
+    res = agent_replay.replay(tr, policy, num_pages, chunk_tokens=1024, gpu=False)
+    o = OracleCache(num_pages, PAGE, 1024, OracleCache.RR if policy == "rr" else OracleCache.LRU)
+    for ev in res.events:
+        if ev[0] == "begin":
+            try:
+                got = o.begin_turn(ev[1], ev[2])
+            except NoMemory:
+                got = None
+            assert got == ev[3], ev
+        elif ev[0] == "end":
+            o.end_turn(ev[1])
+        else:
+            o.complete(ev[1])
+    assert o.evictions == res.stats["evictions"] > 0
+    assert len(res.turns) == tr.num_agents * 6
+
+
+def test_round_robin_spreads_the_loss_on_a_replay():
+    """The paper's claim on a synthetic agent workload: round-robin tail eviction
+    leaves fewer full misses and a smaller tail of uncached tokens than LRU."""
+    from paper_2609_32278_amd import agent_replay
+    from paper_2609_32278_amd import workloads as wl
+    tr = wl.make_agent_trace(48, 8, seed=0)
+    total = sum(tr.max_context(i) for i in range(tr.num_agents))
+    num_pages = int(0.6 * total) // PAGE
+    s = {p: agent_replay.replay(tr, p, num_pages, gpu=False).summary() for p in ("lru", "rr")}
+    assert s["rr"]["full_misses"] < s["lru"]["full_misses"]
+    assert s["rr"]["uncached_p99"] < s["lru"]["uncached_p99"]

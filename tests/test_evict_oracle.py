@@ -1,0 +1,180 @@
+"""Pins of the eviction oracle (oracle/evict.py) against the paper: the closed
+forms of the homogeneous analysis (Section 3.3, Equations 1-3) and hand-traced
+runs of Algorithm 1 and of the LRU baseline on toy histories."""
+
+import pytest
+
+from oracle.evict import NoMemory, OracleCache
+
+PAGE = 16
+
+
+def _fill(cache, agent, pages):
+    """One turn that leaves `pages` whole pages cached for `agent`."""
+    cache.begin_turn(agent, pages * PAGE + 1)
+    cache.end_turn(agent)
+
+
+def _homogeneous(policy, n, na, m, u, chunk_pages):
+    """n trajectories of u pages each; ns = n - na idle ones cached first, then na
+    fresh active ones start turns that need their whole prompt; capacity m * u pages
+    (Section 3.3's model, with every idle prefix one unit)."""
+    ns = n - na
+    c = OracleCache(m * u, PAGE, chunk_pages * PAGE, policy)
+    for i in range(ns):
+        _fill(c, i, u)
+    for j in range(na):
+        c.begin_turn(1000 + j, u * PAGE)  # u pages, prefix 0, active
+    return c, [c.cached_tokens(i) / (u * PAGE) for i in range(ns)]
+
+
+# (n, na, m): na < m < n (Equation 1) and ns <= m so every idle prefix fits first
+REGIME = [(10, 4, 7), (12, 4, 9), (20, 8, 15), (6, 2, 5)]
+
+
+@pytest.mark.parametrize("n,na,m", REGIME)
+def test_round_robin_keeps_the_same_fraction_of_every_idle_prefix(n, na, m):
+    """Equation 2: ideal round-robin retains h = (m - na) / (n s) of every idle prefix."""
+    ns = n - na
+    u = 8 * ns  # (n - m) * u pages split evenly over ns agents
+    c, kept = _homogeneous(OracleCache.RR, n, na, m, u, chunk_pages=1)
+    h = (m - na) / ns
+    assert all(abs(k - h) < 1e-12 for k in kept), (kept, h)
+    q = 1 - h
+    assert abs(q - (n - m) / ns) < 1e-12
+    # Equation 3: X_RR = q for every returning idle agent
+    assert all(abs((1 - k) - q) < 1e-12 for k in kept)
+
+
+@pytest.mark.parametrize("n,na,m", REGIME)
+def test_round_robin_with_coarse_chunks_stays_within_one_chunk(n, na, m):
+    ns = n - na
+    u = 64
+    chunk = 8
+    c, kept = _homogeneous(OracleCache.RR, n, na, m, u, chunk_pages=chunk)
+    h = (m - na) / ns
+    assert all(abs(k - h) <= chunk / u + 1e-12 for k in kept), (kept, h)
+
+
+@pytest.mark.parametrize("n,na,m", REGIME)
+def test_lru_removes_whole_prefixes_of_a_fraction_q(n, na, m):
+    """Equation 3: LRU retains m - na idle prefixes whole and loses n - m whole."""
+    ns = n - na
+    c, kept = _homogeneous(OracleCache.LRU, n, na, m, 16, chunk_pages=1)
+    assert sorted(kept) == [0.0] * (n - m) + [1.0] * (m - na)
+    # the least recently used ones go first
+    assert kept[: n - m] == [0.0] * (n - m)
+    q = (n - m) / ns
+    x = [1 - k for k in kept]
+    assert abs(sum(x) / ns - q) < 1e-12  # E[X_LRU] = q
+    assert abs(sum(x) / ns - (1 - sum(_homogeneous(OracleCache.RR, n, na, m, 8 * ns, 1)[1]) / ns)) < 1e-12
+
+
+@pytest.mark.parametrize("policy", [OracleCache.LRU, OracleCache.RR])
+def test_no_eviction_when_everything_fits(policy):
+    """m >= n: eviction is unnecessary (Equation 1's upper bound)."""
+    n, na, u = 8, 3, 32
+    c, kept = _homogeneous(policy, n, na, n, u, 1)
+    assert kept == [1.0] * (n - na) and c.evictions == 0
+
+
+@pytest.mark.parametrize("policy", [OracleCache.LRU, OracleCache.RR])
+def test_active_demand_above_capacity_cannot_be_met(policy):
+    """m < na: active trajectories alone exceed the capacity (Equation 1's lower bound)."""
+    n, na, m, u = 8, 5, 4, 16
+    c = OracleCache(m * u, PAGE, PAGE, policy)
+    for i in range(n - na):
+        _fill(c, i, 1)
+    with pytest.raises(NoMemory):
+        for j in range(na):
+            c.begin_turn(1000 + j, u * PAGE)
+    assert all(c.cached_tokens(i) == 0 for i in range(n - na))  # every idle page was given up
+
+
+def _toy(policy):
+    """Agents 1, 2, 3 idle with 5, 1 and 4 cached pages (one node each), 2 pages free."""
+    c = OracleCache(12, PAGE, 2 * PAGE, policy)
+    _fill(c, 1, 5)
+    _fill(c, 2, 1)
+    _fill(c, 3, 4)
+    assert c.free == 2
+    return c
+
+
+def test_algorithm1_hand_trace():
+    """Reclaim 9 pages with 2-page chunks: queue [1, 2, 3];
+    1 loses 2 (3 left), 2 loses its last page and leaves the queue, 3 loses 2,
+    1 loses 2, 3 loses its last 2 -> 9 freed in 5 steps."""
+    c = _toy(OracleCache.RR)
+    assert c.begin_turn(9, 11 * PAGE) == 0  # needs 11 pages, 2 free
+    assert [c.cached_tokens(i) // PAGE for i in (1, 2, 3)] == [1, 0, 0]
+    assert (c.evictions, c.evicted_pages, c.free) == (5, 9, 0)
+    assert c.rr_last == 3
+    # the next reclamation continues the rotation after agent 3: agent 9 (now idle,
+    # 11 pages) comes before agent 1
+    c.end_turn(9)
+    _fill(c, 4, 1)  # needs 2 pages, none free
+    assert (c.cached_tokens(9), c.cached_tokens(1)) == (9 * PAGE, PAGE)
+
+
+def test_algorithm1_rotation_continues_across_reclamations():
+    c = OracleCache(6, PAGE, PAGE, OracleCache.RR)
+    for a in (1, 2, 3):
+        c.begin_turn(a, 2 * PAGE)  # two whole pages, nothing partial
+        c.end_turn(a)
+    assert c.free == 0
+    order = []
+    for k in range(3):  # three one-page reclamations, the new agents stay active
+        before = [c.cached_tokens(a) for a in (1, 2, 3)]
+        c.begin_turn(10 + k, PAGE)
+        after = [c.cached_tokens(a) for a in (1, 2, 3)]
+        order.append([a for a, x, y in zip((1, 2, 3), before, after) if y < x])
+    assert order == [[1], [2], [3]]
+
+
+def test_algorithm1_skips_active_trajectories():
+    c = _toy(OracleCache.RR)
+    c.begin_turn(1, 5 * PAGE + 1)  # agent 1 resumes: active, its 5 pages pinned (needs 1 more)
+    assert c.cached_tokens(1) == 5 * PAGE
+    c.begin_turn(9, 5 * PAGE)  # needs 5; 1 free -> reclaim 4 from agents 2 and 3 only
+    assert c.cached_tokens(1) == 5 * PAGE
+    assert [c.cached_tokens(i) // PAGE for i in (2, 3)] == [0, 1]
+
+
+def test_lru_hand_trace():
+    """Same toy history: LRU drops whole leaves oldest first -- agent 1 (5 pages),
+    agent 2 (1), agent 3 (4) -- and over-reclaims the last node."""
+    c = _toy(OracleCache.LRU)
+    c.begin_turn(9, 11 * PAGE)
+    assert [c.cached_tokens(i) for i in (1, 2, 3)] == [0, 0, 0]
+    assert (c.evictions, c.evicted_pages, c.free) == (3, 10, 1)
+
+
+def test_lru_takes_a_whole_synchronized_path_before_the_next_agent():
+    """Recency synchronization (Section 3.1): all nodes of an agent's path carry
+    the time of its last access, so LRU empties one agent node after node."""
+    c = OracleCache(64, PAGE, PAGE, OracleCache.LRU)
+    c.begin_turn(1, 3 * PAGE + 1); c.end_turn(1)   # node 3 pages
+    c.begin_turn(1, 6 * PAGE + 1); c.end_turn(1)   # node 3 more
+    c.begin_turn(2, 4 * PAGE + 1); c.end_turn(2)   # node 4 pages
+    assert c.agents[1].nodes == [3, 3]
+    c.begin_turn(1, 6 * PAGE + 1)  # agent 1 resumes: its whole path is now the newest
+    c.end_turn(1)
+    free = c.free
+    c.begin_turn(3, (free + 5) * PAGE)  # reclaim 5: agent 2 (4, oldest), then agent 1's leaf (3)
+    assert c.cached_tokens(2) == 0 and c.agents[1].nodes == [3]
+
+
+def test_turns_reuse_whole_pages_and_compute_at_least_one_token():
+    c = OracleCache(64, PAGE, PAGE, OracleCache.RR)
+    assert c.begin_turn(1, 40) == 0
+    c.end_turn(1)
+    assert c.cached_tokens(1) == 32             # the partial page is not kept
+    assert c.begin_turn(1, 100) == 32
+    c.end_turn(1)
+    assert c.cached_tokens(1) == 96
+    assert c.begin_turn(1, 96) == 80            # at least one token computed: page 5 recomputed
+    c.end_turn(1)
+    assert c.cached_tokens(1) == 96
+    c.complete(1)
+    assert c.free == 64 and c.cached_tokens(1) == 0

@@ -1,0 +1,65 @@
+"""Multi-turn agent replay on the GPU: the prefix cache's page tables carry each
+agent's history across turns, evictions and recomputations; every batch's
+suffix rows must match a brute-force attention over the agent's logical context
+(no page table), and the cache's reuse decisions must match the eviction oracle."""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_harness import compare
+from helpers import brute_force, to_f64
+from oracle.evict import NoMemory, OracleCache
+from paper_2609_32278_amd import agent_replay
+from paper_2609_32278_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _trace():
+    return wl.make_agent_trace(6, 4, seed=3, first=(200, 700), new=(20, 300), reply=(10, 80), idle=(1, 4),
+                               spread=3, num_q_heads=8, num_kv_heads=2, head_dim=64)
+
+
+def _replay_oracle(events, num_pages, chunk_tokens, policy):
+    o = OracleCache(num_pages, 16, chunk_tokens, OracleCache.RR if policy == "rr" else OracleCache.LRU)
+    for ev in events:
+        if ev[0] == "begin":
+            try:
+                got = o.begin_turn(ev[1], ev[2])
+            except NoMemory:
+                got = None
+            assert got == ev[3], ev
+        elif ev[0] == "end":
+            o.end_turn(ev[1])
+        else:
+            o.complete(ev[1])
+    return o
+
+
+@pytest.mark.parametrize("policy", ["lru", "rr"])
+def test_replay_batches_match_brute_force(policy):
+    tr = _trace()
+    total = sum(tr.max_context(i) for i in range(tr.num_agents))
+    num_pages = int(0.45 * total) // 16
+    print(f"[replay] policy={policy} agents={tr.num_agents} pages={num_pages}", flush=True)
+    checked = []
+
+    def on_batch(reqs, q, out):
+        row = 0
+        for r in reqs:
+            k, v = wl.agent_kv(tr, r.agent, r.prompt, "cuda")  # same generator the replay used
+            ref, _ = brute_force(to_f64(q[row:row + r.uncached]), to_f64(k), to_f64(v), r.prefix, tr.sm_scale)
+            got = out[row:row + r.uncached].float().cpu().numpy()
+            compare(got, ref, f"{policy} agent {r.agent} turn {r.turn} P={r.prefix} E={r.uncached}")
+            row += r.uncached
+            checked.append(r)
+
+    res = agent_replay.replay(tr, policy, num_pages, chunk_tokens=64, on_batch=on_batch)
+    torch.cuda.synchronize()
+    assert len(checked) == tr.num_agents * len(tr.new[0])
+    o = _replay_oracle(res.events, num_pages, 64, policy)
+    assert o.evictions == res.stats["evictions"] > 0
+    # some returning turns reuse part of their history, some recompute
+    back = [t for t in checked if t.turn > 0]
+    assert any(0 < t.prefix for t in back) and any(t.recomputed_history > 0 for t in back)
