@@ -21,6 +21,7 @@ from __future__ import annotations
 import argparse
 import json
 import sys
+import time
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -57,6 +58,8 @@ class ReplayResult:
     events: list = field(default_factory=list)   # ("begin", agent, prompt, prefix | None), ("end", a), ("complete", a)
     batch_ms: list = field(default_factory=list)
     stats: dict = field(default_factory=dict)
+    cache_calls: int = 0
+    cache_seconds: float = 0.0  # host time inside the cache's calls
 
     def summary(self) -> dict:
         back = [t for t in self.turns if t.turn > 0]
@@ -84,6 +87,7 @@ class ReplayResult:
             out.update({"batches": len(b), "prefill_ms_total": float(b.sum()),
                         "prefill_ms_p50": float(np.percentile(b, 50)), "prefill_ms_p99": float(np.percentile(b, 99))})
         out["cache"] = self.stats
+        out["cache_us_per_call"] = 1e6 * self.cache_seconds / max(self.cache_calls, 1)
         return out
 
 
@@ -112,7 +116,10 @@ def replay(tr: wl.AgentTrace, policy: str, num_pages: int, *, chunk_tokens: int 
                 raise RuntimeError("replay did not finish (capacity below the active demand?)")
             for a in range(n):
                 if running_until[a] == tick:
+                    t0 = time.perf_counter()
                     kvx.kvx_cache_end_turn(cache, a)
+                    res.cache_seconds += time.perf_counter() - t0
+                    res.cache_calls += 1
                     res.events.append(("end", a))
                     running_until[a] = -1
                     ctx[a] += tr.reply[a][turn[a]]
@@ -128,13 +135,18 @@ def replay(tr: wl.AgentTrace, policy: str, num_pages: int, *, chunk_tokens: int 
                 if done[a] or running_until[a] >= 0 or due[a] > tick:
                     continue
                 prompt = ctx[a] + tr.new[a][turn[a]]
+                t0 = time.perf_counter()
                 try:
                     prefix, table = kvx.kvx_cache_begin_turn(cache, a, prompt)
                 except kvx.KvxError as e:
+                    res.cache_seconds += time.perf_counter() - t0
+                    res.cache_calls += 1
                     if e.status != kvx.KVX_ENOMEM:
                         raise
                     res.events.append(("begin", a, prompt, None))
                     continue  # waits for pages to free up
+                res.cache_seconds += time.perf_counter() - t0
+                res.cache_calls += 1
                 res.events.append(("begin", a, prompt, prefix))
                 rec = TurnRecord(a, turn[a], tick, prompt, prefix, ctx[a])
                 res.turns.append(rec)
