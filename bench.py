@@ -45,6 +45,10 @@ DESCRIPTIONS = {
                "page 16, bf16 K/V",
     "wide70b_fp8": "70B-shaped layer: 48 requests, P~logU[16384,262144], E~U[512,8192], Hq 64 / Hkv 8, d 128, "
                    "page 16, fp8 e4m3 K/V with per-head scales U[0.01,0.1]",
+    "decode_llama8b": "decode step (E = 1): 128 agents, P~U[4096,32768] (page-rounded), Hq 32 / Hkv 8, d 128, "
+                      "page 16, bf16 K/V, values N(0,0.25)",
+    "decode_long": "decode step (E = 1): 32 agents, P~U[65536,131072] (page-rounded), Hq 32 / Hkv 8, d 128, "
+                   "page 16, bf16 K/V",
 }
 
 
@@ -267,6 +271,11 @@ def main():
             "kernel_source": attn_source_hash(),
         },
     }
+    if args.config.startswith("decode"):
+        # one query per request: intensity ~ 2 Hq/Hkv / b_kv flop/B, far below the ridge -> HBM-bound
+        gbps = attn_alg_bytes / (attn_ms * 1e-3) / 1e9
+        result["roofline"].update({"bound": "hbm", "achieved": round(gbps, 1), "peak": PEAK_HBM_GBPS,
+                                   "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4)})
     if not args.no_cpu_baseline:
         cb = run_cpu_baseline(args.config, args.cpu_rows, args.cpu_reqs)
         result["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v) for k, v in cb.items()}

@@ -46,6 +46,8 @@ CONFIG_IDS = {
     "rr_partial": 4,    # 64 agents that lost 1-4 tail chunks of 2048 tokens
     "wide70b": 5,       # 48 requests, 64/8 heads, bf16 K/V pool
     "wide70b_fp8": 5,   # same batch, fp8 e4m3 K/V pool with per-head scales
+    "decode_llama8b": 8,  # decode step: 128 agents, one new token each, Llama-3-8B-shaped
+    "decode_long": 9,     # decode step: 32 agents with 64k-128k contexts
 }
 
 
@@ -219,6 +221,17 @@ def make_workload(name: str, seed: int = 0) -> Workload:
         new = rng.integers(128, 4096 + 1, 64)
         p = ctx - 2048 * k
         e = 2048 * k + new
+        num_pages = None
+    elif name == "decode_llama8b":
+        hq, hkv, d = 32, 8, 128
+        p = _round_to(rng.integers(4096, 32768 + 1, 128), PAGE_SIZE)
+        e = np.ones(128, np.int64)
+        sigma = 0.5
+        num_pages = None
+    elif name == "decode_long":
+        hq, hkv, d = 32, 8, 128
+        p = _round_to(rng.integers(65536, 131072 + 1, 32), PAGE_SIZE)
+        e = np.ones(32, np.int64)
         num_pages = None
     else:  # wide70b, wide70b_fp8
         hq, hkv, d = 64, 8, 128

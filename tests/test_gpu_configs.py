@@ -1,4 +1,4 @@
-"""The five agent-shaped configurations at full size on the GPU.
+"""The five agent-shaped configurations, and two decode steps, at full size on the GPU.
 
 The whole batch runs through store_kv + extend_attention exactly as the benchmark
 launches it; the oracle then checks sampled rows (first, last, page-boundary and
@@ -25,6 +25,9 @@ SAMPLING = {
     "rr_partial": (6, 6),
     "wide70b": (4, 6),
     "wide70b_fp8": (4, 6),
+    # decode steps (one row per request; the planner splits every long key range)
+    "decode_llama8b": (32, 1),
+    "decode_long": (12, 1),
 }
 
 
