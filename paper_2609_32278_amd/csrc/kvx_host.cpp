@@ -227,7 +227,7 @@ struct Plan {
 
 // Work plan of extend_attention.
 //   * every request's suffix is cut into tiles of tile_tok tokens (x group query heads
-//     = 128 rows) per KV head; a tile covers keys [0, P + last token of the tile];
+//     = 256 rows) per KV head; a tile covers keys [0, P + last token of the tile];
 //   * when the batch has too little work to fill the chip, or a tile's key range is
 //     far longer than the average work per workgroup slot, the key range is split at
 //     multiples of the tile width into parts merged by log-sum-exp afterwards;
@@ -381,6 +381,85 @@ int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, in
   return KVX_OK;
 }
 
+// ---- decode steps: every request with work has exactly one suffix token
+using kvx::DecodeMerge;
+using kvx::DecodeUnit;
+
+struct DecodePlan {
+  std::vector<DecodeUnit> units;
+  std::vector<DecodeMerge> merges;
+  std::vector<kvx_work_item> items;
+  int64_t n_parts = 0;
+};
+
+bool is_decode_batch(const kvx_batch* b, int32_t Hq, int32_t Hkv) {
+  if (Hq / Hkv > kvx::kDecodeMaxGroup) return false;
+  bool any = false;
+  for (int r = 0; r < b->num_reqs; r++) {
+    if (b->extend_lens[r] > 1) return false;
+    any |= b->extend_lens[r] == 1;
+  }
+  return any;
+}
+
+// Work plan of a decode step: each (request, KV head) key range [0, P] is cut into
+// chunks of a common length, a multiple of 64 keys chosen so that the batch yields
+// about 2048 chunks (8 per workgroup slot at two resident workgroups per CU), at
+// least 512 keys each; a range of more than one chunk becomes parts merged by
+// log-sum-exp.  Chunks are dispatched longest first.
+int make_decode_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hkv, DecodePlan& plan) {
+  const int64_t A = kvx::kDecodeChunkAlign;
+  int64_t total = 0;
+  for (int r = 0; r < b->num_reqs; r++)
+    if (b->extend_lens[r] == 1) total += (int64_t)Hkv * ((int64_t)b->prefix_lens[r] + 1);
+  int64_t chunk;
+  if (g_split_keys > 0) {
+    chunk = g_split_keys;
+  } else {
+    chunk = std::max<int64_t>(512, (total + 2047) / 2048);
+    chunk = (chunk + A - 1) / A * A;
+  }
+  for (;;) {  // bound the partial results like the prefill planner does
+    int64_t parts = 0;
+    for (int r = 0; r < b->num_reqs; r++) {
+      if (b->extend_lens[r] != 1) continue;
+      const int64_t n = ((int64_t)b->prefix_lens[r] + 1 + chunk - 1) / chunk;
+      if (n > 1) parts += n * Hkv;
+    }
+    if (parts <= kMaxParts) break;
+    chunk *= 2;
+  }
+  for (int r = 0; r < b->num_reqs; r++) {
+    if (b->extend_lens[r] != 1) continue;
+    const int64_t L = (int64_t)b->prefix_lens[r] + 1;
+    const int64_t nc = (L + chunk - 1) / chunk;
+    for (int32_t h = 0; h < Hkv; h++) {
+      const int64_t part0 = plan.n_parts;
+      for (int64_t c = 0; c < nc; c++) {
+        DecodeUnit u{};
+        u.qo_row = (int32_t)qo[(size_t)r];
+        u.page_base = b->page_indptr[r];
+        u.key_begin = (int32_t)(c * chunk);
+        u.key_end = (int32_t)std::min<int64_t>(L, (c + 1) * chunk);
+        u.head = h;
+        u.part = nc > 1 ? (int32_t)plan.n_parts++ : -1;
+        u.req = r;
+        plan.units.push_back(u);
+      }
+      if (nc > 1) plan.merges.push_back(DecodeMerge{(int32_t)qo[(size_t)r], h, (int32_t)part0, (int32_t)nc});
+    }
+  }
+  std::stable_sort(plan.units.begin(), plan.units.end(), [](const DecodeUnit& x, const DecodeUnit& y) {
+    return x.key_end - x.key_begin > y.key_end - y.key_begin;
+  });
+  for (size_t i = 0; i < plan.units.size(); i++) {
+    const DecodeUnit& u = plan.units[i];
+    kvx_work_item it{u.req, u.head, 0, 1, u.key_begin, u.key_end, u.part, (int32_t)(i % kvx::kNumXcd)};
+    plan.items.push_back(it);
+  }
+  return KVX_OK;
+}
+
 int check_heads(int32_t Hq, int32_t Hkv, int32_t D) {
   if (Hkv <= 0 || Hq <= 0 || Hq % Hkv != 0)
     return fail(KVX_EINVAL, "num_q_heads (%d) must be a positive multiple of num_kv_heads (%d)", Hq, Hkv);
@@ -388,6 +467,53 @@ int check_heads(int32_t Hq, int32_t Hkv, int32_t D) {
     return fail(KVX_EUNSUPPORTED, "query heads per KV head (%d) above %d", Hq / Hkv, kvx::kTileRows);
   if (Hkv >= (1 << 15)) return fail(KVX_EUNSUPPORTED, "num_kv_heads too large");
   if (D != 64 && D != 128) return fail(KVX_EUNSUPPORTED, "head_dim %d (supported: 64, 128)", D);
+  return KVX_OK;
+}
+
+int decode_attention(kvx_pool* pool, const kvx_batch* batch, const std::vector<int64_t>& qo, const void* q,
+                     int32_t num_q_heads, float sm_scale, void* out, float* lse, hipStream_t s) {
+  DecodePlan plan;
+  if (int rc = make_decode_plan(batch, qo, pool->num_kv_heads, plan)) return rc;
+  const int D = pool->head_dim;
+  constexpr int R = kvx::kDecodeMaxGroup;
+  if (plan.n_parts > 0)
+    if (int rc = pool->parts.ensure((size_t)plan.n_parts * R * (D + 1) * sizeof(float))) return rc;
+  const size_t ub = plan.units.size() * sizeof(DecodeUnit), mb = plan.merges.size() * sizeof(DecodeMerge);
+  std::vector<uint8_t> blob(ub + mb);
+  if (ub) std::memcpy(blob.data(), plan.units.data(), ub);
+  if (mb) std::memcpy(blob.data() + ub, plan.merges.data(), mb);
+  void* dev = nullptr;
+  if (int rc = pool->st_attn.upload(blob.data(), blob.size(), s, &dev)) return rc;
+  kvx::DecodeParams p;
+  p.q = (const uint16_t*)q;
+  p.out = (uint16_t*)out;
+  p.lse = lse;
+  p.k_pool = pool->k;
+  p.v_pool = pool->v;
+  p.page_ids = batch->page_ids;
+  p.units = (const DecodeUnit*)dev;
+  p.o_part = plan.n_parts ? (float*)pool->parts.ptr : nullptr;
+  p.lse_part = plan.n_parts ? (float*)pool->parts.ptr + (size_t)plan.n_parts * R * D : nullptr;
+  p.k_scale = pool->scales_d;
+  p.v_scale = pool->scales_d ? pool->scales_d + pool->num_kv_heads : nullptr;
+  p.num_q_heads = num_q_heads;
+  p.num_kv_heads = pool->num_kv_heads;
+  p.group = num_q_heads / pool->num_kv_heads;
+  p.scale_log2 = sm_scale * 1.4426950408889634f;
+  hipError_t e = kvx::launch_decode(p, (int64_t)plan.units.size(), D, pool->kv_dtype == KVX_KV_FP8_E4M3, s);
+  if (e != hipSuccess) return hip_fail(e, "decode kernel launch");
+  if (!plan.merges.empty()) {
+    kvx::DecodeMergeParams m;
+    m.merges = (const DecodeMerge*)((const uint8_t*)dev + ub);
+    m.o_part = p.o_part;
+    m.lse_part = p.lse_part;
+    m.out = (uint16_t*)out;
+    m.lse = lse;
+    m.num_q_heads = num_q_heads;
+    m.group = p.group;
+    e = kvx::launch_decode_merge(m, (int64_t)plan.merges.size(), D, s);
+    if (e != hipSuccess) return hip_fail(e, "decode merge kernel launch");
+  }
   return KVX_OK;
 }
 
@@ -603,13 +729,22 @@ int extend_attention_plan(const kvx_batch* batch, int32_t num_q_heads, int32_t n
   std::vector<int64_t> qo;
   if (int rc = check_batch(batch, qo, false)) return rc;
   if (cap < 0) return fail(KVX_EINVAL, "cap < 0");
-  Plan plan;
-  if (qo.back() > 0)
-    if (int rc = make_plan(batch, qo, num_q_heads, num_kv_heads, plan)) return rc;
-  *count = (int64_t)plan.items.size();
+  std::vector<kvx_work_item> out_items;
+  if (qo.back() > 0) {
+    if (is_decode_batch(batch, num_q_heads, num_kv_heads)) {
+      DecodePlan dp;
+      if (int rc = make_decode_plan(batch, qo, num_kv_heads, dp)) return rc;
+      out_items = std::move(dp.items);
+    } else {
+      Plan plan;
+      if (int rc = make_plan(batch, qo, num_q_heads, num_kv_heads, plan)) return rc;
+      out_items = std::move(plan.items);
+    }
+  }
+  *count = (int64_t)out_items.size();
   if (items != nullptr) {
     const int64_t m = std::min<int64_t>(cap, *count);
-    for (int64_t i = 0; i < m; i++) items[i] = plan.items[(size_t)i];
+    for (int64_t i = 0; i < m; i++) items[i] = out_items[(size_t)i];
   }
   return KVX_OK;
 }
@@ -628,6 +763,9 @@ int extend_attention(kvx_pool* pool, const kvx_batch* batch, const void* q, int3
   hipStream_t s = (hipStream_t)stream;
   if (validate_mode())
     if (int rc = check_page_ids(pool, batch, s)) return rc;
+
+  if (is_decode_batch(batch, num_q_heads, pool->num_kv_heads))
+    return decode_attention(pool, batch, qo, q, num_q_heads, sm_scale, out, lse, s);
 
   Plan plan;
   if (int rc = make_plan(batch, qo, num_q_heads, pool->num_kv_heads, plan)) return rc;

@@ -96,6 +96,61 @@ struct PageIoParams {
   int32_t to_pool;          // 1: write pages into the pool, 0: read them out
 };
 
+// ---- decode (one query token per request): a key chunk of one (request, KV head)
+constexpr int kDecodeThreads = 256;  // 4 waves, each streaming every 4th pair of pages
+constexpr int kDecodeMaxGroup = 16;  // query heads per KV head held in one MFMA column block
+constexpr int kDecodeChunkAlign = 64;  // chunk boundaries are multiples of it (keys)
+
+struct DecodeUnit {
+  int32_t qo_row;     // the request's only suffix row
+  int32_t page_base;  // offset of the request's page list in page_ids
+  int32_t key_begin;  // multiple of kDecodeChunkAlign
+  int32_t key_end;    // exclusive
+  int32_t head;       // KV head
+  int32_t part;       // -1: final result; else index of this chunk's partial result
+  int32_t req;
+  int32_t pad;
+};
+static_assert(sizeof(DecodeUnit) == 32, "DecodeUnit is 32 bytes");
+
+struct DecodeMerge {
+  int32_t qo_row;
+  int32_t head;
+  int32_t part0;
+  int32_t nparts;
+};
+
+struct DecodeParams {
+  const uint16_t* q;      // bf16 [T, Hq, D]
+  uint16_t* out;          // bf16 [T, Hq, D]
+  float* lse;             // fp32 [T, Hq] or null
+  const void* k_pool;     // [page][kv_head][slot][D], bf16 or fp8
+  const void* v_pool;     // [page][kv_head][D][slot]
+  const int32_t* page_ids;
+  const DecodeUnit* units;
+  float* o_part;          // fp32 [parts, kDecodeMaxGroup, D]
+  float* lse_part;        // fp32 [parts, kDecodeMaxGroup]
+  const float* k_scale;   // fp8 pool: device [Hkv]
+  const float* v_scale;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t group;          // Hq / Hkv <= kDecodeMaxGroup
+  float scale_log2;
+};
+
+struct DecodeMergeParams {
+  const DecodeMerge* merges;
+  const float* o_part;
+  const float* lse_part;
+  uint16_t* out;
+  float* lse;
+  int32_t num_q_heads;
+  int32_t group;
+};
+
+hipError_t launch_decode(const DecodeParams& p, int64_t n_units, int head_dim, bool fp8, hipStream_t stream);
+hipError_t launch_decode_merge(const DecodeMergeParams& p, int64_t n_merges, int head_dim, hipStream_t stream);
+
 // Record a failure for kvx_last_error() and return `code` (host code of any file).
 int report(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 

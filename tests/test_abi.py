@@ -121,9 +121,25 @@ def _check_plan(w, split=0):
     return items
 
 
-@pytest.mark.parametrize("name", ["tiny", "llama8b", "tail_outlier", "rr_partial", "wide70b"])
+@pytest.mark.parametrize("name", ["tiny", "llama8b", "tail_outlier", "rr_partial", "wide70b", "decode_llama8b",
+                                  "decode_long"])
 def test_plan_covers_every_visible_pair_once(name):
     _check_plan(wl.make_workload(name))
+
+
+def test_decode_steps_get_key_chunks_of_one_token():
+    """A batch of one-token suffixes (a decode step) is planned as key chunks of
+    (request, KV head), split so that the step fills the chip."""
+    w = wl.make_workload("decode_long")
+    b = kvx.Batch(w.prefix_lens, w.extend_lens, w.page_indptr, 0)
+    items = kvx.extend_attention_plan(b, w.num_q_heads, w.num_kv_heads, w.head_dim)
+    assert (items["tok_count"] == 1).all() and (items["tok_begin"] == 0).all()
+    assert len(items) >= 1024 and (items["part"] >= 0).all()
+    # a batch with a longer suffix anywhere goes through the prefill tiles instead
+    w2 = wl.make_custom([5000, 300], [1, 2], 32, 8, 128)
+    b2 = kvx.Batch(w2.prefix_lens, w2.extend_lens, w2.page_indptr, 0)
+    items2 = kvx.extend_attention_plan(b2, 32, 8, 128)
+    assert (items2["tok_count"] == 2).any()
 
 
 @pytest.mark.parametrize("split", [64, 1024])

@@ -53,6 +53,11 @@ CASES = {
     "g8_fp8_d128": ([300, 16, 0], [57, 129, 40], 16, 2, 128, wl.KV_FP8_E4M3),
     "g2_fp8_d64": ([7, 200], [99, 3], 4, 2, 64, wl.KV_FP8_E4M3),
     "decode_like": ([5000, 3001, 64], [1, 1, 1], 8, 1, 128, wl.KV_BF16),
+    # decode steps on the decode kernel: fp8 pool, 16 heads per KV head, an empty
+    # prefix (a single key), a request with no suffix at all
+    "decode_fp8_g8_d128": ([3000, 77, 1025], [1, 1, 1], 16, 2, 128, wl.KV_FP8_E4M3),
+    "decode_g16_d64": ([700, 16, 0, 4100], [1, 1, 1, 0], 32, 2, 64, wl.KV_BF16),
+    "decode_fp8_d64": ([9000, 33], [1, 1], 8, 4, 64, wl.KV_FP8_E4M3),
     "long_causal": ([0], [1000], 4, 1, 128, wl.KV_BF16),
 }
 
