@@ -52,21 +52,28 @@ DESCRIPTIONS = {
 }
 
 
-def attn_source_hash() -> str:
-    path = os.path.join(ROOT, "paper_2609_32278_amd", "csrc", "kvx_attn.hip")
+def is_decode(config: str) -> bool:
+    """Decode steps (one suffix token per request) run the decode kernel."""
+    return config.startswith("decode")
+
+
+def attn_source_hash(config: str = "llama8b") -> str:
+    name = "kvx_decode.hip" if is_decode(config) else "kvx_attn.hip"
+    path = os.path.join(ROOT, "paper_2609_32278_amd", "csrc", name)
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
 def traffic_from_profiles(config: str):
     """HBM bytes per attention launch from the committed rocprofv3 counter summary,
     only if it was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"extend_attn_{config}_hbm_counters.md")
+    kernel = "decode_kernel" if is_decode(config) else "extend_attn"
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{config}_hbm_counters.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m_hash = re.search(r"kernel source sha256\[:16\]:\s*`?([0-9a-f]{16})", text)
     m_bytes = re.search(r"HBM bytes per launch \(scaled\):\s*`?([0-9.eE+]+)", text)
-    if not (m_hash and m_bytes) or m_hash.group(1) != attn_source_hash():
+    if not (m_hash and m_bytes) or m_hash.group(1) != attn_source_hash(config):
         return None
     return float(m_bytes.group(1))
 
@@ -268,14 +275,14 @@ def main():
             "frac": round(tflops_attn / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
             "algorithmic_bytes": attn_alg_bytes,
-            "kernel_source": attn_source_hash(),
+            "kernel_source": attn_source_hash(args.config),
         },
     }
-    if args.config.startswith("decode"):
+    if is_decode(args.config):
         # one query per request: intensity ~ 2 Hq/Hkv / b_kv flop/B, far below the ridge -> HBM-bound
         gbps = attn_alg_bytes / (attn_ms * 1e-3) / 1e9
-        result["roofline"].update({"bound": "hbm", "achieved": round(gbps, 1), "peak": PEAK_HBM_GBPS,
-                                   "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4)})
+        result["roofline"].update({"kernel": "decode_kernel", "bound": "hbm", "achieved": round(gbps, 1),
+                                   "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4)})
     if not args.no_cpu_baseline:
         cb = run_cpu_baseline(args.config, args.cpu_rows, args.cpu_reqs)
         result["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v) for k, v in cb.items()}

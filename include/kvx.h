@@ -158,6 +158,9 @@ int store_kv(kvx_pool *pool, const kvx_batch *batch, const void *k_ext, const vo
  *   out          device bf16 [T, num_q_heads, head_dim] (round to nearest even)
  *   lse          device fp32 [T, num_q_heads] natural-log sum of exp of the scaled
  *                scores, or NULL
+ * A decode step -- every request has at most one suffix token, and at most 16
+ * query heads share a KV head -- runs a dedicated decode kernel (key chunks of
+ * each request and KV head streamed from HBM); the result is the same operation.
  * Uses a library-owned device workspace (grown with hipMalloc when a batch needs
  * more than any earlier one).  Errors: EINVAL, EUNSUPPORTED, ERANGE (validation
  * mode), ENOMEM, EHIP.  R = 0 or T = 0: no-op.
@@ -185,7 +188,8 @@ typedef struct {
 /*
  * The host-side work plan extend_attention would launch for a batch (host only,
  * no device work): ragged (P, E) pairs cut into tiles, long key ranges split,
- * items ordered longest first within each XCD.  Writes at most `cap` items to
+ * items ordered longest first within each XCD; for a decode step, key chunks of
+ * every (request, KV head), longest first (tok_count 1).  Writes at most `cap` items to
  * `items` (may be NULL) and the total count to *count.
  *   num_kv_heads, num_q_heads, head_dim as for extend_attention.
  * Errors: EINVAL, EUNSUPPORTED.
