@@ -66,6 +66,10 @@ def _load():
         lib.oracle_extend_attention.restype = ctypes.c_int
         lib.oracle_extend_attention.argtypes = [i32, P, P, P, P, i32, i64, i32, i32, i32, i32, P, P,
                                                 P, P, i64, P, P, P, dbl, P, P, i32, i32]
+        lib.oracle_store_kv_f64.restype = ctypes.c_int
+        lib.oracle_store_kv_f64.argtypes = [i32, P, P, P, P, P, i32, i64, i32, i32, i32, P, P, P, P, P, P]
+        lib.oracle_bf16_round_array.restype = None
+        lib.oracle_bf16_round_array.argtypes = [P, i64, P]
         lib.oracle_e4m3_encode_array.restype = None
         lib.oracle_e4m3_encode_array.argtypes = [P, i64, P]
         lib.oracle_e4m3_decode_array.restype = None
@@ -103,6 +107,21 @@ def e4m3_encode(x: np.ndarray) -> np.ndarray:
     out = np.empty(x.shape, dtype=np.uint8)
     _load().oracle_e4m3_encode_array(_ptr(x), x.size, _ptr(out))
     return out
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns nearest to float64 values (ties to even), rounded once."""
+    x = _c(x, np.float64)
+    out = np.empty(x.shape, dtype=np.uint16)
+    _load().oracle_bf16_round_array(_ptr(x), x.size, _ptr(out))
+    return out
+
+
+def bf16_value(bits) -> np.ndarray:
+    """float64 values of bf16 bit patterns (uint16 array or torch bf16)."""
+    b = bf16_bits(bits)
+    with np.errstate(invalid="ignore"):  # signalling-NaN patterns stay NaN
+        return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
 def e4m3_decode(codes: np.ndarray) -> np.ndarray:
@@ -159,6 +178,27 @@ def store_kv(pool: OraclePool, prefix_lens, extend_lens, page_indptr, page_ids, 
                                  _ptr(kb), _ptr(vb), _ptr(pool.k), _ptr(pool.v))
     if rc != 0:
         raise ValueError(f"oracle_store_kv failed ({rc}): page id outside the pool")
+
+
+def store_kv_values(pool: OraclePool, prefix_lens, extend_lens, page_indptr, page_ids, k_vals, v_ext):
+    """store_kv with K given as exact float64 values [T, Hkv, d]: a bf16 pool holds
+    their nearest bf16, an fp8 pool encode(float32(x) * float32(1/scale))."""
+    p = _c(prefix_lens, np.int32)
+    e = _c(extend_lens, np.int32)
+    qo = np.zeros(len(e) + 1, dtype=np.int64)
+    np.cumsum(e, out=qo[1:])
+    kd = _c(k_vals, np.float64).reshape(-1)
+    vb = bf16_bits(v_ext).reshape(-1)
+    if kd.size != int(qo[-1]) * pool.num_kv_heads * pool.head_dim or vb.size != kd.size:
+        raise ValueError("k_vals / v_ext size does not match sum(extend_lens) * Hkv * d")
+    pi = _indptr64(page_indptr)
+    ids = _c(page_ids, np.int32)
+    rc = _load().oracle_store_kv_f64(len(p), _ptr(p), _ptr(e), _ptr(qo), _ptr(pi), _ptr(ids),
+                                     pool.page_size, pool.num_pages, pool.num_kv_heads, pool.head_dim,
+                                     pool.kv_dtype, _ptr(pool.k_scale), _ptr(pool.v_scale),
+                                     _ptr(kd), _ptr(vb), _ptr(pool.k), _ptr(pool.v))
+    if rc != 0:
+        raise ValueError(f"oracle_store_kv_f64 failed ({rc}): page id outside the pool")
 
 
 def extend_attention(pool: OraclePool, prefix_lens, extend_lens, page_indptr, page_ids, q_rows,

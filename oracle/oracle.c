@@ -16,6 +16,9 @@
  * attention layer, Section 2).  The oracle is that definition written out:
  *
  *   oracle_store_kv:        pool[page_of(P+i)][h][(P+i) % S][:] = K_ext[row][h][:]
+ *   oracle_store_kv_f64:    the same placement for K given as exact values
+ *                            (the rotated keys of the RoPE store, oracle/rope.py),
+ *                            rounded once into the pool's format
  *   oracle_extend_attention: s_j = scale * <q, k_j>, w_j = exp(s_j - max s),
  *                            o = sum_j w_j v_j / sum_j w_j,  lse = max s + ln(sum w)
  *
@@ -73,6 +76,38 @@ static float bf16_to_float(uint16_t bits)
     float f;
     memcpy(&f, &u, sizeof f);
     return f;
+}
+
+/* The bf16 value nearest to a double, ties to the even significand: bf16 keeps
+ * 8 significant bits (7 stored) over binary32's exponent range, so the
+ * quantum of |x| in [2^(e-1), 2^e) is 2^(e-8), and 2^-133 below the smallest
+ * normal 2^-126.  Rounding straight from the double (not through a float)
+ * avoids a second rounding.  Magnitudes past the largest finite bf16 round to
+ * infinity the way binary32 overflow does. */
+uint16_t oracle_bf16_round(double x)
+{
+    if (isnan(x))
+        return 0x7FC0;
+    double a = fabs(x);
+    uint16_t sign = signbit(x) ? 0x8000 : 0;
+    if (a == 0.0)
+        return sign;
+    int e;
+    frexp(a, &e);
+    int q = e - 8;
+    if (q < -133)
+        q = -133;
+    double r = ldexp(nearbyint(ldexp(a, -q)), q); /* default rounding: ties to even */
+    float f = (float)r;                            /* exact, or inf past the range */
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    return (uint16_t)(sign | (uint16_t)((u >> 16) & 0x7FFF));
+}
+
+void oracle_bf16_round_array(const double *x, int64_t n, uint16_t *out)
+{
+    for (int64_t i = 0; i < n; i++)
+        out[i] = oracle_bf16_round(x[i]);
 }
 
 /* OCP 8-bit floating point, E4M3 variant: 1 sign bit, 4 exponent bits (bias 7),
@@ -167,15 +202,20 @@ static int64_t pool_offset(int64_t page, int h, int slot, int c, int num_kv_head
     return (((page * num_kv_heads) + h) * page_size + slot) * (int64_t)head_dim + c;
 }
 
-/* Write every suffix token's K and V rows into the request's pages.  Returns 0,
+/* Write every suffix token's K and V rows into the request's pages.  K comes
+ * either as bf16 bits (k_bits) or as exact real values (k_vals, double; the
+ * rotated keys of the RoPE store): a bf16 pool holds bf16 bits, rounded to
+ * nearest-even from the double when k_vals is given; an fp8 pool holds
+ * encode(float(x) * float(1/scale)).  V always comes as bf16 bits.  Returns 0,
  * or -1 if a page id falls outside [0, num_pages) (those tokens are skipped).
  * Suffix tokens map to distinct (page, slot) pairs in a valid batch, so the
  * per-token loop may run in parallel. */
-int oracle_store_kv(int32_t num_reqs, const int32_t *prefix_lens, const int32_t *extend_lens,
-                    const int64_t *qo_indptr, const int64_t *page_indptr, const int32_t *page_ids,
-                    int32_t page_size, int64_t num_pages, int32_t num_kv_heads, int32_t head_dim,
-                    int32_t kv_dtype, const float *k_scale, const float *v_scale,
-                    const uint16_t *k_ext, const uint16_t *v_ext, void *k_pool, void *v_pool)
+static int store_rows(int32_t num_reqs, const int32_t *prefix_lens, const int32_t *extend_lens,
+                      const int64_t *qo_indptr, const int64_t *page_indptr, const int32_t *page_ids,
+                      int32_t page_size, int64_t num_pages, int32_t num_kv_heads, int32_t head_dim,
+                      int32_t kv_dtype, const float *k_scale, const float *v_scale,
+                      const uint16_t *k_bits, const double *k_vals, const uint16_t *v_ext,
+                      void *k_pool, void *v_pool)
 {
     int status = 0;
     e4m3_table_init();
@@ -196,12 +236,13 @@ int oracle_store_kv(int32_t num_reqs, const int32_t *prefix_lens, const int32_t 
                     int64_t src = (row * num_kv_heads + h) * (int64_t)head_dim + c;
                     int64_t dst = pool_offset(page, h, slot, c, num_kv_heads, page_size, head_dim);
                     if (kv_dtype == ORACLE_KV_BF16) {
-                        ((uint16_t *)k_pool)[dst] = k_ext[src];
+                        ((uint16_t *)k_pool)[dst] = k_vals ? oracle_bf16_round(k_vals[src]) : k_bits[src];
                         ((uint16_t *)v_pool)[dst] = v_ext[src];
                     } else {
                         float kinv = 1.0f / k_scale[h];
                         float vinv = 1.0f / v_scale[h];
-                        float kx = bf16_to_float(k_ext[src]) * kinv;
+                        float k = k_vals ? (float)k_vals[src] : bf16_to_float(k_bits[src]);
+                        float kx = k * kinv;
                         float vx = bf16_to_float(v_ext[src]) * vinv;
                         ((uint8_t *)k_pool)[dst] = e4m3_encode_nearest(kx);
                         ((uint8_t *)v_pool)[dst] = e4m3_encode_nearest(vx);
@@ -211,6 +252,29 @@ int oracle_store_kv(int32_t num_reqs, const int32_t *prefix_lens, const int32_t 
         }
     }
     return status;
+}
+
+int oracle_store_kv(int32_t num_reqs, const int32_t *prefix_lens, const int32_t *extend_lens,
+                    const int64_t *qo_indptr, const int64_t *page_indptr, const int32_t *page_ids,
+                    int32_t page_size, int64_t num_pages, int32_t num_kv_heads, int32_t head_dim,
+                    int32_t kv_dtype, const float *k_scale, const float *v_scale,
+                    const uint16_t *k_ext, const uint16_t *v_ext, void *k_pool, void *v_pool)
+{
+    return store_rows(num_reqs, prefix_lens, extend_lens, qo_indptr, page_indptr, page_ids, page_size,
+                      num_pages, num_kv_heads, head_dim, kv_dtype, k_scale, v_scale, k_ext, NULL, v_ext,
+                      k_pool, v_pool);
+}
+
+/* The same store with K given as doubles (see store_rows). */
+int oracle_store_kv_f64(int32_t num_reqs, const int32_t *prefix_lens, const int32_t *extend_lens,
+                        const int64_t *qo_indptr, const int64_t *page_indptr, const int32_t *page_ids,
+                        int32_t page_size, int64_t num_pages, int32_t num_kv_heads, int32_t head_dim,
+                        int32_t kv_dtype, const float *k_scale, const float *v_scale,
+                        const double *k_vals, const uint16_t *v_ext, void *k_pool, void *v_pool)
+{
+    return store_rows(num_reqs, prefix_lens, extend_lens, qo_indptr, page_indptr, page_ids, page_size,
+                      num_pages, num_kv_heads, head_dim, kv_dtype, k_scale, v_scale, NULL, k_vals, v_ext,
+                      k_pool, v_pool);
 }
 
 /* ------------------------------------------------------------------- attention */
