@@ -78,7 +78,17 @@ def traffic_from_profiles(config: str):
     return float(m_bytes.group(1))
 
 
-def setup(config: str, seed: int = 0):
+def rope_args(w, dev="cuda"):
+    """Keyword arguments of store_kv_rope for the Qwen3-shaped setting: half-layout
+    rotation of the whole head, base 10^6, RMS norm of every Q and K head."""
+    from paper_2609_32278_amd import workloads as wl
+    spec = wl.RopeSpec(rotary_dim=w.head_dim)
+    qn, kn = wl.norm_weights(w, dev)
+    return dict(theta=spec.theta, rotary_dim=spec.rotary_dim, style=spec.style, q_norm=qn, k_norm=kn,
+                norm_eps=spec.eps)
+
+
+def setup(config: str, seed: int = 0, rope: bool = False):
     import torch
     from paper_2609_32278_amd import kvx
     from paper_2609_32278_amd import workloads as wl
@@ -86,6 +96,7 @@ def setup(config: str, seed: int = 0):
     w = wl.make_workload(config, seed)
     dev = "cuda"
     pool = kvx.kv_pool_create(w.num_pages, w.page_size, w.num_kv_heads, w.head_dim, w.kv_dtype, w.k_scale, w.v_scale)
+    rk = rope_args(w, dev) if rope else None
     qs, ke, ve = [], [], []
     for r in range(w.num_reqs):
         k, v = wl.request_kv(w, r, dev)
@@ -94,7 +105,10 @@ def setup(config: str, seed: int = 0):
             n = (p + w.page_size - 1) // w.page_size
             ids = torch.from_numpy(np.ascontiguousarray(w.pages_of(r)[:n])).to(dev)
             hb = kvx.Batch([0], [p], [0, n], ids)
-            kvx.store_kv(pool, hb, k[:p].contiguous(), v[:p].contiguous())
+            if rope:
+                kvx.store_kv_rope(pool, hb, k[:p].contiguous(), v[:p].contiguous(), **rk)
+            else:
+                kvx.store_kv(pool, hb, k[:p].contiguous(), v[:p].contiguous())
             torch.cuda.synchronize()
         qs.append(wl.request_q(w, r, dev))
         ke.append(k[p:].clone())
@@ -108,24 +122,28 @@ def setup(config: str, seed: int = 0):
     batch = kvx.Batch(w.prefix_lens, w.extend_lens, w.page_indptr, ids)
     out = torch.empty_like(q)
     torch.cuda.synchronize()
-    return dict(w=w, pool=pool, batch=batch, ids=ids, q=q, k_ext=k_ext, v_ext=v_ext, out=out)
+    return dict(w=w, pool=pool, batch=batch, ids=ids, q=q, k_ext=k_ext, v_ext=v_ext, out=out, rope=rk)
 
 
-def run_gpu(config: str, steps: int, warmup: int):
+def run_gpu(config: str, steps: int, warmup: int, rope: bool = False):
     import torch
     from paper_2609_32278_amd import kvx
 
-    s = setup(config)
+    s = setup(config, rope=rope)
     w, pool, batch = s["w"], s["pool"], s["batch"]
     q, k_ext, v_ext, out = s["q"], s["k_ext"], s["v_ext"], s["out"]
+    q_rot = torch.empty_like(q) if rope else q
 
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        kvx.store_kv(pool, batch, k_ext, v_ext)
+        if rope:  # norm + rotate Q and K, store K and V: one fused kernel
+            kvx.store_kv_rope(pool, batch, k_ext, v_ext, q=q, num_q_heads=w.num_q_heads, q_out=q_rot, **s["rope"])
+        else:
+            kvx.store_kv(pool, batch, k_ext, v_ext)
         if ev is not None:
             ev[1].record()
-        kvx.extend_attention(pool, batch, q, w.num_q_heads, w.sm_scale, out)
+        kvx.extend_attention(pool, batch, q_rot, w.num_q_heads, w.sm_scale, out)
         if ev is not None:
             ev[2].record()
 
@@ -197,6 +215,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="llama8b", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--rope", action="store_true",
+                    help="the step's store also RMS-normalises and rotates Q and K (store_kv_rope)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=32)
     ap.add_argument("--cpu-reqs", type=int, default=16)
@@ -227,13 +247,15 @@ def main():
         print(json.dumps({"calib_copy_bytes_read": 4 * n, "calib_copy_bytes_written": 4 * n, "launches": 3}))
         return
 
-    w, ms_step, store_ms, attn_ms = run_gpu(args.config, args.steps, args.warmup)
+    w, ms_step, store_ms, attn_ms = run_gpu(args.config, args.steps, args.warmup, args.rope)
     flops = w.flops()
     T = w.total_extend
     tflops_step = flops / (ms_step * 1e-3) / 1e12
     tflops_attn = flops / (attn_ms * 1e-3) / 1e12
     eb = 2 if w.kv_dtype == 0 else 1
     store_bytes = T * w.num_kv_heads * w.head_dim * 2 * (2 + eb)
+    if args.rope:  # plus Q read and written back rotated
+        store_bytes += T * w.num_q_heads * w.head_dim * 2 * 2
     ctx = int(w.seq_lens.sum())
     attn_alg_bytes = (2 * T * w.num_q_heads * w.head_dim * 2 + 2 * eb * ctx * w.num_kv_heads * w.head_dim
                       + 4 * int(np.ceil(w.seq_lens / 16).sum()))
@@ -252,7 +274,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": f"{args.config}: {DESCRIPTIONS[args.config]}",
+            "workload": f"{args.config}: {DESCRIPTIONS[args.config]}"
+                        + ("; store fused with Q/K RMS norm + RoPE (half layout, base 1e6)" if args.rope else ""),
             "requests": w.num_reqs,
             "uncached_tokens": T,
             "context_tokens": ctx,
@@ -264,6 +287,7 @@ def main():
         "attn_ms": round(attn_ms, 4),
         "attn_tflops": round(tflops_attn, 2),
         "uncached_tokens_per_s_attn_only": round(T / (attn_ms * 1e-3), 1),
+        "store_kernel": "store_kv_rope_kernel" if args.rope else "store_kv_kernel",
         "store_ms": round(store_ms, 4),
         "store_GBps": round(store_bytes / (store_ms * 1e-3) / 1e9, 1),
         "roofline": {

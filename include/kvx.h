@@ -144,6 +144,49 @@ typedef struct {
 int store_kv(kvx_pool *pool, const kvx_batch *batch, const void *k_ext, const void *v_ext,
              kvx_stream_t stream);
 
+/* Layout of the rotation planes of a head (see store_kv_rope). */
+enum {
+    KVX_ROPE_HALF = 0,        /* plane j = dims (j, j + rotary_dim/2): GPT-NeoX, Llama, Qwen */
+    KVX_ROPE_INTERLEAVED = 1  /* plane j = dims (2j, 2j + 1): GPT-J */
+};
+
+typedef struct {
+    double theta;            /* frequency base > 0: plane j turns theta^(-2j/rotary_dim) rad per position */
+    const double *inv_freq;  /* host [rotary_dim/2] rates (rad per position, finite, >= 0) used instead of
+                                theta -- scaled or extended frequency tables -- or NULL; read during the call */
+    int32_t rotary_dim;      /* rotated leading dims of a head: a multiple of 16 in [16, head_dim];
+                                the dims past it pass through */
+    int32_t style;           /* KVX_ROPE_HALF or KVX_ROPE_INTERLEAVED */
+    const void *q_norm;      /* device bf16 [head_dim] RMS-norm weight for every Q head, or NULL: no norm */
+    const void *k_norm;      /* the same for every K head */
+    float norm_eps;          /* finite, >= 0; added to the mean square */
+} kvx_rope;
+
+/*
+ * store_kv with the steps that produce attention's queries and keys fused in.
+ * The paper describes neither step; the models it serves (Section 4) normalise
+ * and rotate Q and K before K is cached.  For suffix token i of request r, at
+ * absolute position t = P_r + i, every Q head and K head row x is
+ *   normalised, when a weight w is given:  y = x * w / sqrt(mean(x^2) + norm_eps)
+ *   (mean over all head_dim dims), then rotated: each plane (a, b) of the first
+ *   rotary_dim dims turns by t * f_j:  (a cos - b sin, a sin + b cos).
+ * The rotated K is stored as store_kv stores K (bf16 round-to-nearest-even, or
+ * e4m3 of float(y) * float(1/scale) on an fp8 pool); V is stored exactly as by
+ * store_kv; the rotated Q goes to q_out as bf16 (round to nearest even).
+ * Arithmetic is float32, with every angle reduced to one turn in float64 first,
+ * and each result is rounded once.
+ *   q, q_out     device bf16 [T, num_q_heads, head_dim]; q_out may be q itself
+ *                (in place) but may not overlap it otherwise; both unused (may be
+ *                NULL) when num_q_heads = 0, which rotates and stores K only
+ *   k_ext, v_ext device bf16 [T, num_kv_heads, head_dim], T = sum E_r (not modified)
+ * Must precede extend_attention of the same batch (which then takes q_out) on the
+ * same stream.  Errors: EINVAL, ERANGE (validation mode), ENOMEM, EHIP.
+ * R = 0 or T = 0: no-op after the argument checks.
+ */
+int store_kv_rope(kvx_pool *pool, const kvx_batch *batch, const kvx_rope *rope, const void *q,
+                  int32_t num_q_heads, void *q_out, const void *k_ext, const void *v_ext,
+                  kvx_stream_t stream);
+
 /*
  * Prefix-extend attention: for each request r, suffix row i and query head hq,
  *   o = softmax_j(sm_scale * q . k_j) v_j  over keys j = 0 .. P_r + i

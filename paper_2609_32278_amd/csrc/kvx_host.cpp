@@ -720,6 +720,82 @@ int store_kv(kvx_pool* pool, const kvx_batch* batch, const void* k_ext, const vo
   return KVX_OK;
 }
 
+int store_kv_rope(kvx_pool* pool, const kvx_batch* batch, const kvx_rope* rope, const void* q, int32_t num_q_heads,
+                  void* q_out, const void* k_ext, const void* v_ext, kvx_stream_t stream) {
+  g_last_error.clear();
+  if (int rc = check_pool(pool)) return rc;
+  std::vector<int64_t> qo;
+  if (int rc = check_batch(batch, qo)) return rc;
+  if (rope == nullptr) return fail(KVX_EINVAL, "rope is NULL");
+  const int D = pool->head_dim;
+  const int rd = rope->rotary_dim;
+  if (rd < 16 || rd > D || rd % 16 != 0)
+    return fail(KVX_EINVAL, "rotary_dim = %d must be a multiple of 16 in [16, head_dim = %d]", rd, D);
+  if (rope->style != KVX_ROPE_HALF && rope->style != KVX_ROPE_INTERLEAVED)
+    return fail(KVX_EINVAL, "style = %d", rope->style);
+  if (!(rope->norm_eps >= 0.0f) || !std::isfinite(rope->norm_eps))
+    return fail(KVX_EINVAL, "norm_eps must be finite and >= 0");
+  kvx::RopeParams p{};
+  for (int j = 0; j < rd / 2; j++) {
+    double f;
+    if (rope->inv_freq) {
+      f = rope->inv_freq[j];
+      if (!(f >= 0.0) || !std::isfinite(f)) return fail(KVX_EINVAL, "inv_freq[%d] must be finite and >= 0", j);
+    } else {
+      if (!(rope->theta > 0.0) || !std::isfinite(rope->theta))
+        return fail(KVX_EINVAL, "theta must be finite and > 0");
+      f = std::pow(rope->theta, -2.0 * j / rd);
+    }
+    p.rev_freq[j] = f / 6.283185307179586476925286766559;  // turns per position
+  }
+  if (num_q_heads < 0) return fail(KVX_EINVAL, "num_q_heads = %d < 0", num_q_heads);
+  if (num_q_heads > 0 && (!q || !q_out)) return fail(KVX_EINVAL, "q and q_out must be non-NULL");
+  if (qo.back() == 0) return KVX_OK;
+  if (!k_ext || !v_ext) return fail(KVX_EINVAL, "k_ext and v_ext must be non-NULL");
+  if (int rc = use_device(pool)) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  if (validate_mode())
+    if (int rc = check_page_ids(pool, batch, s)) return rc;
+  std::vector<kvx::RopeUnit> units;
+  const int S = kvx::kPageSize;
+  for (int r = 0; r < batch->num_reqs; r++) {
+    const int64_t P = batch->prefix_lens[r], E = batch->extend_lens[r];
+    if (E == 0) continue;
+    const int64_t L = P + E;
+    for (int64_t lp = P / S; lp <= (L - 1) / S; lp++) {
+      kvx::RopeUnit u;
+      u.row_slot0 = (int32_t)(qo[(size_t)r] + lp * S - P);
+      u.page_pos = (int32_t)(batch->page_indptr[r] + lp);
+      u.slot_begin = (int32_t)(std::max<int64_t>(P, lp * S) - lp * S);
+      u.slot_end = (int32_t)(std::min<int64_t>(L, lp * S + S) - lp * S);
+      u.pos_slot0 = (int32_t)(lp * S);
+      units.push_back(u);
+    }
+  }
+  void* units_d = nullptr;
+  if (int rc = pool->st_store.upload(units.data(), units.size() * sizeof(kvx::RopeUnit), s, &units_d)) return rc;
+  p.q = (const uint16_t*)q;
+  p.q_out = (uint16_t*)q_out;
+  p.k_ext = (const uint16_t*)k_ext;
+  p.v_ext = (const uint16_t*)v_ext;
+  p.k_pool = pool->k;
+  p.v_pool = pool->v;
+  p.page_ids = batch->page_ids;
+  p.units = (const kvx::RopeUnit*)units_d;
+  p.k_inv_scale = pool->scales_d ? pool->scales_d + 2 * pool->num_kv_heads : nullptr;
+  p.v_inv_scale = pool->scales_d ? pool->scales_d + 3 * pool->num_kv_heads : nullptr;
+  p.q_norm = (const uint16_t*)rope->q_norm;
+  p.k_norm = (const uint16_t*)rope->k_norm;
+  p.num_q_heads = num_q_heads;
+  p.num_kv_heads = pool->num_kv_heads;
+  p.rotary_dim = rd;
+  p.norm_eps = rope->norm_eps;
+  hipError_t e = kvx::launch_store_kv_rope(p, (int64_t)units.size(), D, pool->kv_dtype == KVX_KV_FP8_E4M3,
+                                           rope->style == KVX_ROPE_INTERLEAVED, s);
+  if (e != hipSuccess) return hip_fail(e, "store_kv_rope kernel launch");
+  return KVX_OK;
+}
+
 int extend_attention_plan(const kvx_batch* batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                           kvx_work_item* items, int64_t cap, int64_t* count) {
   g_last_error.clear();

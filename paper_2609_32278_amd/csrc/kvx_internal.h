@@ -86,6 +86,37 @@ struct StoreParams {
   int32_t num_kv_heads;
 };
 
+// One fused-store workgroup: a StoreUnit plus the absolute position of slot 0.
+struct RopeUnit {
+  int32_t row_slot0;
+  int32_t page_pos;
+  int32_t slot_begin;
+  int32_t slot_end;
+  int32_t pos_slot0;  // position t of slot 0 of the page (a multiple of 16)
+};
+
+constexpr int kRopeMaxPlanes = 64;  // rotary_dim / 2 <= head_dim / 2
+
+struct RopeParams {
+  const uint16_t* q;      // bf16 [T, Hq, D], or null when num_q_heads == 0
+  uint16_t* q_out;        // may equal q
+  const uint16_t* k_ext;  // bf16 [T, Hkv, D]
+  const uint16_t* v_ext;
+  void* k_pool;
+  void* v_pool;
+  const int32_t* page_ids;
+  const RopeUnit* units;
+  const float* k_inv_scale;  // fp8 pool: device [Hkv], fp32 1/scale
+  const float* v_inv_scale;
+  const uint16_t* q_norm;    // bf16 [D] RMS-norm weights, or null
+  const uint16_t* k_norm;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t rotary_dim;        // multiple of 16, <= D
+  float norm_eps;
+  double rev_freq[kRopeMaxPlanes];  // plane rate in revolutions per position: f_j / (2 pi)
+};
+
 struct PageIoParams {
   const int32_t* page_ids;  // device [n]
   void* k_pool;
@@ -159,6 +190,8 @@ hipError_t launch_extend_attention(const AttnParams& p, int64_t n_units, int hea
 hipError_t launch_merge(const MergeParams& p, int64_t n_merges, int head_dim, hipStream_t stream);
 hipError_t launch_store_kv(const StoreParams& p, int64_t n_units, int head_dim, bool fp8,
                            hipStream_t stream);
+hipError_t launch_store_kv_rope(const RopeParams& p, int64_t n_units, int head_dim, bool fp8, bool interleaved,
+                                hipStream_t stream);
 hipError_t launch_page_io(const PageIoParams& p, int64_t n_pages, int head_dim, int elem_bytes,
                           hipStream_t stream);
 

@@ -30,6 +30,54 @@ __device__ __forceinline__ uint32_t e4m3x4(float a, float b, float c, float d) {
   return (uint32_t)r;
 }
 
+// Write the staged V rows vs[slot][dim] of one (page, head) block as the pool's
+// [dim][slot] columns, 8 slots per thread and step (16 bytes bf16 / 8 bytes fp8);
+// only slots in [slot_begin, slot_end) are written.
+template <int D, bool FP8>
+__device__ __forceinline__ void write_vt(const uint16_t (&vs)[kPageSize][D + 8], void* v_pool, size_t blk,
+                                         int slot_begin, int slot_end, float vinv) {
+  const bool full = slot_begin == 0 && slot_end == kPageSize;
+  for (int c = threadIdx.x; c < 2 * D; c += kStoreThreads) {
+    const int d = c / 2, half = c % 2;
+    const int s0 = half * 8;
+    if (s0 + 8 <= slot_begin || s0 >= slot_end) continue;
+    float x[8];
+    uint16_t raw[8];
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+      raw[e] = vs[s0 + e][d];
+      x[e] = bf16_to_f32(raw[e]) * vinv;
+    }
+    const bool whole = full || (s0 >= slot_begin && s0 + 8 <= slot_end);
+    if constexpr (FP8) {
+      uint8_t* dst = (uint8_t*)v_pool + blk + (size_t)d * kPageSize + s0;
+      uint2 code;
+      code.x = e4m3x4(x[0], x[1], x[2], x[3]);
+      code.y = e4m3x4(x[4], x[5], x[6], x[7]);
+      if (whole) {
+        *(uint2*)dst = code;
+      } else {
+        const uint8_t* cb = (const uint8_t*)&code;
+        for (int e = 0; e < 8; e++)
+          if (s0 + e >= slot_begin && s0 + e < slot_end) dst[e] = cb[e];
+      }
+    } else {
+      uint16_t* dst = (uint16_t*)v_pool + blk + (size_t)d * kPageSize + s0;
+      if (whole) {
+        uint4 w;
+        w.x = raw[0] | ((uint32_t)raw[1] << 16);
+        w.y = raw[2] | ((uint32_t)raw[3] << 16);
+        w.z = raw[4] | ((uint32_t)raw[5] << 16);
+        w.w = raw[6] | ((uint32_t)raw[7] << 16);
+        *(uint4*)dst = w;
+      } else {
+        for (int e = 0; e < 8; e++)
+          if (s0 + e >= slot_begin && s0 + e < slot_end) dst[e] = raw[e];
+      }
+    }
+  }
+}
+
 template <int D, bool FP8>
 __global__ __launch_bounds__(kStoreThreads) void store_kv_kernel(StoreParams p) {
   // V rows of this page for one head, staged for the transpose: [16 slots][D] bf16
@@ -39,7 +87,6 @@ __global__ __launch_bounds__(kStoreThreads) void store_kv_kernel(StoreParams p) 
   const int H = p.num_kv_heads;
   constexpr int CPR = D / 8;                // 16-byte chunks per bf16 row
   constexpr int CHUNKS = kPageSize * CPR;   // per head
-  const bool full = su.slot_begin == 0 && su.slot_end == kPageSize;
 
   for (int hd = 0; hd < H; hd++) {
     const float kinv = FP8 ? p.k_inv_scale[hd] : 1.0f;
@@ -68,46 +115,201 @@ __global__ __launch_bounds__(kStoreThreads) void store_kv_kernel(StoreParams p) 
       *(uint4*)(&vs[slot][cc * 8]) = vx;
     }
     __syncthreads();
-    // V^T: dim d, slots [8*half, 8*half+8)
-    for (int c = threadIdx.x; c < 2 * D; c += kStoreThreads) {
-      const int d = c / 2, half = c % 2;
-      const int s0 = half * 8;
-      if (s0 + 8 <= su.slot_begin || s0 >= su.slot_end) continue;
-      float x[8];
-      uint16_t raw[8];
-#pragma unroll
-      for (int e = 0; e < 8; e++) {
-        raw[e] = vs[s0 + e][d];
-        x[e] = bf16_to_f32(raw[e]) * vinv;
-      }
-      const bool whole = full || (s0 >= su.slot_begin && s0 + 8 <= su.slot_end);
-      if constexpr (FP8) {
-        uint8_t* dst = (uint8_t*)p.v_pool + blk + (size_t)d * kPageSize + s0;
-        uint2 code;
-        code.x = e4m3x4(x[0], x[1], x[2], x[3]);
-        code.y = e4m3x4(x[4], x[5], x[6], x[7]);
-        if (whole) {
-          *(uint2*)dst = code;
-        } else {
-          const uint8_t* cb = (const uint8_t*)&code;
-          for (int e = 0; e < 8; e++)
-            if (s0 + e >= su.slot_begin && s0 + e < su.slot_end) dst[e] = cb[e];
-        }
-      } else {
-        uint16_t* dst = (uint16_t*)p.v_pool + blk + (size_t)d * kPageSize + s0;
-        if (whole) {
-          uint4 w;
-          w.x = raw[0] | ((uint32_t)raw[1] << 16);
-          w.y = raw[2] | ((uint32_t)raw[3] << 16);
-          w.z = raw[4] | ((uint32_t)raw[5] << 16);
-          w.w = raw[6] | ((uint32_t)raw[7] << 16);
-          *(uint4*)dst = w;
-        } else {
-          for (int e = 0; e < 8; e++)
-            if (s0 + e >= su.slot_begin && s0 + e < su.slot_end) dst[e] = raw[e];
-        }
-      }
+    write_vt<D, FP8>(vs, p.v_pool, blk, su.slot_begin, su.slot_end, vinv);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------- fused RoPE store
+//
+// The step before attention, fused into the store (the models the paper serves
+// normalise and rotate Q and K before K is cached; the paper itself describes
+// neither step): every Q and K head row of the unit's tokens is optionally
+// RMS-normalised, rotated by its absolute position, and then written -- Q to
+// q_out as bf16, K into the pool as store_kv would store it.  V is stored as by
+// store_kv.  Arithmetic is fp32; each angle is reduced to [-pi, pi] in fp64 from
+// the plane's rate in revolutions per position, so positions far past 2^24
+// keep full precision.  Results are rounded once (RNE bf16 or e4m3).
+//
+// A head row of D bf16 values is D/8 16-byte chunks held by D/8 consecutive
+// lanes; the RMS sum is reduced across those lanes, and in the half layout a
+// chunk of the first half meets its plane partners in the chunk rotary_dim/16
+// lanes further on (one lane shuffle per value).
+
+constexpr int kRopeBatch = 4;  // chunks per thread loaded before any is processed
+
+template <int D, bool INTERLEAVED>
+struct RopeLane {
+  static constexpr int CPR = D / 8;
+  int cc;           // chunk of the row this lane handles (fixed for the thread)
+  int partner;      // lane holding the plane partners (half layout)
+  int jb;           // first plane of the chunk
+  bool rot;         // the chunk lies inside rotary_dim
+  float sgn;        // half layout: -1 for the plane's first dims, +1 for its second
+
+  __device__ RopeLane(int rotary_dim) {
+    cc = threadIdx.x % CPR;
+    const int lane = threadIdx.x & 63;
+    if constexpr (INTERLEAVED) {
+      rot = cc < (rotary_dim >> 3);
+      jb = 4 * cc;
+      partner = lane;
+      sgn = 0.0f;
+    } else {
+      const int r16 = rotary_dim >> 4;
+      const bool first = cc < r16;
+      rot = cc < 2 * r16;
+      jb = first ? 8 * cc : 8 * (cc - r16);
+      partner = lane + (first ? r16 : (rot ? -r16 : 0));
+      sgn = first ? -1.0f : 1.0f;
     }
+  }
+};
+
+// x: the 8 values of this lane's chunk of one row at `slot`; in place -> rotated.
+// Every lane of the row must execute this (shuffles).
+template <int D, bool INTERLEAVED>
+__device__ __forceinline__ void rope_chunk(float (&x)[8], const RopeLane<D, INTERLEAVED>& rl,
+                                           const float2* cs_slot) {
+  if constexpr (INTERLEAVED) {
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const float2 t = rl.rot ? cs_slot[rl.jb + i] : make_float2(1.0f, 0.0f);
+      const float a = x[2 * i], b = x[2 * i + 1];
+      x[2 * i] = a * t.x - b * t.y;
+      x[2 * i + 1] = a * t.y + b * t.x;
+    }
+  } else {
+    float pe[8];
+#pragma unroll
+    for (int e = 0; e < 8; e++) pe[e] = __shfl(x[e], rl.partner, 64);
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+      const float2 t = rl.rot ? cs_slot[rl.jb + e] : make_float2(1.0f, 0.0f);
+      // first dims: a cos - b sin (b = partner); second dims: b cos + a sin (a = partner)
+      x[e] = x[e] * t.x + rl.sgn * (pe[e] * t.y);
+    }
+  }
+}
+
+// Normalise and rotate the n_rows head rows at src ([row][D] bf16; row = tok *
+// heads + head, token tok at slot slot_begin + tok) and hand each chunk's
+// results to out(row, chunk, y).
+template <int D, bool INTERLEAVED, class Out>
+__device__ __forceinline__ void rope_rows(const uint16_t* __restrict__ src, int n_rows, int heads,
+                                          int slot_begin, const float2 (*cs)[kRopeMaxPlanes],
+                                          const uint16_t* norm_w, float eps, int rotary_dim, Out&& out) {
+  constexpr int CPR = D / 8;
+  const int n = n_rows * CPR;
+  const RopeLane<D, INTERLEAVED> rl(rotary_dim);
+  float w[8];
+  if (norm_w) {
+    const uint4 wr = *(const uint4*)(norm_w + rl.cc * 8);
+    const uint16_t* wh = (const uint16_t*)&wr;
+#pragma unroll
+    for (int e = 0; e < 8; e++) w[e] = bf16_to_f32(wh[e]);
+  }
+  for (int c0 = threadIdx.x; c0 < n; c0 += kRopeBatch * kStoreThreads) {
+    uint4 raw[kRopeBatch];
+#pragma unroll
+    for (int b = 0; b < kRopeBatch; b++) {
+      const int c = c0 + b * kStoreThreads;
+      raw[b] = c < n ? *(const uint4*)(src + (size_t)c * 8) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int b = 0; b < kRopeBatch; b++) {
+      const int c = c0 + b * kStoreThreads;
+      const int row = c / CPR;
+      const uint16_t* h16 = (const uint16_t*)&raw[b];
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; e++) x[e] = bf16_to_f32(h16[e]);
+      if (norm_w) {
+        float ss = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; e++) ss = fmaf(x[e], x[e], ss);
+#pragma unroll
+        for (int m = 1; m < CPR; m <<= 1) ss += __shfl_xor(ss, m, 64);
+        const float inv = 1.0f / sqrtf(ss * (1.0f / D) + eps);
+#pragma unroll
+        for (int e = 0; e < 8; e++) x[e] = (x[e] * inv) * w[e];
+      }
+      const int slot = slot_begin + (c < n ? row / heads : 0);
+      rope_chunk<D, INTERLEAVED>(x, rl, cs[slot]);
+      if (c < n) out(row, rl.cc, x);
+    }
+  }
+}
+
+__device__ __forceinline__ uint4 pack_bf16x8(const float (&y)[8]) {
+  uint4 r;
+  uint32_t* w = (uint32_t*)&r;
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const __bf16 lo = (__bf16)y[2 * i], hi = (__bf16)y[2 * i + 1];
+    w[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+  }
+  return r;
+}
+
+template <int D, bool FP8, bool INTERLEAVED>
+__global__ __launch_bounds__(kStoreThreads) void store_kv_rope_kernel(RopeParams p) {
+  __shared__ float2 cs[kPageSize][kRopeMaxPlanes];  // (cos, sin) of every live slot and plane
+  __shared__ __attribute__((aligned(16))) uint16_t vs[kPageSize][D + 8];
+  const RopeUnit u = p.units[blockIdx.x];
+  const int page = p.page_ids[u.page_pos];
+  const int planes = p.rotary_dim / 2;
+  const int ntok = u.slot_end - u.slot_begin;
+
+  for (int e = threadIdx.x; e < ntok * planes; e += kStoreThreads) {
+    const int s = u.slot_begin + e / planes, j = e % planes;
+    double rev = (double)(u.pos_slot0 + s) * p.rev_freq[j];  // exact position times the rate
+    rev -= rint(rev);                                          // [-1/2, 1/2] turn, exact
+    float sn, cn;
+    sincospif(2.0f * (float)rev, &sn, &cn);
+    cs[s][j] = make_float2(cn, sn);
+  }
+  __syncthreads();
+
+  constexpr int CPR = D / 8;
+  const int Hq = p.num_q_heads, H = p.num_kv_heads;
+  const int row0 = u.row_slot0 + u.slot_begin;  // first suffix row of the unit
+  if (Hq > 0) {
+    const size_t base = (size_t)row0 * Hq * D;
+    uint16_t* qo = p.q_out + base;
+    rope_rows<D, INTERLEAVED>(p.q + base, ntok * Hq, Hq, u.slot_begin, cs, p.q_norm, p.norm_eps, p.rotary_dim,
+                              [&](int row, int cc, const float(&y)[8]) {
+                                *(uint4*)(qo + (size_t)row * D + cc * 8) = pack_bf16x8(y);
+                              });
+  }
+  rope_rows<D, INTERLEAVED>(
+      p.k_ext + (size_t)row0 * H * D, ntok * H, H, u.slot_begin, cs, p.k_norm, p.norm_eps, p.rotary_dim,
+      [&](int row, int cc, const float(&y)[8]) {
+        const int hd = row % H, slot = u.slot_begin + row / H;
+        const size_t blk = ((size_t)page * H + hd) * (size_t)(kPageSize * D);
+        if constexpr (FP8) {
+          const float kinv = p.k_inv_scale[hd];
+          uint2 code;
+          code.x = e4m3x4(y[0] * kinv, y[1] * kinv, y[2] * kinv, y[3] * kinv);
+          code.y = e4m3x4(y[4] * kinv, y[5] * kinv, y[6] * kinv, y[7] * kinv);
+          *(uint2*)((uint8_t*)p.k_pool + blk + (size_t)slot * D + cc * 8) = code;
+        } else {
+          *(uint4*)((uint16_t*)p.k_pool + blk + (size_t)slot * D + cc * 8) = pack_bf16x8(y);
+        }
+      });
+
+  // V: staged per head in LDS and written as [dim][slot] columns
+  for (int hd = 0; hd < H; hd++) {
+    for (int c = threadIdx.x; c < kPageSize * CPR; c += kStoreThreads) {
+      const int slot = c / CPR, cc = c % CPR;
+      uint4 vx = make_uint4(0, 0, 0, 0);
+      if (slot >= u.slot_begin && slot < u.slot_end)
+        vx = *(const uint4*)(p.v_ext + ((size_t)(u.row_slot0 + slot) * H + hd) * D + cc * 8);
+      *(uint4*)(&vs[slot][cc * 8]) = vx;
+    }
+    __syncthreads();
+    const size_t blk = ((size_t)page * H + hd) * (size_t)(kPageSize * D);
+    write_vt<D, FP8>(vs, p.v_pool, blk, u.slot_begin, u.slot_end, FP8 ? p.v_inv_scale[hd] : 1.0f);
     __syncthreads();
   }
 }
@@ -169,6 +371,22 @@ hipError_t launch_store_kv(const StoreParams& p, int64_t n_units, int head_dim, 
     if (fp8) hipLaunchKernelGGL((store_kv_kernel<64, true>), grid, block, 0, stream, p);
     else hipLaunchKernelGGL((store_kv_kernel<64, false>), grid, block, 0, stream, p);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_store_kv_rope(const RopeParams& p, int64_t n_units, int head_dim, bool fp8, bool interleaved,
+                                hipStream_t stream) {
+  if (n_units <= 0) return hipSuccess;
+  dim3 grid((unsigned)n_units), block(kStoreThreads);
+#define KVX_ROPE_LAUNCH(D, F, I) hipLaunchKernelGGL((store_kv_rope_kernel<D, F, I>), grid, block, 0, stream, p)
+  if (head_dim == 128) {
+    if (fp8) { if (interleaved) KVX_ROPE_LAUNCH(128, true, true); else KVX_ROPE_LAUNCH(128, true, false); }
+    else { if (interleaved) KVX_ROPE_LAUNCH(128, false, true); else KVX_ROPE_LAUNCH(128, false, false); }
+  } else {
+    if (fp8) { if (interleaved) KVX_ROPE_LAUNCH(64, true, true); else KVX_ROPE_LAUNCH(64, true, false); }
+    else { if (interleaved) KVX_ROPE_LAUNCH(64, false, true); else KVX_ROPE_LAUNCH(64, false, false); }
+  }
+#undef KVX_ROPE_LAUNCH
   return hipGetLastError();
 }
 

@@ -24,10 +24,11 @@ STATUS_NAMES = {0: "KVX_OK", 1: "KVX_EINVAL", 2: "KVX_ENOMEM", 3: "KVX_ERANGE",
                 4: "KVX_EUNSUPPORTED", 5: "KVX_EHIP"}
 
 KVX_EVICT_LRU, KVX_EVICT_RR = 0, 1
+KVX_ROPE_HALF, KVX_ROPE_INTERLEAVED = 0, 1
 
 # Every symbol include/kvx.h and include/kvx_cache.h declare.
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_layout", "kv_pool_write_pages",
-           "kv_pool_read_pages", "store_kv", "extend_attention", "extend_attention_plan",
+           "kv_pool_read_pages", "store_kv", "store_kv_rope", "extend_attention", "extend_attention_plan",
            "kvx_set_split_keys", "kvx_last_error",
            "kvx_cache_create", "kvx_cache_destroy", "kvx_cache_begin_turn", "kvx_cache_end_turn",
            "kvx_cache_complete", "kvx_cache_agent", "kvx_cache_stats"]
@@ -58,6 +59,12 @@ class kvx_pool_layout(ctypes.Structure):
                 ("v_stride_page", ctypes.c_int64), ("v_stride_head", ctypes.c_int64),
                 ("v_stride_slot", ctypes.c_int64), ("v_stride_dim", ctypes.c_int64),
                 ("k_scale", ctypes.c_void_p), ("v_scale", ctypes.c_void_p)]
+
+
+class kvx_rope(ctypes.Structure):
+    _fields_ = [("theta", ctypes.c_double), ("inv_freq", ctypes.c_void_p), ("rotary_dim", ctypes.c_int32),
+                ("style", ctypes.c_int32), ("q_norm", ctypes.c_void_p), ("k_norm", ctypes.c_void_p),
+                ("norm_eps", ctypes.c_float)]
 
 
 class kvx_work_item(ctypes.Structure):
@@ -91,6 +98,7 @@ def lib():
             "kv_pool_write_pages": [P, P, i64, P, P, P],
             "kv_pool_read_pages": [P, P, i64, P, P, P],
             "store_kv": [P, ctypes.POINTER(kvx_batch), P, P, P],
+            "store_kv_rope": [P, ctypes.POINTER(kvx_batch), ctypes.POINTER(kvx_rope), P, i32, P, P, P, P],
             "extend_attention": [P, ctypes.POINTER(kvx_batch), P, i32, f32, P, P, P],
             "extend_attention_plan": [ctypes.POINTER(kvx_batch), i32, i32, i32, P, i64, ctypes.POINTER(i64)],
             "kvx_set_split_keys": [i32],
@@ -202,6 +210,17 @@ def kv_pool_read_pages(pool, page_ids, k_dst, v_dst, stream=None) -> None:
 
 def store_kv(pool, batch: Batch, k_ext, v_ext, stream=None) -> None:
     _check(lib().store_kv(pool, ctypes.byref(batch.c), _dptr(k_ext), _dptr(v_ext), _stream(stream)), "store_kv")
+
+
+def store_kv_rope(pool, batch: Batch, k_ext, v_ext, *, theta: float = 10000.0, rotary_dim: int, style: int = 0,
+                  q=None, num_q_heads: int = 0, q_out=None, q_norm=None, k_norm=None, norm_eps: float = 1e-6,
+                  inv_freq=None, stream=None) -> None:
+    """store_kv with RMS norm (optional) and rotary embedding of Q and K fused in."""
+    freqs = None if inv_freq is None else np.ascontiguousarray(inv_freq, dtype=np.float64)
+    r = kvx_rope(float(theta), None if freqs is None else freqs.ctypes.data, int(rotary_dim), int(style),
+                 _dptr(q_norm), _dptr(k_norm), float(norm_eps))
+    _check(lib().store_kv_rope(pool, ctypes.byref(batch.c), ctypes.byref(r), _dptr(q), int(num_q_heads),
+                               _dptr(q_out), _dptr(k_ext), _dptr(v_ext), _stream(stream)), "store_kv_rope")
 
 
 def extend_attention(pool, batch: Batch, q, num_q_heads: int, sm_scale: float, out, lse=None, stream=None) -> None:

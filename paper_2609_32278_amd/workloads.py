@@ -17,7 +17,9 @@ Generation order (fixed, so every draw is reproducible):
   * ``numpy.random.default_rng([config_id, 0, seed])`` draws the lengths, then
     one permutation of the pool's pages, then the fp8 K scales and V scales.
   * Each request's values come from torch generators seeded by
-    ``SeedSequence([config_id, 1, seed, kind, r])`` with kind 0 = Q, 1 = K, 2 = V.
+    ``SeedSequence([config_id, 1, seed, kind, r])`` with kind 0 = Q, 1 = K, 2 = V;
+    the RMS-norm weights of the fused RoPE store from ``SeedSequence([config_id,
+    2, seed, kind])`` with kind 0 = Q, 1 = K, uniform in [0.5, 1.5].
     Values are drawn as fp32 N(0, sigma^2) and rounded to bf16 (RNE); the bf16
     values *are* the inputs.  The values depend on the device type the
     generator runs on (torch's CPU and GPU generators differ), so a test always
@@ -291,6 +293,30 @@ def request_kv(w: Workload, r: int, device="cpu"):
     k = _randn_bf16(shape, w.sigma, _torch_seed(w.config_id, 1, w.seed, 1, w.value_id(r)), device)
     v = _randn_bf16(shape, w.sigma, _torch_seed(w.config_id, 1, w.seed, 2, w.value_id(r)), device)
     return k, v
+
+
+@dataclasses.dataclass(frozen=True)
+class RopeSpec:
+    """Rotary-embedding and Q/K-norm settings of the fused store (plain data).
+    The default is shaped like the Qwen3 models the paper serves: half-layout
+    rotation of the whole head with base 10^6, and an RMS norm of every Q and K
+    head before it."""
+    theta: float = 1e6
+    rotary_dim: int = 128
+    style: int = 0          # 0: half layout, 1: interleaved
+    norm: bool = True
+    eps: float = 1e-6
+
+
+def norm_weights(w: Workload, device="cpu"):
+    """RMS-norm weights (q_norm, k_norm), bf16 [d] each, uniform in [0.5, 1.5]."""
+    out = []
+    for kind in (0, 1):
+        g = torch.Generator(device=torch.device(device))
+        g.manual_seed(_torch_seed(w.config_id, 2, w.seed, kind))
+        x = torch.rand((w.head_dim,), generator=g, device=torch.device(device), dtype=torch.float32)
+        out.append((0.5 + x).to(torch.bfloat16))
+    return out[0], out[1]
 
 
 def batch_tensors(w: Workload, device="cpu", reqs: Optional[Sequence[int]] = None):

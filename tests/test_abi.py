@@ -63,6 +63,7 @@ def test_pool_argument_errors():
 def test_hot_path_argument_errors_before_any_device_work():
     b = kvx.Batch([16], [4], [0, 2], 0x1000)
     assert _err(kvx.store_kv, None, b, 1, 1) == kvx.KVX_EINVAL
+    assert _err(lambda: kvx.store_kv_rope(None, b, 1, 1, rotary_dim=64)) == kvx.KVX_EINVAL
     assert _err(kvx.extend_attention, None, b, 1, 4, 0.125, 1) == kvx.KVX_EINVAL
     # plan-level checks
     assert _err(kvx.extend_attention_plan, b, 6, 4, 128) == kvx.KVX_EINVAL      # 6 % 4 != 0
