@@ -34,6 +34,22 @@ takes; each is listed in DESIGN.md):
    one reclamation to the next.
 6. LRU ties (equal stamps cannot happen with a strictly increasing clock) would
    go to the smaller agent id.
+
+Host tier (the paper's future work, Section 6: spill idle state to CPU memory
+instead of dropping it), when ``host_pages`` > 0:
+
+7. An idle agent's history is its device pages followed by its host pages, in
+   logical order; the host pages continue the device prefix without a gap.
+8. Pages the device policy evicts are spilled to host records, farthest page
+   first (so within an agent, older records are always farther pages).  A
+   spill that finds no free record first drops the oldest record whose owner
+   is idle -- that owner's farthest host page.  If every record belongs to an
+   active agent, the page is dropped instead.
+9. A turn start reuses device pages, then host pages, up to reading 3's limit;
+   the reused host pages are reloaded into freshly allocated device pages (they
+   are pinned while the turn allocates) and their records freed.  Pages past
+   the limit are dropped, host pages first.  An agent inside a turn holds no
+   host pages.
 """
 
 from __future__ import annotations
@@ -48,6 +64,7 @@ class NoMemory(Exception):
 class _Agent:
     def __init__(self) -> None:
         self.nodes: list[int] = []  # pages per node, root .. leaf
+        self.host: list[int] = []   # host record ids, nearest page first
         self.active = False
         self.stamp = 0
         self.prompt_len = 0
@@ -62,8 +79,15 @@ class OracleCache:
     LRU = 0
     RR = 1
 
-    def __init__(self, num_pages: int, page_size: int, chunk_tokens: int, policy: int) -> None:
-        assert page_size == 16 and chunk_tokens % page_size == 0 and chunk_tokens > 0
+    def __init__(self, num_pages: int, page_size: int, chunk_tokens: int, policy: int, host_pages: int = 0) -> None:
+        assert page_size == 16 and chunk_tokens % page_size == 0 and chunk_tokens > 0 and host_pages >= 0
+        self.host_pages = host_pages
+        self.records: list[tuple[int, int]] = []  # live host records (id, owner), oldest first
+        self.next_record = 0
+        self.spilled_pages = 0
+        self.reloaded_pages = 0
+        self.host_dropped_pages = 0
+        self.last_moves = (0, 0)  # (spills, reloads) of the last turn start
         self.num_pages = num_pages
         self.page_size = page_size
         self.chunk = chunk_tokens // page_size
@@ -85,6 +109,39 @@ class OracleCache:
             self.free += k
             n -= k
 
+    def _forget(self, rec: int) -> None:
+        self.records = [(r, o) for r, o in self.records if r != rec]
+
+    def _host_record(self) -> int | None:
+        """A free host record, dropping the oldest idle-owned one if none is free."""
+        if len(self.records) < self.host_pages:
+            self.next_record += 1
+            return self.next_record
+        for rec, owner in self.records:
+            o = self.agents[owner]
+            if not o.active:
+                assert o.host[-1] == rec  # the owner's farthest host page
+                o.host.pop()
+                self._forget(rec)
+                self.host_dropped_pages += 1
+                self.next_record += 1
+                return self.next_record
+        return None
+
+    def _evict(self, agent_id: int, a: _Agent, n: int) -> None:
+        """Device eviction of a's last n pages; spilled to the host tier if there is one."""
+        self._drop_tail(a, n)
+        if self.host_pages == 0:
+            return
+        for _ in range(n):  # farthest page first
+            rec = self._host_record()
+            if rec is None:
+                continue  # dropped (the agent has no host pages: nothing past it is lost)
+            a.host.insert(0, rec)
+            self.records.append((rec, agent_id))
+            self.spilled_pages += 1
+            self.moves_spill += 1
+
     def _evictable(self, agent_id: int) -> bool:
         a = self.agents.get(agent_id)
         return a is not None and not a.active and a.pages > 0
@@ -104,7 +161,7 @@ class OracleCache:
                 continue
             a = self.agents[tau]
             c = min(self.chunk, a.nodes[-1], M - freed)  # SelectTailChunk(tau, M - M_freed)
-            self._drop_tail(a, c)  # Evict(c)
+            self._evict(tau, a, c)  # Evict(c)
             freed += c
             self.evicted_pages += c
             self.evictions += 1
@@ -122,7 +179,7 @@ class OracleCache:
             _, victim = min(leaves)
             a = self.agents[victim]
             n = a.nodes[-1]
-            self._drop_tail(a, n)
+            self._evict(victim, a, n)
             freed += n
             self.evicted_pages += n
             self.evictions += 1
@@ -134,9 +191,21 @@ class OracleCache:
         assert not a.active
         self.clock += 1
         a.stamp = self.clock
-        reuse = min(a.pages, (prompt_len - 1) // self.page_size)
-        self._drop_tail(a, a.pages - reuse)
-        need = -(-prompt_len // self.page_size) - reuse
+        self.moves_spill = 0
+        self.last_moves = (0, 0)
+        limit = (prompt_len - 1) // self.page_size
+        reuse = min(a.pages + len(a.host), limit)
+        if reuse < a.pages:  # past the limit: host pages go first, then device pages
+            for rec in a.host:
+                self._forget(rec)
+            a.host = []
+            self._drop_tail(a, a.pages - reuse)
+        else:
+            for rec in a.host[reuse - a.pages:]:
+                self._forget(rec)
+            a.host = a.host[: reuse - a.pages]
+        reload = len(a.host)
+        need = -(-prompt_len // self.page_size) - a.pages  # reloaded pages + new pages
         a.active = True
         if self.free < need:
             if self.policy == self.RR:
@@ -145,8 +214,14 @@ class OracleCache:
                 self._reclaim_lru(need - self.free)
         if self.free < need:
             a.active = False
+            self.last_moves = (self.moves_spill, 0)
             raise NoMemory(agent_id)
         self.free -= need
+        for rec in a.host:
+            self._forget(rec)
+        a.host = []
+        self.reloaded_pages += reload
+        self.last_moves = (self.moves_spill, reload)
         a.turn_pages = need
         a.prompt_len = prompt_len
         return reuse * self.page_size
@@ -167,8 +242,18 @@ class OracleCache:
         a = self.agents[agent_id]
         assert not a.active
         self._drop_tail(a, a.pages)
+        for rec in a.host:
+            self._forget(rec)
         del self.agents[agent_id]
 
     def cached_tokens(self, agent_id: int) -> int:
         a = self.agents.get(agent_id)
         return 0 if a is None else a.pages * self.page_size
+
+    def host_tokens(self, agent_id: int) -> int:
+        a = self.agents.get(agent_id)
+        return 0 if a is None else len(a.host) * self.page_size
+
+    @property
+    def host_used(self) -> int:
+        return len(self.records)

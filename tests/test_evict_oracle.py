@@ -178,3 +178,102 @@ def test_turns_reuse_whole_pages_and_compute_at_least_one_token():
     assert c.cached_tokens(1) == 96
     c.complete(1)
     assert c.free == 64 and c.cached_tokens(1) == 0
+
+
+# ------------------------------------------------------------------ host tier
+
+def test_host_tier_hand_trace():
+    """Toy history of test_algorithm1_hand_trace with a 3-record host tier: the 9
+    pages Algorithm 1 evicts are spilled farthest page first, and each spill that
+    finds the tier full drops the oldest idle-owned record (its owner's farthest
+    host page).  Traced by hand:
+      agent 1 loses pages 5, 4 -> records r1 (p5), r2 (p4)
+      agent 2 loses page 1     -> r3
+      agent 3 loses pages 4, 3 -> drop r1, r2; r4 (p4), r5 (p3)
+      agent 1 loses pages 3, 2 -> drop r3, r4; r6 (p3), r7 (p2)
+      agent 3 loses pages 2, 1 -> drop r5, r6; r8 (p2), r9 (p1)
+    leaving agent 1 = device p1 + host p2, agent 2 = nothing, agent 3 = host p1, p2."""
+    c = OracleCache(12, PAGE, 2 * PAGE, OracleCache.RR, host_pages=3)
+    _fill(c, 1, 5)
+    _fill(c, 2, 1)
+    _fill(c, 3, 4)
+    assert c.begin_turn(9, 11 * PAGE) == 0
+    assert [c.cached_tokens(i) // PAGE for i in (1, 2, 3)] == [1, 0, 0]
+    assert [c.host_tokens(i) // PAGE for i in (1, 2, 3)] == [1, 0, 2]
+    assert c.last_moves == (9, 0)
+    assert (c.spilled_pages, c.host_dropped_pages, c.host_used) == (9, 6, 3)
+    c.end_turn(9)
+    # agent 3 returns with a 5-page prompt: both host pages come back, 3 new pages
+    free_before = c.free
+    assert c.begin_turn(3, 5 * PAGE) == 2 * PAGE
+    assert c.last_moves[1] == 2 and c.host_tokens(3) == 0 and c.reloaded_pages == 2
+    assert c.host_used == 1
+
+
+@pytest.mark.parametrize("policy", [OracleCache.RR, OracleCache.LRU])
+@pytest.mark.parametrize("n,na,m", REGIME)
+def test_a_host_tier_as_large_as_the_histories_loses_nothing(policy, n, na, m):
+    """Equation 3 with a host tier holding every idle page: X = 0 for every
+    returning agent (each reuses its whole history: device pages + reloads)."""
+    ns = n - na
+    u = 8 * ns
+    c = OracleCache(m * u, PAGE, PAGE, policy, host_pages=n * u)
+    for i in range(ns):
+        _fill(c, i, u)
+    for j in range(na):
+        c.begin_turn(1000 + j, u * PAGE)
+    assert all(c.cached_tokens(i) + c.host_tokens(i) == u * PAGE for i in range(ns))
+    assert c.host_dropped_pages == 0 and c.spilled_pages == (n - m) * u
+    for j in range(na):  # the active turns end and their agents finish
+        c.end_turn(1000 + j)
+        c.complete(1000 + j)
+    for i in range(ns):
+        host = c.host_tokens(i) // PAGE
+        assert c.begin_turn(i, u * PAGE + 1) == u * PAGE
+        assert c.last_moves[1] == host
+        c.end_turn(i)
+    assert c.reloaded_pages == c.spilled_pages
+
+
+def test_a_host_tier_of_size_zero_changes_nothing():
+    runs = []
+    for host in (0, None):
+        c = OracleCache(12, PAGE, 2 * PAGE, OracleCache.RR) if host is None else \
+            OracleCache(12, PAGE, 2 * PAGE, OracleCache.RR, host_pages=0)
+        _fill(c, 1, 5)
+        _fill(c, 2, 1)
+        _fill(c, 3, 4)
+        c.begin_turn(9, 11 * PAGE)
+        runs.append(([c.cached_tokens(i) for i in (1, 2, 3)], c.evictions, c.free, c.spilled_pages))
+    assert runs[0] == runs[1] and runs[0][3] == 0
+
+
+def test_reuse_past_the_prompt_drops_host_pages_first():
+    c = OracleCache(8, PAGE, PAGE, OracleCache.RR, host_pages=8)
+    _fill(c, 1, 6)
+    c.begin_turn(2, 4 * PAGE)          # 2 free, evicts 2 of agent 1's pages -> host
+    assert (c.cached_tokens(1), c.host_tokens(1)) == (4 * PAGE, 2 * PAGE)
+    c.end_turn(2)
+    c.complete(2)
+    assert c.begin_turn(1, 5 * PAGE + 1) == 5 * PAGE  # limit 5: 4 device + 1 reloaded, 1 host dropped
+    assert c.last_moves == (0, 1) and c.host_used == 0
+    c.end_turn(1)
+    assert c.begin_turn(1, 3 * PAGE) == 2 * PAGE       # limit 2: device pages dropped past it
+    assert c.last_moves == (0, 0)
+
+
+def test_records_of_an_agent_inside_a_turn_are_never_dropped():
+    """Agent 1 returns and must reload 2 host pages while its own allocation
+    evicts a page of agent 2: the tier is full of agent 1's pinned records, so
+    agent 2's page is dropped, not spilled."""
+    c = OracleCache(7, PAGE, 2 * PAGE, OracleCache.RR, host_pages=2)
+    _fill(c, 1, 4)                     # 4 pages kept, 3 free
+    _fill(c, 2, 2)                     # 2 kept, 1 free
+    c.begin_turn(3, 3 * PAGE)          # reclaims one 2-page chunk: agent 1's pages 4, 3 -> host (tier full)
+    assert (c.cached_tokens(1), c.host_tokens(1), c.host_used) == (2 * PAGE, 2 * PAGE, 2)
+    c.end_turn(3)
+    c.complete(3)
+    assert c.free == 3
+    assert c.begin_turn(1, 6 * PAGE) == 4 * PAGE  # 2 reloads + 2 new pages: 3 free + 1 of agent 2's
+    assert c.last_moves == (0, 2) and c.host_dropped_pages == 0
+    assert (c.cached_tokens(2), c.host_tokens(2)) == (PAGE, 0)
