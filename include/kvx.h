@@ -116,6 +116,29 @@ int kv_pool_write_pages(kvx_pool *pool, const int32_t *page_ids, int64_t n, cons
 int kv_pool_read_pages(const kvx_pool *pool, const int32_t *page_ids, int64_t n, void *k_dst,
                        void *v_dst, kvx_stream_t stream);
 
+/*
+ * KV spill to host memory and reload, instead of recomputing an evicted tail
+ * (the paper's stated future work, Section 6: keep evicted KV in a slower tier
+ * and bring it back).  A spill record holds one page exactly as the pool holds
+ * it -- its K block then its V block, kv_pool_record_bytes() bytes, raw (bf16 or
+ * fp8 codes; the scales stay with the pool) -- so spill + reload is a bit-exact
+ * round trip into any page of a pool of the same shape and dtype.
+ *   kv_pool_spill:  record slots[i] of host := page page_ids[i]
+ *   kv_pool_reload: page page_ids[i] := record slots[i] of host
+ * page_ids, slots: host [n]; page ids in [0, num_pages), slots in [0, host_slots);
+ *   the written side may not repeat (slots of a spill, page ids of a reload).
+ * host: pinned host memory (hipHostMalloc or a pinned torch tensor) of at least
+ *   host_slots records; the kernel reaches it over the host link.  Asynchronous
+ *   on `stream`: the host buffer and pool pages must not be touched until the
+ *   stream has passed the call.  Errors: EINVAL (also unpinned host memory),
+ *   ERANGE, ENOMEM, EHIP.  n = 0: no-op.
+ */
+int kv_pool_record_bytes(const kvx_pool *pool, int64_t *bytes);
+int kv_pool_spill(const kvx_pool *pool, const int32_t *page_ids, const int32_t *slots, int64_t n,
+                  void *host, int64_t host_slots, kvx_stream_t stream);
+int kv_pool_reload(kvx_pool *pool, const int32_t *page_ids, const int32_t *slots, int64_t n,
+                   const void *host, int64_t host_slots, kvx_stream_t stream);
+
 /* ---------------------------------------------------------------- the batch */
 
 /* One prefix-extend batch.  Request r has a cached prefix of P_r tokens already

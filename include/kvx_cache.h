@@ -28,6 +28,19 @@
  * Completion signals (Section 3.2, "Handling stale agent trajectories") are
  * kvx_cache_complete: the agent's pages are freed at once.
  *
+ * Host tier (optional; the paper's future work, Section 6: idle state spilled to
+ * CPU memory and reloaded instead of recomputed).  A tiered cache also manages
+ * `host_pages` page records of a caller-owned pinned host buffer (see
+ * kv_pool_spill / kv_pool_reload in kvx.h).  An idle agent's history is then its
+ * device pages followed, without a gap, by its host pages.  Pages the policy
+ * evicts are spilled to host records instead of dropped, farthest page first; a
+ * spill that finds every record taken first drops the oldest record whose owner
+ * is idle (that owner's farthest host page), and if every record belongs to an
+ * agent inside a turn the page is dropped instead.  A turn start reuses device
+ * pages, then host pages, up to the prompt's limit; the reused host pages are
+ * reloaded into freshly allocated device pages and their records freed, so an
+ * agent inside a turn holds no host pages.
+ *
  * Conventions: every call is synchronous host code, returns KVX_OK or a
  * kvx_status code from kvx.h (kvx_last_error() describes the failure), and is not
  * thread-safe for one cache (callers serialize calls on a cache).  Page ids are
@@ -61,7 +74,26 @@ typedef struct {
     int64_t evictions;      /* eviction steps (LRU nodes or RR chunks) since creation */
     int32_t agents;         /* agents known to the cache */
     int32_t active_agents;  /* agents inside a turn */
+    int64_t host_pages;     /* host records managed (0: no host tier) */
+    int64_t host_used;      /* records holding a spilled page */
+    int64_t spilled_pages;  /* pages spilled since creation */
+    int64_t reloaded_pages; /* pages reloaded since creation */
+    int64_t host_dropped_pages; /* records dropped to make room since creation */
 } kvx_cache_counters;
+
+/* Page moves a tiered turn start asks for, to run on the pool in this order
+ * before the turn's store_kv: first every spill (kv_pool_spill of
+ * spill_pages[i] into record spill_slots[i]), then every reload (kv_pool_reload
+ * of record reload_slots[i] into page reload_pages[i]).  Moves of successive
+ * calls must run in call order (one stream). */
+typedef struct {
+    const int32_t *spill_pages;   /* [n_spill]; the four arrays are owned by the cache and */
+    const int32_t *spill_slots;   /* stay valid until the next call on it                  */
+    const int32_t *reload_pages;  /* [n_reload] */
+    const int32_t *reload_slots;
+    int64_t n_spill;
+    int64_t n_reload;
+} kvx_cache_moves;
 
 /*
  * Create a cache over `num_pages` pages of `page_size` tokens.
@@ -73,6 +105,16 @@ typedef struct {
  */
 int kvx_cache_create(int64_t num_pages, int32_t page_size, int32_t chunk_tokens, int32_t policy,
                      kvx_cache **out);
+
+/*
+ * A cache with a host tier of `host_pages` >= 0 records (0: the same as
+ * kvx_cache_create).  Record r is bytes [r * R, (r + 1) * R) of the caller's
+ * pinned host buffer, R = kv_pool_record_bytes of the pool.  Turns of a cache
+ * with host_pages > 0 start with kvx_cache_begin_turn_tiered.  Errors: as
+ * kvx_cache_create, and EINVAL for host_pages outside [0, 2^31 - 1].
+ */
+int kvx_cache_create_tiered(int64_t num_pages, int64_t host_pages, int32_t page_size, int32_t chunk_tokens,
+                            int32_t policy, kvx_cache **out);
 
 /* Free a cache.  NULL is a no-op. */
 int kvx_cache_destroy(kvx_cache *cache);
@@ -98,6 +140,17 @@ int kvx_cache_begin_turn(kvx_cache *cache, int64_t agent, int32_t prompt_len, in
                          int32_t *page_ids, int64_t cap);
 
 /*
+ * kvx_cache_begin_turn on a cache of any kind, also returning the page moves it
+ * needs (`moves`, filled on success and on ENOMEM; on ENOMEM only spills are
+ * listed, and they must still run).  *prefix_len counts the reused device pages
+ * and the reloaded host pages.  Errors: as kvx_cache_begin_turn, and EINVAL for
+ * moves == NULL (checked first).  kvx_cache_begin_turn on a cache with a host
+ * tier fails with EINVAL (its spills would be lost).
+ */
+int kvx_cache_begin_turn_tiered(kvx_cache *cache, int64_t agent, int32_t prompt_len, int32_t *prefix_len,
+                                int32_t *page_ids, int64_t cap, kvx_cache_moves *moves);
+
+/*
  * End the running turn of `agent`: the prompt's whole pages stay cached as the
  * agent's history (a new node holding the pages this turn added), its partial
  * last page is freed, and the agent becomes idle.  Errors: EINVAL (not active).
@@ -117,6 +170,14 @@ int kvx_cache_complete(kvx_cache *cache, int64_t agent);
  */
 int kvx_cache_agent(const kvx_cache *cache, int64_t agent, int32_t *cached_tokens, int32_t *page_ids,
                     int64_t cap);
+
+/*
+ * Host pages of `agent` in tokens (0 for an unknown agent) and, if `slots` is
+ * non-NULL, their records in logical order (at most `cap` written).  For tests
+ * and tools.  Errors: EINVAL.
+ */
+int kvx_cache_agent_host(const kvx_cache *cache, int64_t agent, int32_t *host_tokens, int32_t *slots,
+                         int64_t cap);
 
 /* Counters of the cache.  Errors: EINVAL. */
 int kvx_cache_stats(const kvx_cache *cache, kvx_cache_counters *out);

@@ -44,7 +44,9 @@ instead of dropping it), when ``host_pages`` > 0:
    first (so within an agent, older records are always farther pages).  A
    spill that finds no free record first drops the oldest record whose owner
    is idle -- that owner's farthest host page.  If every record belongs to an
-   active agent, the page is dropped instead.
+   active agent, the page is dropped instead.  A record spilled into earlier in
+   the same turn start and dropped again before it ends voids that spill: the
+   page counts as dropped, not spilled (the moves never write it).
 9. A turn start reuses device pages, then host pages, up to reading 3's limit;
    the reused host pages are reloaded into freshly allocated device pages (they
    are pinned while the turn allocates) and their records freed.  Pages past
@@ -123,7 +125,12 @@ class OracleCache:
                 assert o.host[-1] == rec  # the owner's farthest host page
                 o.host.pop()
                 self._forget(rec)
-                self.host_dropped_pages += 1
+                if rec in self.call_spills:  # written earlier in this turn start: that spill is void
+                    self.call_spills.discard(rec)
+                    self.spilled_pages -= 1
+                    self.moves_spill -= 1
+                else:
+                    self.host_dropped_pages += 1
                 self.next_record += 1
                 return self.next_record
         return None
@@ -139,6 +146,7 @@ class OracleCache:
                 continue  # dropped (the agent has no host pages: nothing past it is lost)
             a.host.insert(0, rec)
             self.records.append((rec, agent_id))
+            self.call_spills.add(rec)
             self.spilled_pages += 1
             self.moves_spill += 1
 
@@ -192,6 +200,7 @@ class OracleCache:
         self.clock += 1
         a.stamp = self.clock
         self.moves_spill = 0
+        self.call_spills: set[int] = set()
         self.last_moves = (0, 0)
         limit = (prompt_len - 1) // self.page_size
         reuse = min(a.pages + len(a.host), limit)

@@ -1,8 +1,9 @@
 // Host-side prefix cache for multi-turn agents: page allocation over a kvx pool
 // and eviction of idle agents' histories, either by round-robin tail chunks
 // (paper Section 3.2, Algorithm 1) or by least-recent whole leaf nodes (the LRU
-// baseline, Section 3.1).  The C ABI and the model are declared in
-// include/kvx_cache.h.
+// baseline, Section 3.1), optionally into a host tier of spilled pages that a
+// returning agent reloads (the paper's future work, Section 6).  The C ABI and
+// the model are declared in include/kvx_cache.h.
 
 #include <algorithm>
 #include <deque>
@@ -27,6 +28,12 @@ struct CacheAgent {
   bool active = false;
   int32_t prompt_len = 0;        // running turn
   std::vector<int32_t> turn;     // pages allocated to the running turn
+  std::deque<int32_t> host;      // host records continuing the device pages, nearest first
+};
+
+struct FifoEntry {
+  int32_t rec;
+  uint32_t gen;  // generation of the record when it was spilled into
 };
 
 }  // namespace
@@ -43,6 +50,15 @@ struct kvx_cache {
   int64_t rr_last = 0;  // agent that lost the last RR chunk
   int64_t evicted_pages = 0;
   int64_t evictions = 0;
+  // host tier
+  int64_t host_pages = 0;
+  std::vector<int32_t> host_free;     // stack of free records
+  std::deque<FifoEntry> host_fifo;    // spills, oldest first (entries of freed records are stale)
+  std::vector<int64_t> rec_owner;     // agent of each live record
+  std::vector<uint32_t> rec_gen;      // bumped at every allocation of the record
+  std::vector<uint8_t> rec_live;
+  int64_t host_used = 0, spilled = 0, reloaded = 0, host_dropped = 0;
+  std::vector<int32_t> mv_spill_pages, mv_spill_slots, mv_reload_pages, mv_reload_slots;
 };
 
 namespace {
@@ -67,19 +83,116 @@ void drop_tail(kvx_cache* c, CacheAgent& a, int64_t n) {
   }
 }
 
+void free_record(kvx_cache* c, int32_t rec) {
+  c->rec_live[(size_t)rec] = 0;
+  c->host_free.push_back(rec);
+  c->host_used--;
+}
+
+void drop_host(kvx_cache* c, CacheAgent& a, size_t keep) {
+  while (a.host.size() > keep) {
+    free_record(c, a.host.back());
+    a.host.pop_back();
+  }
+}
+
+// A record for a spill of `owner`'s page: a free one, else the oldest live record
+// whose owner is idle is dropped (it is always that owner's farthest host page);
+// -1 if every record belongs to an agent inside a turn.
+int32_t take_record(kvx_cache* c, int64_t owner) {
+  int32_t rec = -1;
+  if (!c->host_free.empty()) {
+    rec = c->host_free.back();
+    c->host_free.pop_back();
+  } else {
+    for (auto it = c->host_fifo.begin(); it != c->host_fifo.end();) {
+      const int32_t r = it->rec;
+      if (!c->rec_live[(size_t)r] || c->rec_gen[(size_t)r] != it->gen) {
+        it = c->host_fifo.erase(it);  // freed since
+        continue;
+      }
+      CacheAgent& o = c->agents.find(c->rec_owner[(size_t)r])->second;
+      if (o.active) {
+        ++it;
+        continue;
+      }
+      // r is o's farthest host page (one agent's spills enter the FIFO farthest
+      // page first); were it not, the pages past it would go too, keeping o's
+      // history free of gaps
+      c->host_fifo.erase(it);
+      while (!o.host.empty() && o.host.back() != r) {
+        free_record(c, o.host.back());
+        o.host.pop_back();
+        c->host_dropped++;
+      }
+      o.host.pop_back();
+      c->host_used--;
+      rec = r;
+      // a record spilled into earlier in this same call: that spill is void (its
+      // page is simply dropped) and leaves the move list
+      auto mv = std::find(c->mv_spill_slots.begin(), c->mv_spill_slots.end(), r);
+      if (mv != c->mv_spill_slots.end()) {
+        c->mv_spill_pages.erase(c->mv_spill_pages.begin() + (mv - c->mv_spill_slots.begin()));
+        c->mv_spill_slots.erase(mv);
+        c->spilled--;
+      } else {
+        c->host_dropped++;
+      }
+      break;
+    }
+    if (rec < 0) return -1;
+  }
+  c->rec_live[(size_t)rec] = 1;
+  c->rec_gen[(size_t)rec]++;
+  c->rec_owner[(size_t)rec] = owner;
+  c->host_used++;
+  c->host_fifo.push_back(FifoEntry{rec, c->rec_gen[(size_t)rec]});
+  if ((int64_t)c->host_fifo.size() > 2 * c->host_pages + 64) {  // drop the entries of freed records
+    std::deque<FifoEntry> live;
+    for (const FifoEntry& e : c->host_fifo)
+      if (c->rec_live[(size_t)e.rec] && c->rec_gen[(size_t)e.rec] == e.gen) live.push_back(e);
+    c->host_fifo.swap(live);
+  }
+  return rec;
+}
+
+// Evict the last n device pages of agent `id`: freed, and spilled to the host
+// tier (farthest page first) when there is one.
+void evict_tail(kvx_cache* c, int64_t id, CacheAgent& a, int64_t n) {
+  std::vector<int32_t> pages;
+  if (c->host_pages > 0) {
+    for (auto nd = a.nodes.rbegin(); nd != a.nodes.rend() && (int64_t)pages.size() < n; ++nd)
+      for (auto pg = nd->pages.rbegin(); pg != nd->pages.rend() && (int64_t)pages.size() < n; ++pg)
+        pages.push_back(*pg);  // farthest first
+  }
+  drop_tail(c, a, n);
+  for (int32_t pg : pages) {
+    const int32_t rec = take_record(c, id);
+    if (rec < 0) continue;  // dropped: the agent holds no host pages past it
+    a.host.push_front(rec);
+    c->mv_spill_pages.push_back(pg);
+    c->mv_spill_slots.push_back(rec);
+    c->spilled++;
+  }
+}
+
 // LRU: whole leaf nodes, oldest time stamp first (ties: smaller id), idle agents only.
 int64_t evict_lru(kvx_cache* c, int64_t need) {
   int64_t freed = 0;
   while (freed < need) {
     CacheAgent* best = nullptr;
+    int64_t best_id = 0;
     for (auto& kv : c->agents) {
       CacheAgent& a = kv.second;
       if (a.active || a.nodes.empty()) continue;
-      if (best == nullptr || a.stamp < best->stamp) best = &a;  // map order breaks ties by id
+      if (best == nullptr || a.stamp < best->stamp) {  // map order breaks ties by id
+        best = &a;
+        best_id = kv.first;
+      }
     }
     if (best == nullptr) break;
     const int64_t n = (int64_t)best->nodes.back().pages.size();
-    drop_tail(c, *best, n);
+    evict_tail(c, best_id, *best, n);
     freed += n;
     c->evicted_pages += n;
     c->evictions++;
@@ -108,7 +221,7 @@ int64_t evict_rr(kvx_cache* c, int64_t need) {
     // what is still to be reclaimed
     const int64_t n = std::min<int64_t>({(int64_t)c->chunk_pages, (int64_t)a.nodes.back().pages.size(),
                                          need - freed});
-    drop_tail(c, a, n);
+    evict_tail(c, id, a, n);
     freed += n;
     c->evicted_pages += n;
     c->evictions++;
@@ -127,6 +240,11 @@ extern "C" {
 
 int kvx_cache_create(int64_t num_pages, int32_t page_size, int32_t chunk_tokens, int32_t policy,
                      kvx_cache** out) {
+  return kvx_cache_create_tiered(num_pages, 0, page_size, chunk_tokens, policy, out);
+}
+
+int kvx_cache_create_tiered(int64_t num_pages, int64_t host_pages, int32_t page_size, int32_t chunk_tokens,
+                            int32_t policy, kvx_cache** out) {
   if (out == nullptr) return report(KVX_EINVAL, "out is NULL");
   *out = nullptr;
   if (num_pages <= 0 || num_pages > (int64_t)std::numeric_limits<int32_t>::max())
@@ -135,15 +253,24 @@ int kvx_cache_create(int64_t num_pages, int32_t page_size, int32_t chunk_tokens,
   if (chunk_tokens <= 0 || chunk_tokens % page_size != 0)
     return report(KVX_EINVAL, "chunk_tokens = %d must be a positive multiple of %d", chunk_tokens, page_size);
   if (policy != KVX_EVICT_LRU && policy != KVX_EVICT_RR) return report(KVX_EINVAL, "policy %d", policy);
+  if (host_pages < 0 || host_pages > (int64_t)std::numeric_limits<int32_t>::max())
+    return report(KVX_EINVAL, "host_pages = %lld must be in [0, 2^31-1]", (long long)host_pages);
   kvx_cache* c = new (std::nothrow) kvx_cache();
   if (c == nullptr) return report(KVX_ENOMEM, "cache allocation failed");
   try {
     c->free_pages.resize((size_t)num_pages);
+    c->host_free.resize((size_t)host_pages);
+    c->rec_owner.assign((size_t)host_pages, 0);
+    c->rec_gen.assign((size_t)host_pages, 0);
+    c->rec_live.assign((size_t)host_pages, 0);
   } catch (...) {
     delete c;
-    return report(KVX_ENOMEM, "free list of %lld pages", (long long)num_pages);
+    return report(KVX_ENOMEM, "free lists of %lld pages and %lld records", (long long)num_pages,
+                  (long long)host_pages);
   }
   for (int64_t i = 0; i < num_pages; i++) c->free_pages[(size_t)i] = (int32_t)(num_pages - 1 - i);  // page 0 first
+  for (int64_t i = 0; i < host_pages; i++) c->host_free[(size_t)i] = (int32_t)(host_pages - 1 - i);
+  c->host_pages = host_pages;
   c->num_pages = num_pages;
   c->page_size = page_size;
   c->chunk_pages = chunk_tokens / page_size;
@@ -157,10 +284,12 @@ int kvx_cache_destroy(kvx_cache* c) {
   return KVX_OK;
 }
 
-int kvx_cache_begin_turn(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_t* prefix_len, int32_t* page_ids,
-                         int64_t cap) {
+static int begin_turn(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_t* prefix_len, int32_t* page_ids,
+                      int64_t cap, kvx_cache_moves* moves) {
   if (c == nullptr || prefix_len == nullptr || page_ids == nullptr)
     return report(KVX_EINVAL, "cache, prefix_len and page_ids must be non-NULL");
+  if (moves == nullptr && c->host_pages > 0)
+    return report(KVX_EINVAL, "a cache with a host tier starts turns with kvx_cache_begin_turn_tiered");
   if (prompt_len < 1) return report(KVX_EINVAL, "prompt_len = %d must be >= 1", prompt_len);
   const int64_t S = c->page_size;
   const int64_t n_total = div_up(prompt_len, S);
@@ -169,19 +298,41 @@ int kvx_cache_begin_turn(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_
   auto found = c->agents.find(agent);
   if (found != c->agents.end() && found->second.active)
     return report(KVX_EINVAL, "agent %lld is already inside a turn", (long long)agent);
+  c->mv_spill_pages.clear();
+  c->mv_spill_slots.clear();
+  c->mv_reload_pages.clear();
+  c->mv_reload_slots.clear();
   CacheAgent& a = c->agents[agent];
   a.stamp = ++c->clock;  // matching the prefix touches every node of the path
-  const int64_t reuse_pages = std::min<int64_t>(a.pages, (prompt_len - 1) / S);
-  if (a.pages > reuse_pages) drop_tail(c, a, a.pages - reuse_pages);
-  const int64_t need = n_total - reuse_pages;
-  a.active = true;  // pinned while this turn allocates
+  // reuse device pages, then host pages, up to the last whole page before the final token
+  const int64_t limit = (prompt_len - 1) / S;
+  const int64_t reuse_pages = std::min<int64_t>(a.pages + (int64_t)a.host.size(), limit);
+  if (reuse_pages < a.pages) {
+    drop_host(c, a, 0);
+    drop_tail(c, a, a.pages - reuse_pages);
+  } else {
+    drop_host(c, a, (size_t)(reuse_pages - a.pages));
+  }
+  const int64_t reload = (int64_t)a.host.size();
+  const int64_t need = n_total - a.pages;  // reloaded pages + the suffix's pages
+  a.active = true;  // pinned (with its host records) while this turn allocates
   if ((int64_t)c->free_pages.size() < need) {
     const int64_t want = need - (int64_t)c->free_pages.size();
     if (c->policy == KVX_EVICT_RR) evict_rr(c, want);
     else evict_lru(c, want);
   }
+  auto fill_moves = [&]() {
+    if (moves == nullptr) return;
+    moves->spill_pages = c->mv_spill_pages.data();
+    moves->spill_slots = c->mv_spill_slots.data();
+    moves->reload_pages = c->mv_reload_pages.data();
+    moves->reload_slots = c->mv_reload_slots.data();
+    moves->n_spill = (int64_t)c->mv_spill_pages.size();
+    moves->n_reload = (int64_t)c->mv_reload_pages.size();
+  };
   if ((int64_t)c->free_pages.size() < need) {
     a.active = false;
+    fill_moves();
     return report(KVX_ENOMEM, "agent %lld: %lld pages needed, %lld free after evicting every idle page",
                   (long long)agent, (long long)need, (long long)c->free_pages.size());
   }
@@ -191,13 +342,32 @@ int kvx_cache_begin_turn(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_
     a.turn.push_back(c->free_pages.back());
     c->free_pages.pop_back();
   }
+  for (int64_t j = 0; j < reload; j++) {
+    c->mv_reload_pages.push_back(a.turn[(size_t)j]);
+    c->mv_reload_slots.push_back(a.host[(size_t)j]);
+  }
+  drop_host(c, a, 0);
+  c->reloaded += reload;
   a.prompt_len = prompt_len;
   int64_t j = 0;
   for (const CacheNode& nd : a.nodes)
     for (int32_t pg : nd.pages) page_ids[j++] = pg;
   for (int32_t pg : a.turn) page_ids[j++] = pg;
   *prefix_len = (int32_t)(reuse_pages * S);
+  fill_moves();
   return KVX_OK;
+}
+
+int kvx_cache_begin_turn(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_t* prefix_len, int32_t* page_ids,
+                         int64_t cap) {
+  return begin_turn(c, agent, prompt_len, prefix_len, page_ids, cap, nullptr);
+}
+
+int kvx_cache_begin_turn_tiered(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_t* prefix_len,
+                                int32_t* page_ids, int64_t cap, kvx_cache_moves* moves) {
+  if (moves == nullptr) return report(KVX_EINVAL, "moves is NULL");
+  *moves = kvx_cache_moves{};
+  return begin_turn(c, agent, prompt_len, prefix_len, page_ids, cap, moves);
 }
 
 int kvx_cache_end_turn(kvx_cache* c, int64_t agent) {
@@ -227,6 +397,7 @@ int kvx_cache_complete(kvx_cache* c, int64_t agent) {
   if (it == c->agents.end()) return report(KVX_EINVAL, "agent %lld is unknown", (long long)agent);
   if (it->second.active) return report(KVX_EINVAL, "agent %lld is inside a turn", (long long)agent);
   drop_tail(c, it->second, it->second.pages);
+  drop_host(c, it->second, 0);
   c->agents.erase(it);
   return KVX_OK;
 }
@@ -248,6 +419,22 @@ int kvx_cache_agent(const kvx_cache* c, int64_t agent, int32_t* cached_tokens, i
   return KVX_OK;
 }
 
+int kvx_cache_agent_host(const kvx_cache* c, int64_t agent, int32_t* host_tokens, int32_t* slots, int64_t cap) {
+  if (c == nullptr || host_tokens == nullptr) return report(KVX_EINVAL, "cache and host_tokens must be non-NULL");
+  auto it = c->agents.find(agent);
+  if (it == c->agents.end()) {
+    *host_tokens = 0;
+    return KVX_OK;
+  }
+  *host_tokens = (int32_t)((int64_t)it->second.host.size() * c->page_size);
+  if (slots != nullptr) {
+    int64_t j = 0;
+    for (int32_t r : it->second.host)
+      if (j < cap) slots[j++] = r;
+  }
+  return KVX_OK;
+}
+
 int kvx_cache_stats(const kvx_cache* c, kvx_cache_counters* out) {
   if (c == nullptr || out == nullptr) return report(KVX_EINVAL, "cache and out must be non-NULL");
   kvx_cache_counters s{};
@@ -261,6 +448,11 @@ int kvx_cache_stats(const kvx_cache* c, kvx_cache_counters* out) {
   s.agents = (int32_t)c->agents.size();
   s.evicted_pages = c->evicted_pages;
   s.evictions = c->evictions;
+  s.host_pages = c->host_pages;
+  s.host_used = c->host_used;
+  s.spilled_pages = c->spilled;
+  s.reloaded_pages = c->reloaded;
+  s.host_dropped_pages = c->host_dropped;
   *out = s;
   return KVX_OK;
 }

@@ -159,7 +159,7 @@ struct kvx_pool {
   void* k = nullptr;
   void* v = nullptr;
   float* scales_d = nullptr;  // [k_scale | v_scale | k_inv | v_inv], each num_kv_heads
-  Staging st_store, st_attn, st_io;
+  Staging st_store, st_attn, st_io, st_move;
   Workspace parts;
 };
 
@@ -601,6 +601,7 @@ int kv_pool_destroy(kvx_pool* pool) {
   pool->st_store.release();
   pool->st_attn.release();
   pool->st_io.release();
+  pool->st_move.release();
   pool->parts.release();
   if (pool->k) (void)hipFree(pool->k);
   if (pool->v) (void)hipFree(pool->v);
@@ -675,6 +676,78 @@ int kv_pool_read_pages(const kvx_pool* pool, const int32_t* page_ids, int64_t n,
                        kvx_stream_t stream) {
   g_last_error.clear();
   return page_io(const_cast<kvx_pool*>(pool), page_ids, n, k_dst, v_dst, 0, stream);
+}
+
+static int64_t record_bytes(const kvx_pool* pool) {
+  return 2 * (int64_t)pool->num_kv_heads * kvx::kPageSize * pool->head_dim * pool->elem_bytes;
+}
+
+int kv_pool_record_bytes(const kvx_pool* pool, int64_t* bytes) {
+  g_last_error.clear();
+  if (int rc = check_pool(pool)) return rc;
+  if (bytes == nullptr) return fail(KVX_EINVAL, "bytes is NULL");
+  *bytes = record_bytes(pool);
+  return KVX_OK;
+}
+
+// Spill (to_host) or reload whole pages between the pool and pinned host records.
+static int page_move(kvx_pool* pool, const int32_t* page_ids, const int32_t* slots, int64_t n, const void* host,
+                     int64_t host_slots, int to_host, kvx_stream_t stream) {
+  if (int rc = check_pool(pool)) return rc;
+  if (n < 0 || host_slots < 0) return fail(KVX_EINVAL, "n = %lld and host_slots = %lld must be >= 0", (long long)n,
+                                           (long long)host_slots);
+  if (n == 0) return KVX_OK;
+  if (!page_ids || !slots || !host) return fail(KVX_EINVAL, "page_ids, slots and host must be non-NULL");
+  if (n > (int64_t)INT32_MAX) return fail(KVX_EINVAL, "too many pages");
+  for (int64_t i = 0; i < n; i++) {
+    if (page_ids[i] < 0 || page_ids[i] >= pool->num_pages)
+      return fail(KVX_ERANGE, "page_ids[%lld] = %d outside [0, %lld)", (long long)i, page_ids[i],
+                  (long long)pool->num_pages);
+    if (slots[i] < 0 || slots[i] >= host_slots)
+      return fail(KVX_ERANGE, "slots[%lld] = %d outside [0, %lld)", (long long)i, slots[i], (long long)host_slots);
+  }
+  // the written side must not repeat: slots of a spill, pages of a reload
+  std::vector<int32_t> dst(to_host ? slots : page_ids, (to_host ? slots : page_ids) + n);
+  std::sort(dst.begin(), dst.end());
+  if (std::adjacent_find(dst.begin(), dst.end()) != dst.end())
+    return fail(KVX_EINVAL, "%s repeats an entry", to_host ? "slots" : "page_ids");
+  if (int rc = use_device(pool)) return rc;
+  hipPointerAttribute_t attr{};
+  if (hipPointerGetAttributes(&attr, host) != hipSuccess || attr.type != hipMemoryTypeHost ||
+      attr.devicePointer == nullptr) {
+    (void)hipGetLastError();
+    return fail(KVX_EINVAL, "host must be pinned host memory (hipHostMalloc, or a pinned torch tensor)");
+  }
+  const int64_t off = (const uint8_t*)host - (const uint8_t*)attr.hostPointer;
+  hipStream_t s = (hipStream_t)stream;
+  std::vector<int32_t> idx((size_t)(2 * n));
+  std::copy(page_ids, page_ids + n, idx.begin());
+  std::copy(slots, slots + n, idx.begin() + n);
+  void* idx_d = nullptr;
+  if (int rc = pool->st_move.upload(idx.data(), idx.size() * sizeof(int32_t), s, &idx_d)) return rc;
+  kvx::PageMoveParams p;
+  p.page_ids = (const int32_t*)idx_d;
+  p.slots = (const int32_t*)idx_d + n;
+  p.k_pool = (uint8_t*)pool->k;
+  p.v_pool = (uint8_t*)pool->v;
+  p.host = (uint8_t*)attr.devicePointer + (attr.hostPointer ? off : 0);
+  p.block_bytes = record_bytes(pool) / 2;
+  p.to_host = to_host;
+  hipError_t e = kvx::launch_page_move(p, n, s);
+  if (e != hipSuccess) return hip_fail(e, "page move kernel launch");
+  return KVX_OK;
+}
+
+int kv_pool_spill(const kvx_pool* pool, const int32_t* page_ids, const int32_t* slots, int64_t n, void* host,
+                  int64_t host_slots, kvx_stream_t stream) {
+  g_last_error.clear();
+  return page_move(const_cast<kvx_pool*>(pool), page_ids, slots, n, host, host_slots, 1, stream);
+}
+
+int kv_pool_reload(kvx_pool* pool, const int32_t* page_ids, const int32_t* slots, int64_t n, const void* host,
+                   int64_t host_slots, kvx_stream_t stream) {
+  g_last_error.clear();
+  return page_move(pool, page_ids, slots, n, host, host_slots, 0, stream);
 }
 
 int store_kv(kvx_pool* pool, const kvx_batch* batch, const void* k_ext, const void* v_ext, kvx_stream_t stream) {

@@ -127,6 +127,18 @@ struct PageIoParams {
   int32_t to_pool;          // 1: write pages into the pool, 0: read them out
 };
 
+// Raw page records between the pool and host memory: record i = the K block then
+// the V block of page page_ids[i], at host + slots[i] * 2 * block_bytes.
+struct PageMoveParams {
+  const int32_t* page_ids;  // device [n]
+  const int32_t* slots;     // device [n]
+  uint8_t* k_pool;
+  uint8_t* v_pool;
+  uint8_t* host;            // device-accessible address of pinned host memory
+  int64_t block_bytes;      // Hkv * 16 * D * elem bytes (a multiple of 1 KiB)
+  int32_t to_host;          // 1: pool -> host (spill), 0: host -> pool (reload)
+};
+
 // ---- decode (one query token per request): a key chunk of one (request, KV head)
 constexpr int kDecodeThreads = 256;  // 4 waves, each streaming every 4th pair of pages
 constexpr int kDecodeMaxGroup = 16;  // query heads per KV head held in one MFMA column block
@@ -192,6 +204,7 @@ hipError_t launch_store_kv(const StoreParams& p, int64_t n_units, int head_dim, 
                            hipStream_t stream);
 hipError_t launch_store_kv_rope(const RopeParams& p, int64_t n_units, int head_dim, bool fp8, bool interleaved,
                                 hipStream_t stream);
+hipError_t launch_page_move(const PageMoveParams& p, int64_t n_pages, hipStream_t stream);
 hipError_t launch_page_io(const PageIoParams& p, int64_t n_pages, int head_dim, int elem_bytes,
                           hipStream_t stream);
 

@@ -314,6 +314,35 @@ __global__ __launch_bounds__(kStoreThreads) void store_kv_rope_kernel(RopeParams
   }
 }
 
+// Spill / reload of whole pages between the pool and pinned host memory.  One
+// workgroup per (page, K|V block): the block is contiguous on both sides, so
+// every lane moves 16-byte pieces, four in flight before any store (host memory
+// is reached over the host link: latency is long, concurrency hides it).
+__global__ __launch_bounds__(256) void page_move_kernel(PageMoveParams p) {
+  constexpr int kUnroll = 4;
+  const int i = blockIdx.x;
+  const int kv = blockIdx.y;  // 0: K block, 1: V block
+  const int64_t page = p.page_ids[i];
+  uint8_t* dev = (kv == 0 ? p.k_pool : p.v_pool) + page * p.block_bytes;
+  uint8_t* host = p.host + ((int64_t)p.slots[i] * 2 + kv) * p.block_bytes;
+  const uint8_t* src = p.to_host ? dev : host;
+  uint8_t* dst = p.to_host ? host : dev;
+  const int64_t pieces = p.block_bytes / 16;
+  for (int64_t c0 = threadIdx.x; c0 < pieces; c0 += kUnroll * 256) {
+    uint4 x[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; u++) {
+      const int64_t c = c0 + u * 256;
+      if (c < pieces) x[u] = *(const uint4*)(src + c * 16);
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; u++) {
+      const int64_t c = c0 + u * 256;
+      if (c < pieces) *(uint4*)(dst + c * 16) = x[u];
+    }
+  }
+}
+
 // Raw page copy between canonical [n][Hkv][16][D] buffers and the pool.
 template <int D, int EB>
 __global__ __launch_bounds__(256) void page_io_kernel(PageIoParams p) {
@@ -387,6 +416,12 @@ hipError_t launch_store_kv_rope(const RopeParams& p, int64_t n_units, int head_d
     else { if (interleaved) KVX_ROPE_LAUNCH(64, false, true); else KVX_ROPE_LAUNCH(64, false, false); }
   }
 #undef KVX_ROPE_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_page_move(const PageMoveParams& p, int64_t n_pages, hipStream_t stream) {
+  if (n_pages <= 0) return hipSuccess;
+  hipLaunchKernelGGL(page_move_kernel, dim3((unsigned)n_pages, 2), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 

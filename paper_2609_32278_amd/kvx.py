@@ -28,10 +28,11 @@ KVX_ROPE_HALF, KVX_ROPE_INTERLEAVED = 0, 1
 
 # Every symbol include/kvx.h and include/kvx_cache.h declare.
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_layout", "kv_pool_write_pages",
-           "kv_pool_read_pages", "store_kv", "store_kv_rope", "extend_attention", "extend_attention_plan",
+           "kv_pool_read_pages", "kv_pool_record_bytes", "kv_pool_spill", "kv_pool_reload", "store_kv", "store_kv_rope", "extend_attention", "extend_attention_plan",
            "kvx_set_split_keys", "kvx_last_error",
-           "kvx_cache_create", "kvx_cache_destroy", "kvx_cache_begin_turn", "kvx_cache_end_turn",
-           "kvx_cache_complete", "kvx_cache_agent", "kvx_cache_stats"]
+           "kvx_cache_create", "kvx_cache_create_tiered", "kvx_cache_destroy", "kvx_cache_begin_turn",
+           "kvx_cache_begin_turn_tiered", "kvx_cache_end_turn", "kvx_cache_complete", "kvx_cache_agent",
+           "kvx_cache_agent_host", "kvx_cache_stats"]
 
 
 class KvxNotBuilt(ImportError):
@@ -78,7 +79,15 @@ WORK_ITEM_DTYPE = np.dtype([(n, np.int32) for n, _ in kvx_work_item._fields_])
 class kvx_cache_stats_t(ctypes.Structure):
     _fields_ = [("num_pages", ctypes.c_int64), ("free_pages", ctypes.c_int64), ("cached_pages", ctypes.c_int64),
                 ("turn_pages", ctypes.c_int64), ("evicted_pages", ctypes.c_int64), ("evictions", ctypes.c_int64),
-                ("agents", ctypes.c_int32), ("active_agents", ctypes.c_int32)]
+                ("agents", ctypes.c_int32), ("active_agents", ctypes.c_int32), ("host_pages", ctypes.c_int64),
+                ("host_used", ctypes.c_int64), ("spilled_pages", ctypes.c_int64), ("reloaded_pages", ctypes.c_int64),
+                ("host_dropped_pages", ctypes.c_int64)]
+
+
+class kvx_cache_moves(ctypes.Structure):
+    _fields_ = [("spill_pages", ctypes.POINTER(ctypes.c_int32)), ("spill_slots", ctypes.POINTER(ctypes.c_int32)),
+                ("reload_pages", ctypes.POINTER(ctypes.c_int32)), ("reload_slots", ctypes.POINTER(ctypes.c_int32)),
+                ("n_spill", ctypes.c_int64), ("n_reload", ctypes.c_int64)]
 
 _lib = None
 
@@ -97,12 +106,18 @@ def lib():
             "kv_pool_layout": [P, ctypes.POINTER(kvx_pool_layout)],
             "kv_pool_write_pages": [P, P, i64, P, P, P],
             "kv_pool_read_pages": [P, P, i64, P, P, P],
+            "kv_pool_record_bytes": [P, ctypes.POINTER(i64)],
+            "kv_pool_spill": [P, P, P, i64, P, i64, P],
+            "kv_pool_reload": [P, P, P, i64, P, i64, P],
             "store_kv": [P, ctypes.POINTER(kvx_batch), P, P, P],
             "store_kv_rope": [P, ctypes.POINTER(kvx_batch), ctypes.POINTER(kvx_rope), P, i32, P, P, P, P],
             "extend_attention": [P, ctypes.POINTER(kvx_batch), P, i32, f32, P, P, P],
             "extend_attention_plan": [ctypes.POINTER(kvx_batch), i32, i32, i32, P, i64, ctypes.POINTER(i64)],
             "kvx_set_split_keys": [i32],
             "kvx_cache_create": [i64, i32, i32, i32, ctypes.POINTER(P)],
+            "kvx_cache_create_tiered": [i64, i64, i32, i32, i32, ctypes.POINTER(P)],
+            "kvx_cache_begin_turn_tiered": [P, i64, i32, ctypes.POINTER(i32), P, i64, ctypes.POINTER(kvx_cache_moves)],
+            "kvx_cache_agent_host": [P, i64, ctypes.POINTER(i32), P, i64],
             "kvx_cache_destroy": [P],
             "kvx_cache_begin_turn": [P, i64, i32, ctypes.POINTER(i32), P, i64],
             "kvx_cache_end_turn": [P, i64],
@@ -208,6 +223,38 @@ def kv_pool_read_pages(pool, page_ids, k_dst, v_dst, stream=None) -> None:
 
 # ----------------------------------------------------------------- hot path
 
+def kv_pool_record_bytes(pool) -> int:
+    b = ctypes.c_int64()
+    _check(lib().kv_pool_record_bytes(pool, ctypes.byref(b)), "kv_pool_record_bytes")
+    return b.value
+
+
+def _host_ptr(t) -> int:
+    """Address of a pinned host tensor (or a raw int address)."""
+    if isinstance(t, int):
+        return t
+    if t.is_cuda or not t.is_contiguous():
+        raise ValueError("expected a contiguous host tensor")
+    return t.data_ptr()
+
+
+def _move(fn, pool, page_ids, slots, host, host_slots, stream):
+    ids = np.ascontiguousarray(page_ids, dtype=np.int32)
+    sl = np.ascontiguousarray(slots, dtype=np.int32)
+    if ids.shape != sl.shape:
+        raise ValueError("page_ids and slots differ in length")
+    _check(getattr(lib(), fn)(pool, ids.ctypes.data, sl.ctypes.data, ids.size, _host_ptr(host), int(host_slots),
+                              _stream(stream)), fn)
+
+
+def kv_pool_spill(pool, page_ids, slots, host, host_slots: int, stream=None) -> None:
+    _move("kv_pool_spill", pool, page_ids, slots, host, host_slots, stream)
+
+
+def kv_pool_reload(pool, page_ids, slots, host, host_slots: int, stream=None) -> None:
+    _move("kv_pool_reload", pool, page_ids, slots, host, host_slots, stream)
+
+
 def store_kv(pool, batch: Batch, k_ext, v_ext, stream=None) -> None:
     _check(lib().store_kv(pool, ctypes.byref(batch.c), _dptr(k_ext), _dptr(v_ext), _stream(stream)), "store_kv")
 
@@ -252,6 +299,14 @@ def kvx_cache_create(num_pages: int, page_size: int = 16, chunk_tokens: int = 10
     return out
 
 
+def kvx_cache_create_tiered(num_pages: int, host_pages: int, page_size: int = 16, chunk_tokens: int = 1024,
+                            policy: int = KVX_EVICT_RR):
+    out = ctypes.c_void_p()
+    _check(lib().kvx_cache_create_tiered(int(num_pages), int(host_pages), page_size, chunk_tokens, policy,
+                                         ctypes.byref(out)), "kvx_cache_create_tiered")
+    return out
+
+
 def kvx_cache_destroy(cache) -> None:
     _check(lib().kvx_cache_destroy(cache), "kvx_cache_destroy")
 
@@ -263,6 +318,35 @@ def kvx_cache_begin_turn(cache, agent: int, prompt_len: int):
     _check(lib().kvx_cache_begin_turn(cache, int(agent), int(prompt_len), ctypes.byref(prefix), ids.ctypes.data,
                                       ids.size), "kvx_cache_begin_turn")
     return prefix.value, ids
+
+
+def _moves(m: kvx_cache_moves) -> dict:
+    def arr(ptr, n):
+        return np.ctypeslib.as_array(ptr, (n,)).copy() if n else np.zeros(0, np.int32)
+    return {"spill_pages": arr(m.spill_pages, m.n_spill), "spill_slots": arr(m.spill_slots, m.n_spill),
+            "reload_pages": arr(m.reload_pages, m.n_reload), "reload_slots": arr(m.reload_slots, m.n_reload)}
+
+
+class KvxNoMemory(KvxError):
+    """ENOMEM from a tiered turn start; ``moves`` holds the spills that must still run."""
+
+    def __init__(self, err: KvxError, moves: dict):
+        super().__init__(err.status, "kvx_cache_begin_turn_tiered", str(err))
+        self.moves = moves
+
+
+def kvx_cache_begin_turn_tiered(cache, agent: int, prompt_len: int):
+    """Returns (prefix_len, page_ids, moves dict of int32 arrays spill_pages / spill_slots /
+    reload_pages / reload_slots).  On ENOMEM raises KvxNoMemory carrying the spills."""
+    ids = np.zeros(max(1, -(-int(prompt_len) // 16)), np.int32)
+    prefix = ctypes.c_int32()
+    m = kvx_cache_moves()
+    st = lib().kvx_cache_begin_turn_tiered(cache, int(agent), int(prompt_len), ctypes.byref(prefix),
+                                           ids.ctypes.data, ids.size, ctypes.byref(m))
+    if st == KVX_ENOMEM:
+        raise KvxNoMemory(KvxError(st, "kvx_cache_begin_turn_tiered", kvx_last_error()), _moves(m))
+    _check(st, "kvx_cache_begin_turn_tiered")
+    return prefix.value, ids, _moves(m)
 
 
 def kvx_cache_end_turn(cache, agent: int) -> None:
@@ -279,6 +363,16 @@ def kvx_cache_agent(cache, agent: int):
     _check(lib().kvx_cache_agent(cache, int(agent), ctypes.byref(tok), None, 0), "kvx_cache_agent")
     ids = np.zeros(tok.value // 16, np.int32)
     _check(lib().kvx_cache_agent(cache, int(agent), ctypes.byref(tok), ids.ctypes.data, ids.size), "kvx_cache_agent")
+    return tok.value, ids
+
+
+def kvx_cache_agent_host(cache, agent: int):
+    """Returns (host_tokens, host records of the agent in logical order)."""
+    tok = ctypes.c_int32()
+    _check(lib().kvx_cache_agent_host(cache, int(agent), ctypes.byref(tok), None, 0), "kvx_cache_agent_host")
+    ids = np.zeros(tok.value // 16, np.int32)
+    _check(lib().kvx_cache_agent_host(cache, int(agent), ctypes.byref(tok), ids.ctypes.data, ids.size),
+           "kvx_cache_agent_host")
     return tok.value, ids
 
 

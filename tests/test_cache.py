@@ -209,3 +209,128 @@ def test_round_robin_spreads_the_loss_on_a_replay():
     s = {p: agent_replay.replay(tr, p, num_pages, gpu=False).summary() for p in ("lru", "rr")}
     assert s["rr"]["full_misses"] < s["lru"]["full_misses"]
     assert s["rr"]["uncached_p99"] < s["lru"]["uncached_p99"]
+
+
+# ------------------------------------------------------------------ host tier
+
+class _TieredPair(_Pair):
+    """The library's tiered cache and the oracle in lockstep, plus a model of the
+    data: what (agent, logical page) each device page and host record holds, moved
+    by the cache's spills and reloads exactly as kv_pool_spill / kv_pool_reload
+    would move it, so every reused prefix can be checked to hold the agent's own
+    pages in logical order."""
+
+    def __init__(self, num_pages, host_pages, chunk_tokens, policy):
+        self.c = kvx.kvx_cache_create_tiered(num_pages, host_pages, PAGE, chunk_tokens, policy)
+        self.o = OracleCache(num_pages, PAGE, chunk_tokens, OracleCache.RR if policy == kvx.KVX_EVICT_RR
+                             else OracleCache.LRU, host_pages=host_pages)
+        self.num_pages = num_pages
+        self.host_pages = host_pages
+        self.tables = {}
+        self.dev = {}   # page -> (agent, logical page)
+        self.host = {}  # record -> (agent, logical page)
+
+    def begin(self, agent, prompt):
+        try:
+            want = self.o.begin_turn(agent, prompt)
+        except NoMemory:
+            want = None
+        try:
+            prefix, table, mv = kvx.kvx_cache_begin_turn_tiered(self.c, agent, prompt)
+        except kvx.KvxNoMemory as e:
+            assert want is None
+            self._apply(e.moves)
+            assert (len(e.moves["spill_pages"]), 0) == self.o.last_moves
+            return None
+        assert want is not None and prefix == want
+        assert (len(mv["spill_pages"]), len(mv["reload_pages"])) == self.o.last_moves
+        assert len(set(mv["spill_slots"].tolist())) == len(mv["spill_slots"])
+        self._apply(mv)
+        n = -(-prompt // PAGE)
+        assert len(table) == n and len(set(table.tolist())) == n
+        # the reused prefix holds this agent's pages in logical order
+        for j in range(prefix // PAGE):
+            assert self.dev.get(int(table[j])) == (agent, j), (agent, j)
+        # this turn writes its suffix pages (store_kv)
+        for j in range(prefix // PAGE, n):
+            self.dev[int(table[j])] = (agent, j)
+        self.tables[agent] = table
+        return prefix
+
+    def _apply(self, mv):
+        for pg, rec in zip(mv["spill_pages"], mv["spill_slots"]):
+            assert int(pg) in self.dev
+            self.host[int(rec)] = self.dev[int(pg)]
+        for pg, rec in zip(mv["reload_pages"], mv["reload_slots"]):
+            self.dev[int(pg)] = self.host[int(rec)]
+
+    def check(self):
+        super().check()
+        st = kvx.kvx_cache_stats(self.c)
+        for key in ("spilled_pages", "reloaded_pages", "host_dropped_pages", "host_used"):
+            assert st[key] == getattr(self.o, key), key
+        recs = []
+        for a in self.o.agents:
+            tok, slots = kvx.kvx_cache_agent_host(self.c, a)
+            assert tok == self.o.host_tokens(a)
+            cached = kvx.kvx_cache_agent(self.c, a)[0] // PAGE
+            for k, r in enumerate(slots.tolist()):
+                assert self.host.get(r) == (a, cached + k), "host pages must continue the device prefix"
+            recs.extend(slots.tolist())
+        assert len(recs) == len(set(recs)) == st["host_used"]
+        assert all(0 <= r < self.host_pages for r in recs)
+
+
+def _tiered_trace(seed, policy, n_agents, num_pages, host_pages, chunk_tokens, steps):
+    rng = np.random.default_rng(seed)
+    pair = _TieredPair(num_pages, host_pages, chunk_tokens, policy)
+    ctx = {}
+    active = set()
+    try:
+        for _ in range(steps):
+            a = int(rng.integers(n_agents))
+            r = rng.random()
+            if a in active:
+                if r < 0.85:
+                    pair.end(a)
+                    active.discard(a)
+                    ctx[a] += int(rng.integers(0, 300))
+            elif a in ctx and r < 0.05:
+                pair.complete(a)
+                del ctx[a]
+            else:
+                grow = int(rng.integers(1, 600)) if r < 0.9 else -int(rng.integers(0, 200))  # sometimes shorter
+                prompt = max(1, ctx.get(a, int(rng.integers(1, 400))) + grow)
+                if pair.begin(a, prompt) is not None:
+                    active.add(a)
+                    ctx[a] = prompt
+            pair.check()
+    finally:
+        pair.close()
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("policy", [kvx.KVX_EVICT_RR, kvx.KVX_EVICT_LRU])
+@pytest.mark.parametrize("host_pages", [1, 40, 400])
+def test_tiered_random_traces_match_the_oracle(seed, policy, host_pages):
+    _tiered_trace(seed, policy, n_agents=12, num_pages=500, host_pages=host_pages,
+                  chunk_tokens=64 * (1 + seed % 3), steps=500)
+
+
+@pytest.mark.parametrize("policy", [kvx.KVX_EVICT_RR, kvx.KVX_EVICT_LRU])
+def test_tiered_traces_under_heavy_pressure(policy):
+    _tiered_trace(98, policy, n_agents=30, num_pages=260, host_pages=120, chunk_tokens=16, steps=1500)
+
+
+def test_tiered_argument_errors():
+    assert _err(kvx.kvx_cache_create_tiered, 64, -1, 16, 64, kvx.KVX_EVICT_RR) == kvx.KVX_EINVAL
+    c = kvx.kvx_cache_create_tiered(64, 8, 16, 64, kvx.KVX_EVICT_RR)
+    try:
+        assert _err(kvx.kvx_cache_begin_turn, c, 1, 40) == kvx.KVX_EINVAL  # spills would be lost
+        ids = np.zeros(4, np.int32)
+        prefix = kvx.ctypes.c_int32()
+        st = kvx.lib().kvx_cache_begin_turn_tiered(c, 1, 40, kvx.ctypes.byref(prefix), ids.ctypes.data, 4, None)
+        assert st == kvx.KVX_EINVAL
+        assert kvx.kvx_cache_stats(c)["agents"] == 0
+    finally:
+        kvx.kvx_cache_destroy(c)

@@ -192,7 +192,9 @@ def test_host_tier_hand_trace():
       agent 3 loses pages 4, 3 -> drop r1, r2; r4 (p4), r5 (p3)
       agent 1 loses pages 3, 2 -> drop r3, r4; r6 (p3), r7 (p2)
       agent 3 loses pages 2, 1 -> drop r5, r6; r8 (p2), r9 (p1)
-    leaving agent 1 = device p1 + host p2, agent 2 = nothing, agent 3 = host p1, p2."""
+    leaving agent 1 = device p1 + host p2, agent 2 = nothing, agent 3 = host p1, p2.
+    r1 .. r6 were written and dropped within this one turn start, so their spills
+    are void: only r7, r8, r9 are written."""
     c = OracleCache(12, PAGE, 2 * PAGE, OracleCache.RR, host_pages=3)
     _fill(c, 1, 5)
     _fill(c, 2, 1)
@@ -200,8 +202,8 @@ def test_host_tier_hand_trace():
     assert c.begin_turn(9, 11 * PAGE) == 0
     assert [c.cached_tokens(i) // PAGE for i in (1, 2, 3)] == [1, 0, 0]
     assert [c.host_tokens(i) // PAGE for i in (1, 2, 3)] == [1, 0, 2]
-    assert c.last_moves == (9, 0)
-    assert (c.spilled_pages, c.host_dropped_pages, c.host_used) == (9, 6, 3)
+    assert c.last_moves == (3, 0)
+    assert (c.spilled_pages, c.host_dropped_pages, c.host_used) == (3, 0, 3)
     c.end_turn(9)
     # agent 3 returns with a 5-page prompt: both host pages come back, 3 new pages
     free_before = c.free
