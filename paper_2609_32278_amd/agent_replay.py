@@ -13,6 +13,12 @@ signal (Section 3.2).
 The figures this produces are the paper's: uncached prompt tokens per returning
 turn (Section 4) and, with the GPU, the time of each batch's KV store + attention.
 
+With a host tier (``--host-pages``, the paper's future work in Section 6), pages
+the policy evicts are spilled to pinned host memory and a returning agent's
+spilled pages are reloaded instead of recomputed: each turn start's spills and
+reloads run on the pool (kv_pool_spill / kv_pool_reload, in call order) before the
+batch's store, inside the batch's timed region.
+
     python -m paper_2609_32278_amd.agent_replay --policy both --agents 48 --turns 8
 """
 
@@ -38,8 +44,9 @@ class TurnRecord:
     turn: int
     tick: int
     prompt: int        # tokens of the turn's prompt
-    prefix: int        # tokens reused from the cache
+    prefix: int        # tokens reused from the cache (device pages and reloaded host pages)
     history: int       # tokens of context the agent had before this turn
+    reloaded: int = 0  # tokens of the prefix reloaded from the host tier
 
     @property
     def uncached(self) -> int:
@@ -56,6 +63,7 @@ class ReplayResult:
     policy: str
     turns: list = field(default_factory=list)
     events: list = field(default_factory=list)   # ("begin", agent, prompt, prefix | None), ("end", a), ("complete", a)
+    moves: list = field(default_factory=list)    # per tiered turn start: (spills, reloads) page counts
     batch_ms: list = field(default_factory=list)
     stats: dict = field(default_factory=dict)
     cache_calls: int = 0
@@ -81,6 +89,7 @@ class ReplayResult:
                 "history_recomputed_mean": float(x.mean()),
                 "history_recomputed_p99": float(np.percentile(x, 99)),
                 "full_misses": int(sum(1 for t in back if t.prefix == 0)),
+                "reloaded_tokens_total": int(sum(t.reloaded for t in back)),
             })
         if self.batch_ms:
             b = np.array(self.batch_ms)
@@ -92,16 +101,39 @@ class ReplayResult:
 
 
 def replay(tr: wl.AgentTrace, policy: str, num_pages: int, *, chunk_tokens: int = 1024, decode_ticks: int = 2,
-           completion_signals: bool = True, gpu: bool = True, on_batch=None, max_ticks: int = 1_000_000) -> ReplayResult:
+           completion_signals: bool = True, gpu: bool = True, on_batch=None, max_ticks: int = 1_000_000,
+           host_pages: int = 0, layer_gemms: tuple | None = None) -> ReplayResult:
     """Run the trace; `on_batch(requests, q, out)` sees each GPU batch (requests:
-    list of TurnRecord, q / out: the batch's [rows, Hq, d] tensors)."""
+    list of TurnRecord, q / out: the batch's [rows, Hq, d] tensors).  With
+    `layer_gemms` = (hidden, ffn), each batch's timed region also runs the
+    projection and MLP GEMMs of one transformer layer (torch bf16 matmuls with
+    random weights) for its uncached tokens, so that the batch time is the
+    recompute cost of a whole layer rather than of its attention alone."""
     res = ReplayResult(policy)
-    cache = kvx.kvx_cache_create(num_pages, wl.PAGE_SIZE, chunk_tokens, POLICIES[policy])
+    tiered = host_pages > 0
+    cache = kvx.kvx_cache_create_tiered(num_pages, host_pages, wl.PAGE_SIZE, chunk_tokens, POLICIES[policy])
     pool = None
     torch = None
+    host = None
     if gpu:
         import torch  # noqa: F811  (device memory and streams only)
         pool = kvx.kv_pool_create(num_pages, wl.PAGE_SIZE, tr.num_kv_heads, tr.head_dim)
+        if tiered:
+            host = torch.empty(host_pages * kvx.kv_pool_record_bytes(pool), dtype=torch.uint8, pin_memory=True)
+    tier = (host, host_pages)
+    if gpu:
+        _warmup(tr, pool, torch, tier)
+    gemm = None
+    if gpu and layer_gemms is not None:
+        H, F = layer_gemms
+        g = torch.Generator(device="cuda").manual_seed(11)
+        qkv = (tr.num_q_heads + 2 * tr.num_kv_heads) * tr.head_dim
+
+        def wgt(a, b):
+            return (torch.randn((a, b), generator=g, device="cuda") * a ** -0.5).to(torch.bfloat16)
+
+        gemm = {"x": H, "w_qkv": wgt(H, qkv), "w_o": wgt(tr.num_q_heads * tr.head_dim, H),
+                "w_gu": wgt(H, 2 * F), "w_d": wgt(F, H)}
     n = tr.num_agents
     turns = len(tr.new[0])
     ctx = [0] * n
@@ -131,30 +163,45 @@ def replay(tr: wl.AgentTrace, policy: str, num_pages: int, *, chunk_tokens: int 
                             kvx.kvx_cache_complete(cache, a)
                             res.events.append(("complete", a))
             batch = []
+            moves = []  # page moves of this tick's turn starts, in call order
             for a in range(n):
                 if done[a] or running_until[a] >= 0 or due[a] > tick:
                     continue
                 prompt = ctx[a] + tr.new[a][turn[a]]
                 t0 = time.perf_counter()
+                mv = None
                 try:
-                    prefix, table = kvx.kvx_cache_begin_turn(cache, a, prompt)
+                    if tiered:
+                        prefix, table, mv = kvx.kvx_cache_begin_turn_tiered(cache, a, prompt)
+                    else:
+                        prefix, table = kvx.kvx_cache_begin_turn(cache, a, prompt)
                 except kvx.KvxError as e:
                     res.cache_seconds += time.perf_counter() - t0
                     res.cache_calls += 1
                     if e.status != kvx.KVX_ENOMEM:
                         raise
+                    if isinstance(e, kvx.KvxNoMemory):  # its spills still run
+                        moves.append(e.moves)
+                        res.moves.append((len(e.moves["spill_pages"]), 0))
                     res.events.append(("begin", a, prompt, None))
                     continue  # waits for pages to free up
                 res.cache_seconds += time.perf_counter() - t0
                 res.cache_calls += 1
                 res.events.append(("begin", a, prompt, prefix))
-                rec = TurnRecord(a, turn[a], tick, prompt, prefix, ctx[a])
+                reloaded = 0
+                if mv is not None:
+                    moves.append(mv)
+                    res.moves.append((len(mv["spill_pages"]), len(mv["reload_pages"])))
+                    reloaded = len(mv["reload_pages"]) * wl.PAGE_SIZE
+                rec = TurnRecord(a, turn[a], tick, prompt, prefix, ctx[a], reloaded)
                 res.turns.append(rec)
                 batch.append((rec, table))
                 running_until[a] = tick + decode_ticks
                 ctx[a] = prompt
-            if batch and gpu:
-                res.batch_ms.append(_run_batch(tr, pool, batch, on_batch, torch))
+            if (batch or moves) and gpu:
+                ms = _run_batch(tr, pool, batch, on_batch, torch, moves, tier, gemm)
+                if batch:
+                    res.batch_ms.append(ms)
             tick += 1
         res.stats = kvx.kvx_cache_stats(cache)
     finally:
@@ -164,8 +211,68 @@ def replay(tr: wl.AgentTrace, policy: str, num_pages: int, *, chunk_tokens: int 
     return res
 
 
-def _run_batch(tr, pool, batch, on_batch, torch) -> float:
+def _warmup(tr, pool, torch, tier):
+    """Run every kernel a batch may use once, untimed, so that no batch pays for
+    loading code: store_kv, a short and a split extend_attention, the page moves."""
+    n = min(int(kvx.kv_pool_layout(pool)["num_pages"]), 4096 // wl.PAGE_SIZE + 2)
+    ids = torch.arange(n, dtype=torch.int32, device="cuda")
+    for P, E in ((0, 64), ((n - 2) * wl.PAGE_SIZE, 16)):
+        b = kvx.Batch([P], [E], [0, n], ids)
+        k = torch.zeros((E, tr.num_kv_heads, tr.head_dim), dtype=torch.bfloat16, device="cuda")
+        q = torch.zeros((E, tr.num_q_heads, tr.head_dim), dtype=torch.bfloat16, device="cuda")
+        kvx.store_kv(pool, b, k, k)
+        kvx.extend_attention(pool, b, q, tr.num_q_heads, tr.sm_scale, torch.empty_like(q))
+    host, host_pages = tier
+    if host is not None:
+        kvx.kv_pool_spill(pool, [0], [0], host, host_pages)
+        kvx.kv_pool_reload(pool, [0], [0], host, host_pages)
+    torch.cuda.synchronize()
+
+
+def _run_moves(pool, moves, tier, kvx_mod=kvx):
+    host, host_pages = tier
+    for mv in moves:  # in call order: a later call may reuse records an earlier one reloaded from
+        if len(mv["spill_pages"]):
+            kvx_mod.kv_pool_spill(pool, mv["spill_pages"], mv["spill_slots"], host, host_pages)
+        if len(mv["reload_pages"]):
+            kvx_mod.kv_pool_reload(pool, mv["reload_pages"], mv["reload_slots"], host, host_pages)
+
+
+GEMM_BUCKET = 512  # GEMM rows are padded to a multiple of this (one library kernel choice per bucket)
+
+
+def _layer_inputs(gemm, T, torch):
+    """N(0, 1) activations for T tokens, grown outside the timed region, and one
+    untimed run of the bucket's GEMMs the first time it is used (the library
+    picks and loads its kernels per shape)."""
+    m = -(-T // GEMM_BUCKET) * GEMM_BUCKET
+    if gemm.get("x_buf") is None or gemm["x_buf"].shape[0] < m:
+        n = max(m, 2 * (0 if gemm.get("x_buf") is None else gemm["x_buf"].shape[0]))
+        gemm["x_buf"] = torch.randn((n, gemm["x"]), device="cuda").to(torch.bfloat16)
+        gemm["o_buf"] = torch.randn((n, gemm["w_o"].shape[0]), device="cuda").to(torch.bfloat16)
+    seen = gemm.setdefault("seen", set())
+    if m not in seen:
+        seen.add(m)
+        _layer_gemms(gemm, T, torch)
+
+
+def _layer_gemms(gemm, T, torch):
+    """Projection and MLP GEMMs of one layer for T tokens (padded to the bucket;
+    values unused)."""
+    m = -(-T // GEMM_BUCKET) * GEMM_BUCKET
+    x = gemm["x_buf"][:m]
+    torch.matmul(x, gemm["w_qkv"])
+    o = torch.matmul(gemm["o_buf"][:m], gemm["w_o"])
+    gu = torch.matmul(o, gemm["w_gu"])
+    f = gemm["w_d"].shape[0]
+    torch.matmul(torch.nn.functional.silu(gu[:, :f]) * gu[:, f:], gemm["w_d"])
+
+
+def _run_batch(tr, pool, batch, on_batch, torch, moves=(), tier=(None, 0), gemm=None) -> float:
     dev = "cuda"
+    if not batch:  # only spills of failed turn starts
+        _run_moves(pool, moves, tier)
+        return 0.0
     P = np.array([r.prefix for r, _ in batch], np.int32)
     E = np.array([r.uncached for r, _ in batch], np.int32)
     indptr = np.zeros(len(batch) + 1, np.int32)
@@ -184,9 +291,14 @@ def _run_batch(tr, pool, batch, on_batch, torch) -> float:
     out = torch.empty_like(q)
     stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if gemm is not None:
+        _layer_inputs(gemm, int(E.sum()), torch)
     e0.record(stream)
+    _run_moves(pool, moves, tier)
     kvx.store_kv(pool, b, k_ext, v_ext)
     kvx.extend_attention(pool, b, q, tr.num_q_heads, tr.sm_scale, out)
+    if gemm is not None:
+        _layer_gemms(gemm, int(E.sum()), torch)
     e1.record(stream)
     e1.synchronize()
     if on_batch is not None:
@@ -205,17 +317,24 @@ def main(argv=None) -> int:
     ap.add_argument("--chunk-tokens", type=int, default=1024)
     ap.add_argument("--decode-ticks", type=int, default=2)
     ap.add_argument("--heads", default="32,8,128", help="Hq,Hkv,head_dim")
+    ap.add_argument("--host-pages", type=float, default=0.0,
+                    help="host tier size as a multiple of the device pool (0: no host tier)")
+    ap.add_argument("--layer-gemms", default="",
+                    help="hidden,ffn: time each batch with one layer's projection + MLP GEMMs (e.g. 4096,14336)")
     ap.add_argument("--no-gpu", action="store_true")
     args = ap.parse_args(argv)
+    lg = tuple(int(x) for x in args.layer_gemms.split(",")) if args.layer_gemms else None
     hq, hkv, d = (int(x) for x in args.heads.split(","))
     tr = wl.make_agent_trace(args.agents, args.turns, seed=args.seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d)
     total = sum(tr.max_context(i) for i in range(tr.num_agents))
     num_pages = int(args.capacity * total) // wl.PAGE_SIZE
     for pol in (["lru", "rr"] if args.policy == "both" else [args.policy]):
+        host_pages = int(args.host_pages * num_pages)
         r = replay(tr, pol, num_pages, chunk_tokens=args.chunk_tokens, decode_ticks=args.decode_ticks,
-                   gpu=not args.no_gpu)
+                   gpu=not args.no_gpu, host_pages=host_pages, layer_gemms=lg)
         s = r.summary()
-        s.update({"agents": args.agents, "turns_per_agent": args.turns, "num_pages": num_pages,
+        s.update({"agents": args.agents, "turns_per_agent": args.turns, "num_pages": num_pages, "host_pages": host_pages,
+                  "layer_gemms": list(lg) if lg else None,
                   "context_tokens_total": total, "heads": [hq, hkv, d], "chunk_tokens": args.chunk_tokens})
         print(json.dumps(s), flush=True)
     return 0

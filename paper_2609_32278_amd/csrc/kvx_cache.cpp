@@ -59,6 +59,13 @@ struct kvx_cache {
   std::vector<uint8_t> rec_live;
   int64_t host_used = 0, spilled = 0, reloaded = 0, host_dropped = 0;
   std::vector<int32_t> mv_spill_pages, mv_spill_slots, mv_reload_pages, mv_reload_slots;
+  // per turn start: FIFO entries before fifo_scan belong to the agent inside the
+  // turn (pinned for the whole call); rec_call / rec_move locate a record's spill
+  // in this call's move list
+  size_t fifo_scan = 0;
+  uint64_t call = 0;
+  std::vector<uint64_t> rec_call;
+  std::vector<int32_t> rec_move;
 };
 
 namespace {
@@ -105,15 +112,16 @@ int32_t take_record(kvx_cache* c, int64_t owner) {
     rec = c->host_free.back();
     c->host_free.pop_back();
   } else {
-    for (auto it = c->host_fifo.begin(); it != c->host_fifo.end();) {
+    for (auto it = c->host_fifo.begin() + (std::ptrdiff_t)c->fifo_scan; it != c->host_fifo.end();) {
       const int32_t r = it->rec;
       if (!c->rec_live[(size_t)r] || c->rec_gen[(size_t)r] != it->gen) {
         it = c->host_fifo.erase(it);  // freed since
         continue;
       }
       CacheAgent& o = c->agents.find(c->rec_owner[(size_t)r])->second;
-      if (o.active) {
+      if (o.active) {  // the agent inside the turn: stays active for the rest of the call
         ++it;
+        c->fifo_scan++;
         continue;
       }
       // r is o's farthest host page (one agent's spills enter the FIFO farthest
@@ -129,11 +137,9 @@ int32_t take_record(kvx_cache* c, int64_t owner) {
       c->host_used--;
       rec = r;
       // a record spilled into earlier in this same call: that spill is void (its
-      // page is simply dropped) and leaves the move list
-      auto mv = std::find(c->mv_spill_slots.begin(), c->mv_spill_slots.end(), r);
-      if (mv != c->mv_spill_slots.end()) {
-        c->mv_spill_pages.erase(c->mv_spill_pages.begin() + (mv - c->mv_spill_slots.begin()));
-        c->mv_spill_slots.erase(mv);
+      // page is simply dropped); its move is struck out and removed at the end
+      if (c->rec_call[(size_t)r] == c->call) {
+        c->mv_spill_pages[(size_t)c->rec_move[(size_t)r]] = -1;
         c->spilled--;
       } else {
         c->host_dropped++;
@@ -152,6 +158,7 @@ int32_t take_record(kvx_cache* c, int64_t owner) {
     for (const FifoEntry& e : c->host_fifo)
       if (c->rec_live[(size_t)e.rec] && c->rec_gen[(size_t)e.rec] == e.gen) live.push_back(e);
     c->host_fifo.swap(live);
+    c->fifo_scan = 0;  // recounted by the next walk
   }
   return rec;
 }
@@ -170,6 +177,8 @@ void evict_tail(kvx_cache* c, int64_t id, CacheAgent& a, int64_t n) {
     const int32_t rec = take_record(c, id);
     if (rec < 0) continue;  // dropped: the agent holds no host pages past it
     a.host.push_front(rec);
+    c->rec_call[(size_t)rec] = c->call;
+    c->rec_move[(size_t)rec] = (int32_t)c->mv_spill_pages.size();
     c->mv_spill_pages.push_back(pg);
     c->mv_spill_slots.push_back(rec);
     c->spilled++;
@@ -263,6 +272,8 @@ int kvx_cache_create_tiered(int64_t num_pages, int64_t host_pages, int32_t page_
     c->rec_owner.assign((size_t)host_pages, 0);
     c->rec_gen.assign((size_t)host_pages, 0);
     c->rec_live.assign((size_t)host_pages, 0);
+    c->rec_call.assign((size_t)host_pages, 0);
+    c->rec_move.assign((size_t)host_pages, 0);
   } catch (...) {
     delete c;
     return report(KVX_ENOMEM, "free lists of %lld pages and %lld records", (long long)num_pages,
@@ -302,6 +313,8 @@ static int begin_turn(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_t* 
   c->mv_spill_slots.clear();
   c->mv_reload_pages.clear();
   c->mv_reload_slots.clear();
+  c->fifo_scan = 0;
+  c->call++;
   CacheAgent& a = c->agents[agent];
   a.stamp = ++c->clock;  // matching the prefix touches every node of the path
   // reuse device pages, then host pages, up to the last whole page before the final token
@@ -323,6 +336,15 @@ static int begin_turn(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_t* 
   }
   auto fill_moves = [&]() {
     if (moves == nullptr) return;
+    size_t w = 0;  // drop the struck-out (void) spills
+    for (size_t i = 0; i < c->mv_spill_pages.size(); i++)
+      if (c->mv_spill_pages[i] >= 0) {
+        c->mv_spill_pages[w] = c->mv_spill_pages[i];
+        c->mv_spill_slots[w] = c->mv_spill_slots[i];
+        w++;
+      }
+    c->mv_spill_pages.resize(w);
+    c->mv_spill_slots.resize(w);
     moves->spill_pages = c->mv_spill_pages.data();
     moves->spill_slots = c->mv_spill_slots.data();
     moves->reload_pages = c->mv_reload_pages.data();

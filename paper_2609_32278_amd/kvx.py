@@ -322,7 +322,10 @@ def kvx_cache_begin_turn(cache, agent: int, prompt_len: int):
 
 def _moves(m: kvx_cache_moves) -> dict:
     def arr(ptr, n):
-        return np.ctypeslib.as_array(ptr, (n,)).copy() if n else np.zeros(0, np.int32)
+        out = np.empty(n, np.int32)
+        if n:
+            ctypes.memmove(out.ctypes.data, ptr, 4 * n)
+        return out
     return {"spill_pages": arr(m.spill_pages, m.n_spill), "spill_slots": arr(m.spill_slots, m.n_spill),
             "reload_pages": arr(m.reload_pages, m.n_reload), "reload_slots": arr(m.reload_slots, m.n_reload)}
 

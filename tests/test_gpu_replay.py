@@ -21,8 +21,10 @@ def _trace():
                                spread=3, num_q_heads=8, num_kv_heads=2, head_dim=64)
 
 
-def _replay_oracle(events, num_pages, chunk_tokens, policy):
-    o = OracleCache(num_pages, 16, chunk_tokens, OracleCache.RR if policy == "rr" else OracleCache.LRU)
+def _replay_oracle(events, num_pages, chunk_tokens, policy, host_pages=0, moves=None):
+    o = OracleCache(num_pages, 16, chunk_tokens, OracleCache.RR if policy == "rr" else OracleCache.LRU,
+                    host_pages=host_pages)
+    mv = iter(moves or [])
     for ev in events:
         if ev[0] == "begin":
             try:
@@ -30,6 +32,8 @@ def _replay_oracle(events, num_pages, chunk_tokens, policy):
             except NoMemory:
                 got = None
             assert got == ev[3], ev
+            if host_pages:
+                assert next(mv) == o.last_moves, ev
         elif ev[0] == "end":
             o.end_turn(ev[1])
         else:
@@ -63,3 +67,35 @@ def test_replay_batches_match_brute_force(policy):
     # some returning turns reuse part of their history, some recompute
     back = [t for t in checked if t.turn > 0]
     assert any(0 < t.prefix for t in back) and any(t.recomputed_history > 0 for t in back)
+
+
+@pytest.mark.parametrize("policy", ["lru", "rr"])
+def test_replay_with_a_host_tier_matches_brute_force(policy):
+    """The same replay with a host tier of a quarter of the pool: evicted pages are
+    spilled to pinned host memory and reloaded by returning agents; every batch's
+    rows -- prefixes partly reloaded -- must still match brute force over the
+    agent's logical context."""
+    tr = _trace()
+    total = sum(tr.max_context(i) for i in range(tr.num_agents))
+    num_pages = int(0.45 * total) // 16
+    host_pages = num_pages // 4
+    print(f"[replay-tier] policy={policy} pages={num_pages} host={host_pages}", flush=True)
+    checked = []
+
+    def on_batch(reqs, q, out):
+        row = 0
+        for r in reqs:
+            k, v = wl.agent_kv(tr, r.agent, r.prompt, "cuda")
+            ref, _ = brute_force(to_f64(q[row:row + r.uncached]), to_f64(k), to_f64(v), r.prefix, tr.sm_scale)
+            got = out[row:row + r.uncached].float().cpu().numpy()
+            compare(got, ref, f"{policy}+host agent {r.agent} turn {r.turn} P={r.prefix} "
+                              f"(reloaded {r.reloaded}) E={r.uncached}")
+            row += r.uncached
+            checked.append(r)
+
+    res = agent_replay.replay(tr, policy, num_pages, chunk_tokens=64, on_batch=on_batch, host_pages=host_pages)
+    torch.cuda.synchronize()
+    assert len(checked) == tr.num_agents * len(tr.new[0])
+    _replay_oracle(res.events, num_pages, 64, policy, host_pages, res.moves)
+    assert res.stats["spilled_pages"] > 0 and res.stats["reloaded_pages"] > 0
+    assert any(t.reloaded > 0 for t in checked)
