@@ -22,6 +22,9 @@
  *   - "host" pointers are ordinary CPU memory read during the call;
  *     "device" pointers are GPU memory (hipMalloc / torch CUDA tensors).
  *   - bf16 means IEEE binary32 truncated to its upper 16 bits (2 bytes).
+ *   - Row buffers (Q, O, K_ext, V_ext, page I/O buffers, norm weights, spill
+ *     records) must start 16-byte aligned (the kernels move 16-byte pieces);
+ *     the argument checks reject other addresses with KVX_EINVAL.
  *   - Rows of Q, O, K_ext and V_ext are the suffix tokens of all requests,
  *     request by request: request r owns rows [sum_{s<r} E_s, sum_{s<=r} E_s).
  *   - Page ids outside [0, num_pages) are undefined behaviour unless the

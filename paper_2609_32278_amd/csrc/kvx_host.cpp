@@ -172,6 +172,13 @@ int check_pool(const kvx_pool* pool) {
   return KVX_OK;
 }
 
+// The kernels move 16-byte pieces: every bf16 row buffer must start 16-byte aligned.
+int check_align(const void* ptr, const char* name) {
+  if (ptr != nullptr && ((uintptr_t)ptr & 15u) != 0)
+    return fail(KVX_EINVAL, "%s = %p is not 16-byte aligned", name, ptr);
+  return KVX_OK;
+}
+
 int use_device(const kvx_pool* pool) {
   int cur = -1;
   KVX_HIP(hipGetDevice(&cur));
@@ -644,6 +651,8 @@ static int page_io(kvx_pool* pool, const int32_t* page_ids, int64_t n, void* k_l
   if (n < 0) return fail(KVX_EINVAL, "n = %lld < 0", (long long)n);
   if (n == 0) return KVX_OK;
   if (!page_ids || !k_lin || !v_lin) return fail(KVX_EINVAL, "page_ids, K and V buffers must be non-NULL");
+  if (int rc = check_align(k_lin, "K buffer")) return rc;
+  if (int rc = check_align(v_lin, "V buffer")) return rc;
   if (n > (int64_t)INT32_MAX) return fail(KVX_EINVAL, "too many pages");
   for (int64_t i = 0; i < n; i++)
     if (page_ids[i] < 0 || page_ids[i] >= pool->num_pages)
@@ -698,6 +707,7 @@ static int page_move(kvx_pool* pool, const int32_t* page_ids, const int32_t* slo
                                            (long long)host_slots);
   if (n == 0) return KVX_OK;
   if (!page_ids || !slots || !host) return fail(KVX_EINVAL, "page_ids, slots and host must be non-NULL");
+  if (int rc = check_align(host, "host")) return rc;
   if (n > (int64_t)INT32_MAX) return fail(KVX_EINVAL, "too many pages");
   for (int64_t i = 0; i < n; i++) {
     if (page_ids[i] < 0 || page_ids[i] >= pool->num_pages)
@@ -757,6 +767,8 @@ int store_kv(kvx_pool* pool, const kvx_batch* batch, const void* k_ext, const vo
   if (int rc = check_batch(batch, qo)) return rc;
   if (qo.back() == 0) return KVX_OK;
   if (!k_ext || !v_ext) return fail(KVX_EINVAL, "k_ext and v_ext must be non-NULL");
+  if (int rc = check_align(k_ext, "k_ext")) return rc;
+  if (int rc = check_align(v_ext, "v_ext")) return rc;
   if (int rc = use_device(pool)) return rc;
   hipStream_t s = (hipStream_t)stream;
   if (validate_mode())
@@ -823,8 +835,16 @@ int store_kv_rope(kvx_pool* pool, const kvx_batch* batch, const kvx_rope* rope, 
   }
   if (num_q_heads < 0) return fail(KVX_EINVAL, "num_q_heads = %d < 0", num_q_heads);
   if (num_q_heads > 0 && (!q || !q_out)) return fail(KVX_EINVAL, "q and q_out must be non-NULL");
+  if (num_q_heads > 0) {
+    if (int rc = check_align(q, "q")) return rc;
+    if (int rc = check_align(q_out, "q_out")) return rc;
+  }
+  if (int rc = check_align(rope->q_norm, "q_norm")) return rc;
+  if (int rc = check_align(rope->k_norm, "k_norm")) return rc;
   if (qo.back() == 0) return KVX_OK;
   if (!k_ext || !v_ext) return fail(KVX_EINVAL, "k_ext and v_ext must be non-NULL");
+  if (int rc = check_align(k_ext, "k_ext")) return rc;
+  if (int rc = check_align(v_ext, "v_ext")) return rc;
   if (int rc = use_device(pool)) return rc;
   hipStream_t s = (hipStream_t)stream;
   if (validate_mode())
@@ -908,6 +928,9 @@ int extend_attention(kvx_pool* pool, const kvx_batch* batch, const void* q, int3
   if (int rc = check_batch(batch, qo)) return rc;
   if (qo.back() == 0) return KVX_OK;
   if (!q || !out) return fail(KVX_EINVAL, "q and out must be non-NULL");
+  if (int rc = check_align(q, "q")) return rc;
+  if (int rc = check_align(out, "out")) return rc;
+  if (lse != nullptr && ((uintptr_t)lse & 3u) != 0) return fail(KVX_EINVAL, "lse is not 4-byte aligned");
   if (int rc = use_device(pool)) return rc;
   hipStream_t s = (hipStream_t)stream;
   if (validate_mode())

@@ -237,6 +237,14 @@ def test_argument_errors():
         assert err(norm_eps=-1.0) == kvx.KVX_EINVAL
         assert err(q=None) == kvx.KVX_EINVAL
         assert err(num_q_heads=-1) == kvx.KVX_EINVAL
+        assert err(q_out=t["q"].data_ptr() + 2) == kvx.KVX_EINVAL          # not 16-byte aligned
+        with pytest.raises(kvx.KvxError) as e:
+            kvx.store_kv(pool, batch, t["k_ext"].data_ptr() + 8, t["v_ext"])
+        assert e.value.status == kvx.KVX_EINVAL
+        out = torch.empty_like(t["q"])
+        with pytest.raises(kvx.KvxError) as e:
+            kvx.extend_attention(pool, batch, t["q"].data_ptr() + 4, w.num_q_heads, w.sm_scale, out)
+        assert e.value.status == kvx.KVX_EINVAL
         torch.cuda.synchronize()
     finally:
         kvx.kv_pool_destroy(pool)

@@ -91,6 +91,7 @@ def test_spill_argument_errors():
         assert err(kvx.kv_pool_spill, [0], [4]) == kvx.KVX_ERANGE
         assert err(kvx.kv_pool_spill, [0, 1], [2, 2]) == kvx.KVX_EINVAL
         assert err(kvx.kv_pool_reload, [3, 3], [0, 1]) == kvx.KVX_EINVAL
+        assert err(kvx.kv_pool_spill, [0], [0], pinned.data_ptr() + 8) == kvx.KVX_EINVAL  # alignment
         kvx.kv_pool_spill(pool, [0, 0], [0, 1], pinned, 4)   # reading a page twice is fine
         kvx.kv_pool_reload(pool, [5, 6], [0, 0], pinned, 4)  # so is reading a record twice
         torch.cuda.synchronize()
