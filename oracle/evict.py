@@ -52,6 +52,16 @@ instead of dropping it), when ``host_pages`` > 0:
    are pinned while the turn allocates) and their records freed.  Pages past
    the limit are dropped, host pages first.  An agent inside a turn holds no
    host pages.
+
+Recency tiering (Section 3.2, stale trajectories without completion signals;
+the paper describes it and does not evaluate it), when ``tier_width`` > 0:
+
+10. Idle agents with evictable pages fall into tiers by age = now - stamp in
+    the cache's logical clock (one tick per turn start and turn end): tier =
+    age // tier_width.  A reclamation visits tiers from the oldest to the
+    newest and runs Algorithm 1's round robin within each (queue in agent-id
+    order after the agent that lost the last chunk), moving to the next tier
+    once the current one holds nothing evictable.
 """
 
 from __future__ import annotations
@@ -81,8 +91,11 @@ class OracleCache:
     LRU = 0
     RR = 1
 
-    def __init__(self, num_pages: int, page_size: int, chunk_tokens: int, policy: int, host_pages: int = 0) -> None:
+    def __init__(self, num_pages: int, page_size: int, chunk_tokens: int, policy: int, host_pages: int = 0,
+                 tier_width: int = 0) -> None:
         assert page_size == 16 and chunk_tokens % page_size == 0 and chunk_tokens > 0 and host_pages >= 0
+        assert tier_width >= 0
+        self.tier_width = tier_width
         self.host_pages = host_pages
         self.records: list[tuple[int, int]] = []  # live host records (id, owner), oldest first
         self.next_record = 0
@@ -157,12 +170,26 @@ class OracleCache:
     # -- Algorithm 1 ---------------------------------------------------------
     def _reclaim_rr(self, M: int) -> None:
         ids = sorted(i for i in self.agents if self._evictable(i))
+        if self.tier_width == 0:
+            groups = [ids]
+        else:  # recency tiers, oldest first
+            tiers: dict[int, list[int]] = {}
+            for i in ids:
+                tiers.setdefault((self.clock - self.agents[i].stamp) // self.tier_width, []).append(i)
+            groups = [tiers[k] for k in sorted(tiers, reverse=True)]
+        freed = 0
+        for group in groups:
+            freed = self._round_robin(group, M, freed)
+            if freed >= M:
+                return
+
+    def _round_robin(self, ids: list[int], M: int, freed: int) -> int:
+        """Algorithm 1 over the idle agents `ids` (in id order); returns M_freed."""
         if self.rr_last is None:
             order = ids
         else:
             order = [i for i in ids if i > self.rr_last] + [i for i in ids if i <= self.rr_last]
         Q = deque(order)
-        freed = 0
         while freed < M and Q:
             tau = Q.popleft()
             if not self._evictable(tau):  # active, or no evictable suffix
@@ -176,6 +203,7 @@ class OracleCache:
             self.rr_last = tau
             if self._evictable(tau):
                 Q.append(tau)
+        return freed
 
     # -- LRU baseline ----------------------------------------------------------
     def _reclaim_lru(self, M: int) -> None:

@@ -279,3 +279,72 @@ def test_records_of_an_agent_inside_a_turn_are_never_dropped():
     assert c.begin_turn(1, 6 * PAGE) == 4 * PAGE  # 2 reloads + 2 new pages: 3 free + 1 of agent 2's
     assert c.last_moves == (0, 2) and c.host_dropped_pages == 0
     assert (c.cached_tokens(2), c.host_tokens(2)) == (PAGE, 0)
+
+
+# ------------------------------------------------------------------ recency tiers
+
+@pytest.mark.parametrize("seed", range(3))
+def test_one_wide_tier_is_plain_round_robin(seed):
+    """A tier wider than the whole clock puts every idle agent in one tier:
+    Algorithm 1 exactly."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    a = OracleCache(300, PAGE, 2 * PAGE, OracleCache.RR)
+    b = OracleCache(300, PAGE, 2 * PAGE, OracleCache.RR, tier_width=10 ** 9)
+    ctx, active = {}, set()
+    for _ in range(400):
+        ag = int(rng.integers(10))
+        if ag in active:
+            a.end_turn(ag), b.end_turn(ag)
+            active.discard(ag)
+            ctx[ag] += int(rng.integers(0, 100))
+            continue
+        prompt = ctx.get(ag, 0) + int(rng.integers(1, 300))
+        try:
+            ra = a.begin_turn(ag, prompt)
+        except NoMemory:
+            ra = None
+        try:
+            rb = b.begin_turn(ag, prompt)
+        except NoMemory:
+            rb = None
+        assert ra == rb
+        if ra is not None:
+            active.add(ag)
+            ctx[ag] = prompt
+    assert a.evictions == b.evictions > 0
+
+
+@pytest.mark.parametrize("n,na,m", REGIME)
+def test_unit_tiers_turn_round_robin_into_whole_agent_eviction(n, na, m):
+    """Tiers one clock tick wide hold one agent each: the oldest idle agent loses
+    its whole prefix before the next is touched -- Equation 3's LRU outcome."""
+    ns = n - na
+    u = 8 * ns
+    c = OracleCache(m * u, PAGE, PAGE, OracleCache.RR, tier_width=1)
+    for i in range(ns):
+        _fill(c, i, u)
+    for j in range(na):
+        c.begin_turn(1000 + j, u * PAGE)
+    kept = [c.cached_tokens(i) / (u * PAGE) for i in range(ns)]
+    assert kept == [0.0] * (n - m) + [1.0] * (m - na)
+
+
+def test_tiers_evict_stale_agents_first():
+    """Agents 1 and 2 finished long ago without a completion signal; agents 3 and 4
+    are recent.  With tiers the stale pair loses its pages first (round-robin
+    between them); plain round robin spreads the loss over all four."""
+    def run(width):
+        c = OracleCache(64, PAGE, PAGE, OracleCache.RR, tier_width=width)
+        for a in (1, 2):
+            _fill(c, a, 8)
+        for k in range(20):          # time passes: other agents' short turns
+            c.begin_turn(100 + k, PAGE)
+            c.end_turn(100 + k)
+            c.complete(100 + k)
+        for a in (3, 4):
+            _fill(c, a, 8)
+        c.begin_turn(9, (c.free + 6) * PAGE)   # reclaim 6 pages
+        return [c.cached_tokens(a) // PAGE for a in (1, 2, 3, 4)]
+    assert run(8) == [5, 5, 8, 8]
+    assert sorted(run(0)) != [5, 5, 8, 8] and sum(run(0)) == 26
