@@ -26,7 +26,9 @@
  *                  queue while it holds pages.  Eligibility (idle, non-empty) is
  *                  rechecked at every pop.
  * Completion signals (Section 3.2, "Handling stale agent trajectories") are
- * kvx_cache_complete: the agent's pages are freed at once.
+ * kvx_cache_complete: the agent's pages are freed at once.  Without them, the
+ * same passage's recency tiering keeps stale agents from holding pages for many
+ * rounds: kvx_cache_set_recency_tiers.
  *
  * Host tier (optional; the paper's future work, Section 6: idle state spilled to
  * CPU memory and reloaded instead of recomputed).  A tiered cache also manages
@@ -115,6 +117,18 @@ int kvx_cache_create(int64_t num_pages, int32_t page_size, int32_t chunk_tokens,
  */
 int kvx_cache_create_tiered(int64_t num_pages, int64_t host_pages, int32_t page_size, int32_t chunk_tokens,
                             int32_t policy, kvx_cache **out);
+
+/*
+ * Recency tiering for KVX_EVICT_RR (Section 3.2, for stale trajectories when no
+ * completion signal arrives; the paper does not evaluate it).  With
+ * tier_width > 0, each reclamation groups the idle agents holding pages into
+ * tiers by age = (logical clock - the agent's last stamp) / tier_width, where
+ * the clock ticks once per turn start and once per turn end; it visits the
+ * tiers from the oldest to the newest and runs the round robin within each,
+ * moving on once a tier holds nothing evictable.  0 (the default) turns it off.
+ * Errors: EINVAL (NULL cache, tier_width < 0, an LRU cache).
+ */
+int kvx_cache_set_recency_tiers(kvx_cache *cache, int64_t tier_width);
 
 /* Free a cache.  NULL is a no-op. */
 int kvx_cache_destroy(kvx_cache *cache);

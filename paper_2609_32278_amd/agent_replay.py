@@ -102,7 +102,7 @@ class ReplayResult:
 
 def replay(tr: wl.AgentTrace, policy: str, num_pages: int, *, chunk_tokens: int = 1024, decode_ticks: int = 2,
            completion_signals: bool = True, gpu: bool = True, on_batch=None, max_ticks: int = 1_000_000,
-           host_pages: int = 0, layer_gemms: tuple | None = None) -> ReplayResult:
+           host_pages: int = 0, layer_gemms: tuple | None = None, tier_width: int = 0) -> ReplayResult:
     """Run the trace; `on_batch(requests, q, out)` sees each GPU batch (requests:
     list of TurnRecord, q / out: the batch's [rows, Hq, d] tensors).  With
     `layer_gemms` = (hidden, ffn), each batch's timed region also runs the
@@ -112,6 +112,8 @@ def replay(tr: wl.AgentTrace, policy: str, num_pages: int, *, chunk_tokens: int 
     res = ReplayResult(policy)
     tiered = host_pages > 0
     cache = kvx.kvx_cache_create_tiered(num_pages, host_pages, wl.PAGE_SIZE, chunk_tokens, POLICIES[policy])
+    if tier_width:
+        kvx.kvx_cache_set_recency_tiers(cache, tier_width)
     pool = None
     torch = None
     host = None
@@ -321,6 +323,8 @@ def main(argv=None) -> int:
                     help="host tier size as a multiple of the device pool (0: no host tier)")
     ap.add_argument("--layer-gemms", default="",
                     help="hidden,ffn: time each batch with one layer's projection + MLP GEMMs (e.g. 4096,14336)")
+    ap.add_argument("--no-completion", action="store_true", help="agents send no completion signal")
+    ap.add_argument("--tiers", type=int, default=0, help="recency tier width for rr (logical clock ticks; 0: off)")
     ap.add_argument("--no-gpu", action="store_true")
     args = ap.parse_args(argv)
     lg = tuple(int(x) for x in args.layer_gemms.split(",")) if args.layer_gemms else None
@@ -331,10 +335,12 @@ def main(argv=None) -> int:
     for pol in (["lru", "rr"] if args.policy == "both" else [args.policy]):
         host_pages = int(args.host_pages * num_pages)
         r = replay(tr, pol, num_pages, chunk_tokens=args.chunk_tokens, decode_ticks=args.decode_ticks,
-                   gpu=not args.no_gpu, host_pages=host_pages, layer_gemms=lg)
+                   gpu=not args.no_gpu, host_pages=host_pages, layer_gemms=lg,
+                   completion_signals=not args.no_completion, tier_width=args.tiers if pol == "rr" else 0)
         s = r.summary()
         s.update({"agents": args.agents, "turns_per_agent": args.turns, "num_pages": num_pages, "host_pages": host_pages,
                   "layer_gemms": list(lg) if lg else None,
+                  "completion_signals": not args.no_completion, "tiers": args.tiers if pol == "rr" else 0,
                   "context_tokens_total": total, "heads": [hq, hkv, d], "chunk_tokens": args.chunk_tokens})
         print(json.dumps(s), flush=True)
     return 0

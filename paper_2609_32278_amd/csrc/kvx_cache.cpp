@@ -50,6 +50,7 @@ struct kvx_cache {
   int64_t rr_last = 0;  // agent that lost the last RR chunk
   int64_t evicted_pages = 0;
   int64_t evictions = 0;
+  int64_t tier_width = 0;  // recency tiers of the round robin (0: off)
   // host tier
   int64_t host_pages = 0;
   std::vector<int32_t> host_free;     // stack of free records
@@ -211,14 +212,16 @@ int64_t evict_lru(kvx_cache* c, int64_t need) {
 
 // Algorithm 1: one queue of idle agents with evictable pages, in id order starting
 // after the agent that lost the previous chunk; one tail chunk per visit.
-int64_t evict_rr(kvx_cache* c, int64_t need) {
+// Algorithm 1 over the idle agents `ids` (ascending id order): one queue starting
+// after the agent that lost the previous chunk, one tail chunk per visit, until
+// `need` pages are freed in total or the queue is empty.
+int64_t round_robin(kvx_cache* c, const std::vector<int64_t>& ids, int64_t need, int64_t freed) {
   std::deque<int64_t> q;
-  auto start = c->rr_has_last ? c->agents.upper_bound(c->rr_last) : c->agents.begin();
-  for (auto it = start; it != c->agents.end(); ++it)
-    if (!it->second.active && it->second.pages > 0) q.push_back(it->first);
-  for (auto it = c->agents.begin(); it != start; ++it)
-    if (!it->second.active && it->second.pages > 0) q.push_back(it->first);
-  int64_t freed = 0;
+  const size_t start = c->rr_has_last
+                           ? (size_t)(std::upper_bound(ids.begin(), ids.end(), c->rr_last) - ids.begin())
+                           : 0;
+  for (size_t i = start; i < ids.size(); i++) q.push_back(ids[i]);
+  for (size_t i = 0; i < start; i++) q.push_back(ids[i]);
   while (freed < need && !q.empty()) {
     const int64_t id = q.front();
     q.pop_front();
@@ -238,6 +241,21 @@ int64_t evict_rr(kvx_cache* c, int64_t need) {
     c->rr_last = id;
     if (a.pages > 0) q.push_back(id);
   }
+  return freed;
+}
+
+// Round-robin reclamation; with recency tiers, tier by tier from the oldest
+// (age = clock - stamp, tier = age / tier_width), round robin within each.
+int64_t evict_rr(kvx_cache* c, int64_t need) {
+  std::map<int64_t, std::vector<int64_t>> tiers;  // tier -> idle agents holding pages, id order
+  for (const auto& kv : c->agents) {
+    const CacheAgent& a = kv.second;
+    if (a.active || a.pages == 0) continue;
+    const int64_t tier = c->tier_width > 0 ? (c->clock - a.stamp) / c->tier_width : 0;
+    tiers[tier].push_back(kv.first);
+  }
+  int64_t freed = 0;
+  for (auto t = tiers.rbegin(); t != tiers.rend() && freed < need; ++t) freed = round_robin(c, t->second, need, freed);
   return freed;
 }
 
@@ -287,6 +305,14 @@ int kvx_cache_create_tiered(int64_t num_pages, int64_t host_pages, int32_t page_
   c->chunk_pages = chunk_tokens / page_size;
   c->policy = policy;
   *out = c;
+  return KVX_OK;
+}
+
+int kvx_cache_set_recency_tiers(kvx_cache* c, int64_t tier_width) {
+  if (c == nullptr) return report(KVX_EINVAL, "cache is NULL");
+  if (tier_width < 0) return report(KVX_EINVAL, "tier_width = %lld must be >= 0", (long long)tier_width);
+  if (c->policy != KVX_EVICT_RR) return report(KVX_EINVAL, "recency tiers apply to KVX_EVICT_RR only");
+  c->tier_width = tier_width;
   return KVX_OK;
 }
 

@@ -30,7 +30,7 @@ KVX_ROPE_HALF, KVX_ROPE_INTERLEAVED = 0, 1
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_layout", "kv_pool_write_pages",
            "kv_pool_read_pages", "kv_pool_record_bytes", "kv_pool_spill", "kv_pool_reload", "store_kv", "store_kv_rope", "extend_attention", "extend_attention_plan",
            "kvx_set_split_keys", "kvx_last_error",
-           "kvx_cache_create", "kvx_cache_create_tiered", "kvx_cache_destroy", "kvx_cache_begin_turn",
+           "kvx_cache_create", "kvx_cache_create_tiered", "kvx_cache_set_recency_tiers", "kvx_cache_destroy", "kvx_cache_begin_turn",
            "kvx_cache_begin_turn_tiered", "kvx_cache_end_turn", "kvx_cache_complete", "kvx_cache_agent",
            "kvx_cache_agent_host", "kvx_cache_stats"]
 
@@ -116,6 +116,7 @@ def lib():
             "kvx_set_split_keys": [i32],
             "kvx_cache_create": [i64, i32, i32, i32, ctypes.POINTER(P)],
             "kvx_cache_create_tiered": [i64, i64, i32, i32, i32, ctypes.POINTER(P)],
+            "kvx_cache_set_recency_tiers": [P, i64],
             "kvx_cache_begin_turn_tiered": [P, i64, i32, ctypes.POINTER(i32), P, i64, ctypes.POINTER(kvx_cache_moves)],
             "kvx_cache_agent_host": [P, i64, ctypes.POINTER(i32), P, i64],
             "kvx_cache_destroy": [P],
@@ -305,6 +306,10 @@ def kvx_cache_create_tiered(num_pages: int, host_pages: int, page_size: int = 16
     _check(lib().kvx_cache_create_tiered(int(num_pages), int(host_pages), page_size, chunk_tokens, policy,
                                          ctypes.byref(out)), "kvx_cache_create_tiered")
     return out
+
+
+def kvx_cache_set_recency_tiers(cache, tier_width: int) -> None:
+    _check(lib().kvx_cache_set_recency_tiers(cache, int(tier_width)), "kvx_cache_set_recency_tiers")
 
 
 def kvx_cache_destroy(cache) -> None:

@@ -52,10 +52,12 @@ def test_argument_errors():
 class _Pair:
     """The library cache and the oracle, driven in lockstep."""
 
-    def __init__(self, num_pages, chunk_tokens, policy):
+    def __init__(self, num_pages, chunk_tokens, policy, tier_width=0):
         self.c = kvx.kvx_cache_create(num_pages, PAGE, chunk_tokens, policy)
+        if tier_width:
+            kvx.kvx_cache_set_recency_tiers(self.c, tier_width)
         self.o = OracleCache(num_pages, PAGE, chunk_tokens, OracleCache.RR if policy == kvx.KVX_EVICT_RR
-                             else OracleCache.LRU)
+                             else OracleCache.LRU, tier_width=tier_width)
         self.num_pages = num_pages
         self.tables = {}  # active agent -> page table of its running turn
 
@@ -111,9 +113,9 @@ class _Pair:
         assert len(owned) + st["free_pages"] == self.num_pages
 
 
-def _trace(seed, policy, n_agents, num_pages, chunk_tokens, steps):
+def _trace(seed, policy, n_agents, num_pages, chunk_tokens, steps, tier_width=0, complete_prob=0.05):
     rng = np.random.default_rng(seed)
-    pair = _Pair(num_pages, chunk_tokens, policy)
+    pair = _Pair(num_pages, chunk_tokens, policy, tier_width)
     ctx = {}
     active = set()
     try:
@@ -125,7 +127,7 @@ def _trace(seed, policy, n_agents, num_pages, chunk_tokens, steps):
                     pair.end(a)
                     active.discard(a)
                     ctx[a] += int(rng.integers(0, 300))  # the model's reply joins the context
-            elif a in ctx and r < 0.05:
+            elif a in ctx and r < complete_prob:
                 pair.complete(a)
                 del ctx[a]
             else:
@@ -136,6 +138,28 @@ def _trace(seed, policy, n_agents, num_pages, chunk_tokens, steps):
             pair.check()
     finally:
         pair.close()
+
+
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("tier_width", [1, 7, 60])
+def test_recency_tiers_match_the_oracle(seed, tier_width):
+    """Round robin with recency tiers and no completion signals (the case tiers exist for)."""
+    _trace(seed, kvx.KVX_EVICT_RR, n_agents=16, num_pages=400, chunk_tokens=32, steps=800,
+           tier_width=tier_width, complete_prob=0.0)
+
+
+def test_recency_tier_errors():
+    c = kvx.kvx_cache_create(64, 16, 64, kvx.KVX_EVICT_LRU)
+    try:
+        assert _err(kvx.kvx_cache_set_recency_tiers, c, 4) == kvx.KVX_EINVAL  # LRU
+    finally:
+        kvx.kvx_cache_destroy(c)
+    c = kvx.kvx_cache_create(64, 16, 64, kvx.KVX_EVICT_RR)
+    try:
+        assert _err(kvx.kvx_cache_set_recency_tiers, c, -1) == kvx.KVX_EINVAL
+        kvx.kvx_cache_set_recency_tiers(c, 0)
+    finally:
+        kvx.kvx_cache_destroy(c)
 
 
 @pytest.mark.parametrize("seed", range(6))
