@@ -62,6 +62,26 @@ the paper describes it and does not evaluate it), when ``tier_width`` > 0:
     newest and runs Algorithm 1's round robin within each (queue in agent-id
     order after the agent that lost the last chunk), moving to the next tier
     once the current one holds nothing evictable.
+
+Shared prefixes (Section 2: agents typically share a short common prefix, such
+as a system prompt, in the serving system's radix tree; Section 3.1: eviction
+starts at idle leaves and exposes parents):
+
+11. An agent may join a group before it holds any pages; the group's shared
+    prefix is its first S whole pages, the same for every member.  The group
+    node is all or nothing: present (S pages, one copy, read by every member's
+    page table) or absent.  A member's history is the group's pages, then its
+    private pages, then its host pages; a member of an absent group holds no
+    private pages.
+12. A member's turn end creates the absent group node from the turn's own
+    pages of the shared span (the turn computed them: nothing was reused);
+    if the node appeared meanwhile, the turn's copies of the span are freed.
+    Private pages are kept only while the group node is present.
+13. The group node is a leaf -- evictable -- only while no member is inside a
+    turn and no member holds private or host pages; it is then evicted whole and
+    never spilled.  Its stamp is the last turn start or end of any member.  LRU
+    weighs it among the other leaves by that stamp; round robin visits it after
+    the agents' queue (it is the parent of every member's path), oldest first.
 """
 
 from __future__ import annotations
@@ -73,10 +93,20 @@ class NoMemory(Exception):
     """Active demand exceeds the capacity even after evicting every idle page."""
 
 
+class _Group:
+    def __init__(self, shared_pages: int) -> None:
+        self.S = shared_pages
+        self.present = False
+        self.stamp = 0
+        self.members: set[int] = set()
+
+
 class _Agent:
     def __init__(self) -> None:
         self.nodes: list[int] = []  # pages per node, root .. leaf
         self.host: list[int] = []   # host record ids, nearest page first
+        self.group = None           # group id, or None
+        self.turn_start = 0         # logical page of the running turn's first page
         self.active = False
         self.stamp = 0
         self.prompt_len = 0
@@ -109,6 +139,7 @@ class OracleCache:
         self.policy = policy
         self.free = num_pages
         self.agents: dict[int, _Agent] = {}
+        self.groups: dict[int, _Group] = {}
         self.clock = 0
         self.rr_last = None
         self.evicted_pages = 0
@@ -163,6 +194,29 @@ class OracleCache:
             self.spilled_pages += 1
             self.moves_spill += 1
 
+    def join(self, agent_id: int, group: int, shared_tokens: int) -> None:
+        S = shared_tokens // self.page_size
+        assert S >= 1
+        a = self.agents.setdefault(agent_id, _Agent())
+        assert not a.active and a.pages == 0 and not a.host and a.group is None
+        g = self.groups.setdefault(group, _Group(S))
+        assert g.S == S
+        a.group = group
+        g.members.add(agent_id)
+
+    def _group_leaf(self, gid: int) -> bool:
+        g = self.groups[gid]
+        return g.present and all(not self.agents[m].active and self.agents[m].pages == 0 and not self.agents[m].host
+                                 for m in g.members)
+
+    def _evict_group(self, gid: int) -> int:
+        g = self.groups[gid]
+        g.present = False
+        self.free += g.S
+        self.evicted_pages += g.S
+        self.evictions += 1
+        return g.S
+
     def _evictable(self, agent_id: int) -> bool:
         a = self.agents.get(agent_id)
         return a is not None and not a.active and a.pages > 0
@@ -180,6 +234,10 @@ class OracleCache:
         freed = 0
         for group in groups:
             freed = self._round_robin(group, M, freed)
+            if freed >= M:
+                return
+        for _, gid in sorted((g.stamp, gid) for gid, g in self.groups.items() if self._group_leaf(gid)):
+            freed += self._evict_group(gid)
             if freed >= M:
                 return
 
@@ -210,9 +268,13 @@ class OracleCache:
         freed = 0
         while freed < M:
             leaves = [(self.agents[i].stamp, i) for i in self.agents if self._evictable(i)]
+            leaves += [(g.stamp, ("group", gid)) for gid, g in self.groups.items() if self._group_leaf(gid)]
             if not leaves:
                 return
-            _, victim = min(leaves)
+            _, victim = min(leaves, key=lambda x: x[0])
+            if isinstance(victim, tuple):
+                freed += self._evict_group(victim[1])
+                continue
             a = self.agents[victim]
             n = a.nodes[-1]
             self._evict(victim, a, n)
@@ -227,22 +289,36 @@ class OracleCache:
         assert not a.active
         self.clock += 1
         a.stamp = self.clock
+        g = self.groups.get(a.group) if a.group is not None else None
+        if g is not None:
+            g.stamp = self.clock
         self.moves_spill = 0
         self.call_spills: set[int] = set()
         self.last_moves = (0, 0)
         limit = (prompt_len - 1) // self.page_size
-        reuse = min(a.pages + len(a.host), limit)
-        if reuse < a.pages:  # past the limit: host pages go first, then device pages
+        gp = g.S if g is not None and g.present else 0  # group pages on the agent's path
+        reuse = min(gp + a.pages + len(a.host), limit)
+        if reuse < gp:  # the prompt ends inside the shared span
+            used_group = reuse
             for rec in a.host:
                 self._forget(rec)
             a.host = []
-            self._drop_tail(a, a.pages - reuse)
+            self._drop_tail(a, a.pages)
         else:
-            for rec in a.host[reuse - a.pages:]:
-                self._forget(rec)
-            a.host = a.host[: reuse - a.pages]
+            used_group = gp
+            r2 = reuse - gp
+            if r2 < a.pages:  # past the limit: host pages go first, then device pages
+                for rec in a.host:
+                    self._forget(rec)
+                a.host = []
+                self._drop_tail(a, a.pages - r2)
+            else:
+                for rec in a.host[r2 - a.pages:]:
+                    self._forget(rec)
+                a.host = a.host[: r2 - a.pages]
         reload = len(a.host)
-        need = -(-prompt_len // self.page_size) - a.pages  # reloaded pages + new pages
+        a.turn_start = used_group + a.pages
+        need = -(-prompt_len // self.page_size) - a.turn_start  # reloaded pages + new pages
         a.active = True
         if self.free < need:
             if self.policy == self.RR:
@@ -266,14 +342,29 @@ class OracleCache:
     def end_turn(self, agent_id: int) -> None:
         a = self.agents[agent_id]
         assert a.active
-        whole = a.prompt_len // self.page_size - a.pages
-        self.free += a.turn_pages - whole
-        if whole > 0:
-            a.nodes.append(whole)
+        g = self.groups.get(a.group) if a.group is not None else None
+        whole = a.prompt_len // self.page_size
+        kept = 0       # turn pages that stay: the new private node, or the new group node
+        new_node = 0
+        if g is None:
+            new_node = whole - a.pages
+        else:
+            if not g.present and whole >= g.S:
+                assert a.turn_start == 0
+                g.present = True   # this turn's pages of the shared span become the group node
+                kept += g.S
+            if g.present:
+                new_node = max(0, whole - max(g.S, a.turn_start))
+        kept += new_node
+        self.free += a.turn_pages - kept
+        if new_node > 0:
+            a.nodes.append(new_node)
         a.turn_pages = 0
         a.active = False
         self.clock += 1
         a.stamp = self.clock
+        if g is not None:
+            g.stamp = self.clock
 
     def complete(self, agent_id: int) -> None:
         a = self.agents[agent_id]
@@ -281,6 +372,8 @@ class OracleCache:
         self._drop_tail(a, a.pages)
         for rec in a.host:
             self._forget(rec)
+        if a.group is not None:
+            self.groups[a.group].members.discard(agent_id)
         del self.agents[agent_id]
 
     def cached_tokens(self, agent_id: int) -> int:
@@ -290,6 +383,10 @@ class OracleCache:
     def host_tokens(self, agent_id: int) -> int:
         a = self.agents.get(agent_id)
         return 0 if a is None else len(a.host) * self.page_size
+
+    def group_tokens(self, gid: int) -> int:
+        g = self.groups.get(gid)
+        return 0 if g is None or not g.present else g.S * self.page_size
 
     @property
     def host_used(self) -> int:

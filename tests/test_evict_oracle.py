@@ -348,3 +348,77 @@ def test_tiers_evict_stale_agents_first():
         return [c.cached_tokens(a) // PAGE for a in (1, 2, 3, 4)]
     assert run(8) == [5, 5, 8, 8]
     assert sorted(run(0)) != [5, 5, 8, 8] and sum(run(0)) == 26
+
+
+# ------------------------------------------------------------------ shared prefixes
+
+def _join_fill(c, agent, group, S, private):
+    """A member whose first turn leaves S shared + `private` private pages cached."""
+    c.join(agent, group, S * PAGE)
+    c.begin_turn(agent, (S + private) * PAGE + 1)
+    c.end_turn(agent)
+
+
+def test_a_shared_prefix_is_stored_once():
+    c = OracleCache(64, PAGE, PAGE, OracleCache.RR)
+    _join_fill(c, 1, 7, 4, 3)           # creates the group node (4 pages) + 3 private
+    assert c.group_tokens(7) == 4 * PAGE and c.cached_tokens(1) == 3 * PAGE
+    used = 64 - c.free
+    _join_fill(c, 2, 7, 4, 5)           # reuses the 4 shared pages, computes 5 private
+    assert 64 - c.free == used + 5
+    assert c.begin_turn(2, 9 * PAGE + 1) == 9 * PAGE   # shared + private reused
+    c.end_turn(2)
+
+
+def test_concurrent_first_turns_keep_one_copy():
+    c = OracleCache(64, PAGE, PAGE, OracleCache.RR)
+    for a in (1, 2):
+        c.join(a, 0, 3 * PAGE)
+    assert c.begin_turn(1, 5 * PAGE + 1) == 0
+    assert c.begin_turn(2, 6 * PAGE + 1) == 0   # both compute the shared span
+    assert c.free == 64 - 6 - 7
+    c.end_turn(1)                               # creates the node from agent 1's pages
+    c.end_turn(2)                               # agent 2's copies of the span are freed
+    assert c.group_tokens(0) == 3 * PAGE
+    assert (c.cached_tokens(1), c.cached_tokens(2)) == (2 * PAGE, 3 * PAGE)
+    assert c.free == 64 - 3 - 2 - 3
+
+
+@pytest.mark.parametrize("n,na,m", REGIME)
+def test_round_robin_closed_form_holds_for_private_histories(n, na, m):
+    """Equation 2 with a shared system prompt: the idle agents' private prefixes of
+    u pages each keep h = (m - na) / ns of their pages; the shared node (one copy)
+    is never touched while any member holds private pages."""
+    ns = n - na
+    u = 8 * ns
+    S = 5
+    c = OracleCache(m * u + S, PAGE, PAGE, OracleCache.RR)
+    for i in range(ns):
+        _join_fill(c, i, 0, S, u)
+    for j in range(na):
+        c.begin_turn(1000 + j, u * PAGE)
+    kept = [c.cached_tokens(i) / (u * PAGE) for i in range(ns)]
+    h = (m - na) / ns
+    assert all(abs(k - h) < 1e-12 for k in kept), kept
+    assert c.group_tokens(0) == S * PAGE
+
+
+@pytest.mark.parametrize("policy", [OracleCache.RR, OracleCache.LRU])
+def test_the_shared_node_goes_only_as_a_whole_leaf(policy):
+    c = OracleCache(20, PAGE, PAGE, policy)
+    _join_fill(c, 1, 0, 4, 3)
+    _join_fill(c, 2, 0, 4, 2)
+    assert c.free == 20 - 4 - 3 - 2
+    c.begin_turn(9, (c.free + 5) * PAGE)        # needs all 5 private pages, not the node
+    assert (c.cached_tokens(1), c.cached_tokens(2), c.group_tokens(0)) == (0, 0, 4 * PAGE)
+    c.end_turn(9)
+    c.complete(9)
+    free = c.free
+    c.begin_turn(8, (free + 2) * PAGE)          # now the node is a leaf: evicted whole
+    assert c.group_tokens(0) == 0 and c.free == 4 - 2
+    # members of an absent group reuse nothing; their next turn recreates the node
+    c.end_turn(8)
+    c.complete(8)
+    assert c.begin_turn(1, 6 * PAGE + 1) == 0
+    c.end_turn(1)
+    assert c.group_tokens(0) == 4 * PAGE and c.cached_tokens(1) == 2 * PAGE
