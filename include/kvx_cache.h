@@ -43,6 +43,20 @@
  * reloaded into freshly allocated device pages and their records freed, so an
  * agent inside a turn holds no host pages.
  *
+ * Shared prefixes (Section 2: agents typically share a short common prefix such
+ * as a system prompt, kept in the radix tree; eviction starts at idle leaves and
+ * exposes parents, Section 3.1).  Agents that join a group share its first S
+ * whole pages: one node, present or absent as a whole, that every member's page
+ * table reads.  A member's history is the group node, then its private pages,
+ * then its host pages; a member holds private pages only while the node is
+ * present.  The first member turn that computes the span creates the node from
+ * its own pages; copies computed concurrently by other members are freed at their
+ * turn end.  The node is a leaf -- evictable, whole, never spilled -- only while
+ * no member is inside a turn and no member holds private or host pages.  Its
+ * stamp is the last turn start or end of any member: LRU weighs it among the
+ * leaves by that stamp; round robin reclaims it after the agents' queue, oldest
+ * first.
+ *
  * Conventions: every call is synchronous host code, returns KVX_OK or a
  * kvx_status code from kvx.h (kvx_last_error() describes the failure), and is not
  * thread-safe for one cache (callers serialize calls on a cache).  Page ids are
@@ -81,6 +95,7 @@ typedef struct {
     int64_t spilled_pages;  /* pages spilled since creation */
     int64_t reloaded_pages; /* pages reloaded since creation */
     int64_t host_dropped_pages; /* records dropped to make room since creation */
+    int64_t group_pages;    /* pages of present shared-prefix group nodes */
 } kvx_cache_counters;
 
 /* Page moves a tiered turn start asks for, to run on the pool in this order
@@ -178,7 +193,8 @@ int kvx_cache_end_turn(kvx_cache *cache, int64_t agent);
 int kvx_cache_complete(kvx_cache *cache, int64_t agent);
 
 /*
- * Cached history of `agent` in tokens (0 for an unknown agent) and, if `page_ids`
+ * Private cached history of `agent` in tokens (0 for an unknown agent; a group's
+ * shared pages are not counted, see kvx_cache_group) and, if `page_ids`
  * is non-NULL, its pages in logical order (at most `cap` written).  For tests and
  * tools.  Errors: EINVAL.
  */
@@ -192,6 +208,24 @@ int kvx_cache_agent(const kvx_cache *cache, int64_t agent, int32_t *cached_token
  */
 int kvx_cache_agent_host(const kvx_cache *cache, int64_t agent, int32_t *host_tokens, int32_t *slots,
                          int64_t cap);
+
+/*
+ * Make `agent` a member of `group` (any id), whose shared prefix is the first
+ * `shared_tokens` tokens of every member's context, rounded down to whole pages.
+ * The agent must be idle, hold no pages and belong to no group (a new agent);
+ * every member of a group gives the same number of whole pages.
+ * Errors: EINVAL (NULL cache, shared_tokens below one page, agent state,
+ * a different span for an existing group).
+ */
+int kvx_cache_join(kvx_cache *cache, int64_t agent, int64_t group, int32_t shared_tokens);
+
+/*
+ * Shared pages of `group` in tokens (0 while its node is absent or the group is
+ * unknown) and, if `page_ids` is non-NULL, the node's pages (at most `cap`).
+ * For tests and tools.  Errors: EINVAL.
+ */
+int kvx_cache_group(const kvx_cache *cache, int64_t group, int32_t *shared_tokens, int32_t *page_ids,
+                    int64_t cap);
 
 /* Counters of the cache.  Errors: EINVAL. */
 int kvx_cache_stats(const kvx_cache *cache, kvx_cache_counters *out);

@@ -114,6 +114,9 @@ def replay(tr: wl.AgentTrace, policy: str, num_pages: int, *, chunk_tokens: int 
     cache = kvx.kvx_cache_create_tiered(num_pages, host_pages, wl.PAGE_SIZE, chunk_tokens, POLICIES[policy])
     if tier_width:
         kvx.kvx_cache_set_recency_tiers(cache, tier_width)
+    if tr.shared >= wl.PAGE_SIZE:  # every agent shares the common system prompt's pages
+        for a in range(tr.num_agents):
+            kvx.kvx_cache_join(cache, a, 0, tr.shared)
     pool = None
     torch = None
     host = None
@@ -324,12 +327,14 @@ def main(argv=None) -> int:
     ap.add_argument("--layer-gemms", default="",
                     help="hidden,ffn: time each batch with one layer's projection + MLP GEMMs (e.g. 4096,14336)")
     ap.add_argument("--no-completion", action="store_true", help="agents send no completion signal")
+    ap.add_argument("--shared", type=int, default=0, help="tokens of a system prompt every agent shares")
     ap.add_argument("--tiers", type=int, default=0, help="recency tier width for rr (logical clock ticks; 0: off)")
     ap.add_argument("--no-gpu", action="store_true")
     args = ap.parse_args(argv)
     lg = tuple(int(x) for x in args.layer_gemms.split(",")) if args.layer_gemms else None
     hq, hkv, d = (int(x) for x in args.heads.split(","))
-    tr = wl.make_agent_trace(args.agents, args.turns, seed=args.seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d)
+    tr = wl.make_agent_trace(args.agents, args.turns, seed=args.seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                             shared=args.shared)
     total = sum(tr.max_context(i) for i in range(tr.num_agents))
     num_pages = int(args.capacity * total) // wl.PAGE_SIZE
     for pol in (["lru", "rr"] if args.policy == "both" else [args.policy]):
@@ -340,7 +345,7 @@ def main(argv=None) -> int:
         s = r.summary()
         s.update({"agents": args.agents, "turns_per_agent": args.turns, "num_pages": num_pages, "host_pages": host_pages,
                   "layer_gemms": list(lg) if lg else None,
-                  "completion_signals": not args.no_completion, "tiers": args.tiers if pol == "rr" else 0,
+                  "completion_signals": not args.no_completion, "shared": args.shared, "tiers": args.tiers if pol == "rr" else 0,
                   "context_tokens_total": total, "heads": [hq, hkv, d], "chunk_tokens": args.chunk_tokens})
         print(json.dumps(s), flush=True)
     return 0

@@ -29,6 +29,19 @@ struct CacheAgent {
   int32_t prompt_len = 0;        // running turn
   std::vector<int32_t> turn;     // pages allocated to the running turn
   std::deque<int32_t> host;      // host records continuing the device pages, nearest first
+  bool in_group = false;
+  int64_t group = 0;
+  int64_t turn_start = 0;        // logical page of the running turn's first page
+};
+
+// A shared prefix (system prompt) of a group of agents: one node of S whole
+// pages, present or absent as a whole, read by every member's page table.
+struct CacheGroup {
+  int64_t S = 0;
+  bool present = false;
+  std::vector<int32_t> pages;
+  int64_t stamp = 0;
+  std::vector<int64_t> members;
 };
 
 struct FifoEntry {
@@ -45,6 +58,8 @@ struct kvx_cache {
   int32_t policy = 0;
   std::vector<int32_t> free_pages;       // stack; the next page handed out is at the back
   std::map<int64_t, CacheAgent> agents;  // ordered by id: the round-robin order
+  std::map<int64_t, CacheGroup> groups;
+  int64_t group_pages = 0;               // pages of present group nodes
   int64_t clock = 0;
   bool rr_has_last = false;
   int64_t rr_last = 0;  // agent that lost the last RR chunk
@@ -102,6 +117,29 @@ void drop_host(kvx_cache* c, CacheAgent& a, size_t keep) {
     free_record(c, a.host.back());
     a.host.pop_back();
   }
+}
+
+// A group node is a leaf while no member is inside a turn and no member holds
+// private or host pages.
+bool group_leaf(const kvx_cache* c, const CacheGroup& g) {
+  if (!g.present) return false;
+  for (int64_t m : g.members) {
+    const CacheAgent& a = c->agents.find(m)->second;
+    if (a.active || a.pages > 0 || !a.host.empty()) return false;
+  }
+  return true;
+}
+
+// Evict a group node whole (never spilled).
+int64_t evict_group(kvx_cache* c, CacheGroup& g) {
+  const int64_t n = (int64_t)g.pages.size();
+  release_pages(c, g.pages.data(), g.pages.size());
+  g.pages.clear();
+  g.present = false;
+  c->group_pages -= n;
+  c->evicted_pages += n;
+  c->evictions++;
+  return n;
 }
 
 // A record for a spill of `owner`'s page: a free one, else the oldest live record
@@ -200,6 +238,15 @@ int64_t evict_lru(kvx_cache* c, int64_t need) {
         best_id = kv.first;
       }
     }
+    CacheGroup* leaf = nullptr;  // a group node older than every agent leaf goes first
+    for (auto& kv : c->groups)
+      if (group_leaf(c, kv.second) && (leaf == nullptr || kv.second.stamp < leaf->stamp) &&
+          (best == nullptr || kv.second.stamp < best->stamp))
+        leaf = &kv.second;
+    if (leaf != nullptr) {
+      freed += evict_group(c, *leaf);
+      continue;
+    }
     if (best == nullptr) break;
     const int64_t n = (int64_t)best->nodes.back().pages.size();
     evict_tail(c, best_id, *best, n);
@@ -256,6 +303,16 @@ int64_t evict_rr(kvx_cache* c, int64_t need) {
   }
   int64_t freed = 0;
   for (auto t = tiers.rbegin(); t != tiers.rend() && freed < need; ++t) freed = round_robin(c, t->second, need, freed);
+  if (freed < need) {  // group nodes, parents of every member's path, oldest first
+    std::vector<std::pair<int64_t, int64_t>> leaves;  // (stamp, group)
+    for (auto& kv : c->groups)
+      if (group_leaf(c, kv.second)) leaves.emplace_back(kv.second.stamp, kv.first);
+    std::sort(leaves.begin(), leaves.end());
+    for (const auto& l : leaves) {
+      if (freed >= need) break;
+      freed += evict_group(c, c->groups[l.second]);
+    }
+  }
   return freed;
 }
 
@@ -343,17 +400,27 @@ static int begin_turn(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_t* 
   c->call++;
   CacheAgent& a = c->agents[agent];
   a.stamp = ++c->clock;  // matching the prefix touches every node of the path
-  // reuse device pages, then host pages, up to the last whole page before the final token
+  CacheGroup* g = a.in_group ? &c->groups[a.group] : nullptr;
+  if (g != nullptr) g->stamp = a.stamp;
+  // reuse the group's shared pages, then device pages, then host pages, up to the
+  // last whole page before the final token
   const int64_t limit = (prompt_len - 1) / S;
-  const int64_t reuse_pages = std::min<int64_t>(a.pages + (int64_t)a.host.size(), limit);
-  if (reuse_pages < a.pages) {
+  const int64_t gp = (g != nullptr && g->present) ? g->S : 0;
+  const int64_t reuse_pages = std::min<int64_t>(gp + a.pages + (int64_t)a.host.size(), limit);
+  int64_t used_group = gp;
+  if (reuse_pages < gp) {  // the prompt ends inside the shared span
+    used_group = reuse_pages;
     drop_host(c, a, 0);
-    drop_tail(c, a, a.pages - reuse_pages);
+    drop_tail(c, a, a.pages);
+  } else if (reuse_pages - gp < a.pages) {
+    drop_host(c, a, 0);
+    drop_tail(c, a, a.pages - (reuse_pages - gp));
   } else {
-    drop_host(c, a, (size_t)(reuse_pages - a.pages));
+    drop_host(c, a, (size_t)(reuse_pages - gp - a.pages));
   }
   const int64_t reload = (int64_t)a.host.size();
-  const int64_t need = n_total - a.pages;  // reloaded pages + the suffix's pages
+  a.turn_start = used_group + a.pages;
+  const int64_t need = n_total - a.turn_start;  // reloaded pages + the suffix's pages
   a.active = true;  // pinned (with its host records) while this turn allocates
   if ((int64_t)c->free_pages.size() < need) {
     const int64_t want = need - (int64_t)c->free_pages.size();
@@ -398,6 +465,7 @@ static int begin_turn(kvx_cache* c, int64_t agent, int32_t prompt_len, int32_t* 
   c->reloaded += reload;
   a.prompt_len = prompt_len;
   int64_t j = 0;
+  for (int64_t i = 0; i < used_group; i++) page_ids[j++] = g->pages[(size_t)i];
   for (const CacheNode& nd : a.nodes)
     for (int32_t pg : nd.pages) page_ids[j++] = pg;
   for (int32_t pg : a.turn) page_ids[j++] = pg;
@@ -424,11 +492,30 @@ int kvx_cache_end_turn(kvx_cache* c, int64_t agent) {
   if (it == c->agents.end() || !it->second.active)
     return report(KVX_EINVAL, "agent %lld is not inside a turn", (long long)agent);
   CacheAgent& a = it->second;
-  // whole pages of the prompt stay cached; a partial last page is freed
-  const int64_t full = a.prompt_len / c->page_size - a.pages;  // whole pages added by this turn
+  // whole pages of the prompt stay cached; a partial last page is freed.  The turn
+  // holds logical pages [turn_start, turn_start + turn.size()).
+  const int64_t whole = a.prompt_len / c->page_size;
+  int64_t keep_from = 0, keep_to = std::max<int64_t>(0, whole - a.turn_start);  // turn indices of the new node
+  if (a.in_group) {
+    CacheGroup& g = c->groups[a.group];
+    int64_t donated = 0;
+    if (!g.present && whole >= g.S) {  // the turn computed the shared span: it becomes the group node
+      g.pages.assign(a.turn.begin(), a.turn.begin() + g.S);
+      g.present = true;
+      c->group_pages += g.S;
+      donated = g.S;
+    }
+    if (g.present) {
+      keep_from = std::max<int64_t>(g.S, a.turn_start) - a.turn_start;  // copies of the span are freed
+      if (keep_from > keep_to) keep_from = keep_to;
+    } else {
+      keep_from = keep_to = 0;  // no private pages without the group node
+    }
+    if (keep_from > donated) release_pages(c, a.turn.data() + donated, (size_t)(keep_from - donated));
+  }
   CacheNode nd;
-  nd.pages.assign(a.turn.begin(), a.turn.begin() + full);
-  if ((size_t)full < a.turn.size()) release_pages(c, a.turn.data() + full, a.turn.size() - (size_t)full);
+  nd.pages.assign(a.turn.begin() + keep_from, a.turn.begin() + keep_to);
+  if ((size_t)keep_to < a.turn.size()) release_pages(c, a.turn.data() + keep_to, a.turn.size() - (size_t)keep_to);
   if (!nd.pages.empty()) {
     a.pages += (int64_t)nd.pages.size();
     a.nodes.push_back(std::move(nd));
@@ -436,6 +523,7 @@ int kvx_cache_end_turn(kvx_cache* c, int64_t agent) {
   a.turn.clear();
   a.active = false;
   a.stamp = ++c->clock;  // inserting the turn's pages touches the whole path
+  if (a.in_group) c->groups[a.group].stamp = a.stamp;
   return KVX_OK;
 }
 
@@ -446,6 +534,10 @@ int kvx_cache_complete(kvx_cache* c, int64_t agent) {
   if (it->second.active) return report(KVX_EINVAL, "agent %lld is inside a turn", (long long)agent);
   drop_tail(c, it->second, it->second.pages);
   drop_host(c, it->second, 0);
+  if (it->second.in_group) {
+    auto& m = c->groups[it->second.group].members;
+    m.erase(std::find(m.begin(), m.end(), agent));
+  }
   c->agents.erase(it);
   return KVX_OK;
 }
@@ -464,6 +556,43 @@ int kvx_cache_agent(const kvx_cache* c, int64_t agent, int32_t* cached_tokens, i
       for (int32_t pg : nd.pages)
         if (j < cap) page_ids[j++] = pg;
   }
+  return KVX_OK;
+}
+
+int kvx_cache_join(kvx_cache* c, int64_t agent, int64_t group, int32_t shared_tokens) {
+  if (c == nullptr) return report(KVX_EINVAL, "cache is NULL");
+  if (shared_tokens < c->page_size)
+    return report(KVX_EINVAL, "shared_tokens = %d must cover at least one page", shared_tokens);
+  const int64_t S = shared_tokens / c->page_size;
+  auto ai = c->agents.find(agent);
+  if (ai != c->agents.end()) {
+    const CacheAgent& a = ai->second;
+    if (a.active || a.pages > 0 || !a.host.empty() || a.in_group)
+      return report(KVX_EINVAL, "agent %lld must be idle, hold no pages and belong to no group", (long long)agent);
+  }
+  auto gi = c->groups.find(group);
+  if (gi != c->groups.end() && gi->second.S != S)
+    return report(KVX_EINVAL, "group %lld shares %lld pages, not %lld", (long long)group, (long long)gi->second.S,
+                  (long long)S);
+  CacheGroup& g = c->groups[group];
+  g.S = S;
+  g.members.push_back(agent);
+  CacheAgent& a = c->agents[agent];
+  a.in_group = true;
+  a.group = group;
+  return KVX_OK;
+}
+
+int kvx_cache_group(const kvx_cache* c, int64_t group, int32_t* shared_tokens, int32_t* page_ids, int64_t cap) {
+  if (c == nullptr || shared_tokens == nullptr) return report(KVX_EINVAL, "cache and shared_tokens must be non-NULL");
+  auto it = c->groups.find(group);
+  if (it == c->groups.end() || !it->second.present) {
+    *shared_tokens = 0;
+    return KVX_OK;
+  }
+  *shared_tokens = (int32_t)(it->second.S * c->page_size);
+  if (page_ids != nullptr)
+    for (int64_t j = 0; j < cap && j < (int64_t)it->second.pages.size(); j++) page_ids[j] = it->second.pages[(size_t)j];
   return KVX_OK;
 }
 
@@ -501,6 +630,7 @@ int kvx_cache_stats(const kvx_cache* c, kvx_cache_counters* out) {
   s.spilled_pages = c->spilled;
   s.reloaded_pages = c->reloaded;
   s.host_dropped_pages = c->host_dropped;
+  s.group_pages = c->group_pages;
   *out = s;
   return KVX_OK;
 }

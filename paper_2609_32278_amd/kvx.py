@@ -32,7 +32,7 @@ EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_layout", "kv_pool_write
            "kvx_set_split_keys", "kvx_last_error",
            "kvx_cache_create", "kvx_cache_create_tiered", "kvx_cache_set_recency_tiers", "kvx_cache_destroy", "kvx_cache_begin_turn",
            "kvx_cache_begin_turn_tiered", "kvx_cache_end_turn", "kvx_cache_complete", "kvx_cache_agent",
-           "kvx_cache_agent_host", "kvx_cache_stats"]
+           "kvx_cache_agent_host", "kvx_cache_join", "kvx_cache_group", "kvx_cache_stats"]
 
 
 class KvxNotBuilt(ImportError):
@@ -81,7 +81,7 @@ class kvx_cache_stats_t(ctypes.Structure):
                 ("turn_pages", ctypes.c_int64), ("evicted_pages", ctypes.c_int64), ("evictions", ctypes.c_int64),
                 ("agents", ctypes.c_int32), ("active_agents", ctypes.c_int32), ("host_pages", ctypes.c_int64),
                 ("host_used", ctypes.c_int64), ("spilled_pages", ctypes.c_int64), ("reloaded_pages", ctypes.c_int64),
-                ("host_dropped_pages", ctypes.c_int64)]
+                ("host_dropped_pages", ctypes.c_int64), ("group_pages", ctypes.c_int64)]
 
 
 class kvx_cache_moves(ctypes.Structure):
@@ -119,6 +119,8 @@ def lib():
             "kvx_cache_set_recency_tiers": [P, i64],
             "kvx_cache_begin_turn_tiered": [P, i64, i32, ctypes.POINTER(i32), P, i64, ctypes.POINTER(kvx_cache_moves)],
             "kvx_cache_agent_host": [P, i64, ctypes.POINTER(i32), P, i64],
+            "kvx_cache_join": [P, i64, i64, i32],
+            "kvx_cache_group": [P, i64, ctypes.POINTER(i32), P, i64],
             "kvx_cache_destroy": [P],
             "kvx_cache_begin_turn": [P, i64, i32, ctypes.POINTER(i32), P, i64],
             "kvx_cache_end_turn": [P, i64],
@@ -381,6 +383,19 @@ def kvx_cache_agent_host(cache, agent: int):
     ids = np.zeros(tok.value // 16, np.int32)
     _check(lib().kvx_cache_agent_host(cache, int(agent), ctypes.byref(tok), ids.ctypes.data, ids.size),
            "kvx_cache_agent_host")
+    return tok.value, ids
+
+
+def kvx_cache_join(cache, agent: int, group: int, shared_tokens: int) -> None:
+    _check(lib().kvx_cache_join(cache, int(agent), int(group), int(shared_tokens)), "kvx_cache_join")
+
+
+def kvx_cache_group(cache, group: int):
+    """Returns (shared_tokens present, page ids of the group node)."""
+    tok = ctypes.c_int32()
+    _check(lib().kvx_cache_group(cache, int(group), ctypes.byref(tok), None, 0), "kvx_cache_group")
+    ids = np.zeros(tok.value // 16, np.int32)
+    _check(lib().kvx_cache_group(cache, int(group), ctypes.byref(tok), ids.ctypes.data, ids.size), "kvx_cache_group")
     return tok.value, ids
 
 

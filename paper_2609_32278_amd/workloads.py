@@ -394,7 +394,9 @@ class AgentTrace:
     """A synthetic multi-turn agent workload (stand-in for replayed agent traces,
     Section 4): agent i starts at tick start[i]; turn k appends new[i][k] tokens
     (user input or tool output) to its context, its reply adds reply[i][k] tokens,
-    and it then waits idle[i][k] ticks (tool or user latency) before the next turn."""
+    and it then waits idle[i][k] ticks (tool or user latency) before the next turn.
+    The first `shared` tokens of every context are the same (a common system
+    prompt, Section 2); the first prompt always covers them."""
     seed: int
     start: list
     new: list
@@ -404,6 +406,7 @@ class AgentTrace:
     num_kv_heads: int = 2
     head_dim: int = 64
     sigma: float = 1.0
+    shared: int = 0
 
     @property
     def num_agents(self) -> int:
@@ -419,8 +422,11 @@ class AgentTrace:
 
 def make_agent_trace(num_agents: int, turns: int, *, seed: int = 0, first=(2048, 8192), new=(64, 1024),
                      reply=(32, 256), idle=(1, 8), spread: int = 8, num_q_heads: int = 8, num_kv_heads: int = 2,
-                     head_dim: int = 64) -> AgentTrace:
-    """Lengths only: integer uniforms (inclusive) from default_rng([7, 0, seed])."""
+                     head_dim: int = 64, shared: int = 0) -> AgentTrace:
+    """Lengths only: integer uniforms (inclusive) from default_rng([7, 0, seed]).
+    `shared` tokens (at most the smallest first prompt) open every context."""
+    if not 0 <= shared <= first[0]:
+        raise ValueError("the shared prefix must fit in every first prompt")
     rng = np.random.default_rng([AGENT_CONFIG_ID, 0, seed])
     start = rng.integers(0, spread + 1, num_agents).tolist()
     news, replies, idles = [], [], []
@@ -430,7 +436,7 @@ def make_agent_trace(num_agents: int, turns: int, *, seed: int = 0, first=(2048,
         news.append(n.tolist())
         replies.append(rng.integers(reply[0], reply[1] + 1, turns).tolist())
         idles.append(rng.integers(idle[0], idle[1] + 1, turns).tolist())
-    return AgentTrace(seed, start, news, replies, idles, num_q_heads, num_kv_heads, head_dim)
+    return AgentTrace(seed, start, news, replies, idles, num_q_heads, num_kv_heads, head_dim, shared=shared)
 
 
 def agent_kv(tr: AgentTrace, agent: int, length: int, device="cpu"):
@@ -440,6 +446,10 @@ def agent_kv(tr: AgentTrace, agent: int, length: int, device="cpu"):
     shape = (tr.max_context(agent), tr.num_kv_heads, tr.head_dim)
     k = _randn_bf16(shape, tr.sigma, _torch_seed(AGENT_CONFIG_ID, 1, tr.seed, 1, agent), device)
     v = _randn_bf16(shape, tr.sigma, _torch_seed(AGENT_CONFIG_ID, 1, tr.seed, 2, agent), device)
+    if tr.shared:  # the common prefix: one generator for every agent
+        sh = (tr.shared, tr.num_kv_heads, tr.head_dim)
+        k[: tr.shared] = _randn_bf16(sh, tr.sigma, _torch_seed(AGENT_CONFIG_ID, 3, tr.seed, 1), device)
+        v[: tr.shared] = _randn_bf16(sh, tr.sigma, _torch_seed(AGENT_CONFIG_ID, 3, tr.seed, 2), device)
     return k[:length], v[:length]
 
 

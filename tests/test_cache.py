@@ -358,3 +358,144 @@ def test_tiered_argument_errors():
         assert kvx.kvx_cache_stats(c)["agents"] == 0
     finally:
         kvx.kvx_cache_destroy(c)
+
+
+# ------------------------------------------------------------------ shared prefixes
+
+class _GroupPair(_TieredPair):
+    """_TieredPair with shared-prefix groups: a shared page holds the group's
+    content ('G', group, j), the same whichever member computed it."""
+
+    def __init__(self, num_pages, host_pages, chunk_tokens, policy, groups):
+        super().__init__(num_pages, host_pages, chunk_tokens, policy)
+        self.groups = groups      # group -> shared pages S
+        self.member = {}          # agent -> group
+
+    def join(self, agent, group):
+        S = self.groups[group]
+        self.o.join(agent, group, S * PAGE)
+        kvx.kvx_cache_join(self.c, agent, group, S * PAGE + 7)  # rounds down to whole pages
+        self.member[agent] = group
+
+    def _content(self, agent, j):
+        g = self.member.get(agent)
+        return ("G", g, j) if g is not None and j < self.groups[g] else (agent, j)
+
+    def begin(self, agent, prompt):
+        try:
+            want = self.o.begin_turn(agent, prompt)
+        except NoMemory:
+            want = None
+        try:
+            prefix, table, mv = kvx.kvx_cache_begin_turn_tiered(self.c, agent, prompt)
+        except kvx.KvxNoMemory as e:
+            assert want is None
+            self._apply(e.moves)
+            return None
+        assert want is not None and prefix == want
+        assert (len(mv["spill_pages"]), len(mv["reload_pages"])) == self.o.last_moves
+        self._apply(mv)
+        n = -(-prompt // PAGE)
+        assert len(table) == n and len(set(table.tolist())) == n
+        for j in range(prefix // PAGE):
+            assert self.dev.get(int(table[j])) == self._content(agent, j), (agent, j)
+        for j in range(prefix // PAGE, n):
+            self.dev[int(table[j])] = self._content(agent, j)
+        self.tables[agent] = table
+        return prefix
+
+    def end(self, agent):
+        self.o.end_turn(agent)
+        kvx.kvx_cache_end_turn(self.c, agent)
+        self.tables.pop(agent)
+
+    def check(self):
+        st = kvx.kvx_cache_stats(self.c)
+        assert st["free_pages"] == self.o.free
+        assert st["evicted_pages"] == self.o.evicted_pages
+        assert st["evictions"] == self.o.evictions
+        assert st["group_pages"] == sum(self.o.group_tokens(g) for g in self.groups) // PAGE
+        owned = []
+        for g in self.groups:
+            tok, pages = kvx.kvx_cache_group(self.c, g)
+            assert tok == self.o.group_tokens(g)
+            for j, pg in enumerate(pages.tolist()):
+                assert self.dev.get(pg) == ("G", g, j)
+            owned.extend(pages.tolist())
+        for a in self.o.agents:
+            cached, pages = kvx.kvx_cache_agent(self.c, a)
+            assert cached == self.o.cached_tokens(a)
+            g = self.member.get(a)
+            start = self.groups[g] if g is not None else 0
+            for k, pg in enumerate(pages.tolist()):
+                assert self.dev.get(pg) == self._content(a, start + k)
+            owned.extend(pages.tolist())
+        for a, t in self.tables.items():
+            # the running turn's own pages: everything past the shared pages and cached ones it reuses
+            g = self.member.get(a)
+            shared = set(kvx.kvx_cache_group(self.c, g)[1].tolist()) if g is not None else set()
+            cached = set(kvx.kvx_cache_agent(self.c, a)[1].tolist())
+            owned.extend(p for p in t.tolist() if p not in shared and p not in cached)
+        assert len(owned) == len(set(owned)), "a page is owned twice"
+        assert len(owned) + st["free_pages"] == self.num_pages
+
+
+def _group_trace(seed, policy, host_pages, steps=700):
+    rng = np.random.default_rng(seed)
+    groups = {0: 6, 1: 3}
+    pair = _GroupPair(400, host_pages, 32, policy, groups)
+    ctx, active, known = {}, set(), set()
+    try:
+        for _ in range(steps):
+            a = int(rng.integers(14))
+            r = rng.random()
+            if a not in known:
+                known.add(a)
+                if a % 3 != 2:                       # two agents in three share a prompt
+                    pair.join(a, a % 2)
+            if a in active:
+                if r < 0.85:
+                    pair.end(a)
+                    active.discard(a)
+                    ctx[a] += int(rng.integers(0, 300))
+            elif a in ctx and r < 0.04:
+                pair.complete(a)
+                del ctx[a]
+                known.discard(a)
+                pair.member.pop(a, None)
+            else:
+                g = pair.member.get(a)
+                base = pair.groups[g] * PAGE + int(rng.integers(0, 40)) if g is not None else int(rng.integers(1, 400))
+                prompt = ctx.get(a, base) + int(rng.integers(1, 500))
+                if r > 0.97:
+                    prompt = int(rng.integers(1, 60))  # now and then a prompt inside the shared span
+                if pair.begin(a, prompt) is not None:
+                    active.add(a)
+                    ctx[a] = prompt
+            pair.check()
+    finally:
+        pair.close()
+    return pair
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("policy", [kvx.KVX_EVICT_RR, kvx.KVX_EVICT_LRU])
+@pytest.mark.parametrize("host_pages", [0, 60])
+def test_shared_prefix_traces_match_the_oracle(seed, policy, host_pages):
+    _group_trace(seed, policy, host_pages)
+
+
+def test_join_errors():
+    c = kvx.kvx_cache_create(64, 16, 64, kvx.KVX_EVICT_RR)
+    try:
+        assert _err(kvx.kvx_cache_join, c, 1, 0, 15) == kvx.KVX_EINVAL     # below one page
+        kvx.kvx_cache_join(c, 1, 0, 64)
+        assert _err(kvx.kvx_cache_join, c, 1, 0, 64) == kvx.KVX_EINVAL     # already a member
+        assert _err(kvx.kvx_cache_join, c, 2, 0, 80) == kvx.KVX_EINVAL     # other span
+        kvx.kvx_cache_begin_turn(c, 3, 40)
+        assert _err(kvx.kvx_cache_join, c, 3, 0, 64) == kvx.KVX_EINVAL     # inside a turn
+        kvx.kvx_cache_end_turn(c, 3)
+        assert _err(kvx.kvx_cache_join, c, 3, 0, 64) == kvx.KVX_EINVAL     # holds pages
+        assert kvx.kvx_cache_group(c, 0)[0] == 0 and kvx.kvx_cache_group(c, 5)[0] == 0
+    finally:
+        kvx.kvx_cache_destroy(c)

@@ -99,3 +99,48 @@ def test_replay_with_a_host_tier_matches_brute_force(policy):
     _replay_oracle(res.events, num_pages, 64, policy, host_pages, res.moves)
     assert res.stats["spilled_pages"] > 0 and res.stats["reloaded_pages"] > 0
     assert any(t.reloaded > 0 for t in checked)
+
+
+@pytest.mark.parametrize("policy", ["lru", "rr"])
+def test_replay_with_a_shared_system_prompt_matches_brute_force(policy):
+    """Every agent's context opens with the same 160 tokens: one shared group node
+    read by every member's page table, created by the first turn that computes it,
+    reclaimed only as a whole leaf.  Every batch against brute force, and the
+    cache's decisions against the oracle."""
+    tr = wl.make_agent_trace(6, 4, seed=4, first=(200, 700), new=(20, 300), reply=(10, 80), idle=(1, 4),
+                             spread=3, num_q_heads=8, num_kv_heads=2, head_dim=64, shared=160)
+    total = sum(tr.max_context(i) for i in range(tr.num_agents))
+    num_pages = int(0.4 * total) // 16
+    print(f"[replay-shared] policy={policy} pages={num_pages}", flush=True)
+    checked = []
+
+    def on_batch(reqs, q, out):
+        row = 0
+        for r in reqs:
+            k, v = wl.agent_kv(tr, r.agent, r.prompt, "cuda")
+            ref, _ = brute_force(to_f64(q[row:row + r.uncached]), to_f64(k), to_f64(v), r.prefix, tr.sm_scale)
+            got = out[row:row + r.uncached].float().cpu().numpy()
+            compare(got, ref, f"{policy}+shared agent {r.agent} turn {r.turn} P={r.prefix} E={r.uncached}")
+            row += r.uncached
+            checked.append(r)
+
+    res = agent_replay.replay(tr, policy, num_pages, chunk_tokens=64, on_batch=on_batch)
+    torch.cuda.synchronize()
+    assert len(checked) == tr.num_agents * len(tr.new[0])
+    o = OracleCache(num_pages, 16, 64, OracleCache.RR if policy == "rr" else OracleCache.LRU)
+    for a in range(tr.num_agents):
+        o.join(a, 0, 160)
+    for ev in res.events:
+        if ev[0] == "begin":
+            try:
+                got = o.begin_turn(ev[1], ev[2])
+            except NoMemory:
+                got = None
+            assert got == ev[3], ev
+        elif ev[0] == "end":
+            o.end_turn(ev[1])
+        else:
+            o.complete(ev[1])
+    assert o.evictions == res.stats["evictions"] > 0
+    # first turns after the node exists reuse the shared pages
+    assert any(t.turn == 0 and t.prefix >= 160 for t in checked)
