@@ -19,6 +19,12 @@
  *   - Device work is queued on `stream` (a hipStream_t; NULL = the null stream)
  *     and is asynchronous: caller-owned buffers must stay alive until the
  *     stream reaches the call.  Calls on one stream execute in order.
+ *   - A pool owns one plan buffer and one partial-result buffer, reused by
+ *     every call on it.  Work on one pool must therefore be ordered: issue its
+ *     calls on one stream, or make a second stream wait (hipStreamWaitEvent)
+ *     for the first one's calls before queuing more on the pool.  Calls on one
+ *     pool that overlap on two streams race on those buffers.  Separate pools
+ *     are independent.
  *   - "host" pointers are ordinary CPU memory read during the call;
  *     "device" pointers are GPU memory (hipMalloc / torch CUDA tensors).
  *   - bf16 means IEEE binary32 truncated to its upper 16 bits (2 bytes).

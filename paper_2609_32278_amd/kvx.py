@@ -158,6 +158,16 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _need(t, nbytes: int, name: str) -> None:
+    """Reject a tensor smaller than the call reads or writes (raw int addresses are
+    the caller's responsibility): the kernels index it by the sizes alone."""
+    if t is None or isinstance(t, int):
+        return
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{name}: {have} bytes, the call needs {nbytes}")
+
+
 def _dptr(t) -> Optional[int]:
     if t is None:
         return None
@@ -180,6 +190,10 @@ class Batch:
         self.extend_lens = np.ascontiguousarray(extend_lens, dtype=np.int32)
         self.page_indptr = np.ascontiguousarray(page_indptr, dtype=np.int32)
         self.page_ids = page_ids_dev  # device int32 tensor (or an int address)
+        if len(self.page_indptr) != len(self.prefix_lens) + 1 or len(self.extend_lens) != len(self.prefix_lens):
+            raise ValueError("prefix_lens and extend_lens need one entry per request, page_indptr one more")
+        if len(self.page_indptr):
+            _need(page_ids_dev, 4 * int(self.page_indptr[-1]), "page_ids")
         self.c = kvx_batch(len(self.prefix_lens), self.prefix_lens.ctypes.data,
                            self.extend_lens.ctypes.data, self.page_indptr.ctypes.data,
                            _dptr(page_ids_dev) if page_ids_dev is not None else None)
@@ -212,14 +226,29 @@ def kv_pool_layout(pool) -> dict:
     return {name: getattr(lay, name) for name, _ in kvx_pool_layout._fields_}
 
 
+def _geometry(pool) -> tuple:
+    """(num_kv_heads, head_dim, elem_bytes) of a pool."""
+    lay = kvx_pool_layout()
+    _check(lib().kv_pool_layout(pool, ctypes.byref(lay)), "kv_pool_layout")
+    return lay.num_kv_heads, lay.head_dim, lay.elem_bytes
+
+
+def _page_buffers(pool, n, k, v) -> None:
+    hkv, d, eb = _geometry(pool)
+    _need(k, n * hkv * 16 * d * eb, "K buffer")
+    _need(v, n * hkv * 16 * d * eb, "V buffer")
+
+
 def kv_pool_write_pages(pool, page_ids, k_src, v_src, stream=None) -> None:
     ids = np.ascontiguousarray(page_ids, dtype=np.int32)
+    _page_buffers(pool, ids.size, k_src, v_src)
     _check(lib().kv_pool_write_pages(pool, ids.ctypes.data, ids.size, _dptr(k_src), _dptr(v_src), _stream(stream)),
            "kv_pool_write_pages")
 
 
 def kv_pool_read_pages(pool, page_ids, k_dst, v_dst, stream=None) -> None:
     ids = np.ascontiguousarray(page_ids, dtype=np.int32)
+    _page_buffers(pool, ids.size, k_dst, v_dst)
     _check(lib().kv_pool_read_pages(pool, ids.ctypes.data, ids.size, _dptr(k_dst), _dptr(v_dst), _stream(stream)),
            "kv_pool_read_pages")
 
@@ -246,6 +275,8 @@ def _move(fn, pool, page_ids, slots, host, host_slots, stream):
     sl = np.ascontiguousarray(slots, dtype=np.int32)
     if ids.shape != sl.shape:
         raise ValueError("page_ids and slots differ in length")
+    if not isinstance(host, int):
+        _need(host, int(host_slots) * kv_pool_record_bytes(pool), "host")
     _check(getattr(lib(), fn)(pool, ids.ctypes.data, sl.ctypes.data, ids.size, _host_ptr(host), int(host_slots),
                               _stream(stream)), fn)
 
@@ -258,7 +289,23 @@ def kv_pool_reload(pool, page_ids, slots, host, host_slots: int, stream=None) ->
     _move("kv_pool_reload", pool, page_ids, slots, host, host_slots, stream)
 
 
+def _suffix_buffers(pool, batch: Batch, num_q_heads: int, **bufs) -> None:
+    """Row buffers of a call: K_ext/V_ext [T, Hkv, d], Q/O [T, Hq, d] bf16, LSE [T, Hq] fp32."""
+    hkv, d, _ = _geometry(pool)
+    t = batch.total_extend
+    rows = {"k_ext": t * hkv, "v_ext": t * hkv, "q": t * num_q_heads, "q_out": t * num_q_heads,
+            "out": t * num_q_heads}
+    for name, buf in bufs.items():
+        if name == "lse":
+            _need(buf, 4 * t * num_q_heads, name)
+        elif name in ("q_norm", "k_norm"):
+            _need(buf, 2 * d, name)
+        else:
+            _need(buf, 2 * d * rows[name], name)
+
+
 def store_kv(pool, batch: Batch, k_ext, v_ext, stream=None) -> None:
+    _suffix_buffers(pool, batch, 0, k_ext=k_ext, v_ext=v_ext)
     _check(lib().store_kv(pool, ctypes.byref(batch.c), _dptr(k_ext), _dptr(v_ext), _stream(stream)), "store_kv")
 
 
@@ -267,6 +314,10 @@ def store_kv_rope(pool, batch: Batch, k_ext, v_ext, *, theta: float = 10000.0, r
                   inv_freq=None, stream=None) -> None:
     """store_kv with RMS norm (optional) and rotary embedding of Q and K fused in."""
     freqs = None if inv_freq is None else np.ascontiguousarray(inv_freq, dtype=np.float64)
+    if freqs is not None and freqs.size < int(rotary_dim) // 2:
+        raise ValueError(f"inv_freq: {freqs.size} entries, rotary_dim {rotary_dim} needs {int(rotary_dim) // 2}")
+    _suffix_buffers(pool, batch, int(num_q_heads), k_ext=k_ext, v_ext=v_ext, q_norm=q_norm, k_norm=k_norm,
+                    **({"q": q, "q_out": q_out} if num_q_heads else {}))
     r = kvx_rope(float(theta), None if freqs is None else freqs.ctypes.data, int(rotary_dim), int(style),
                  _dptr(q_norm), _dptr(k_norm), float(norm_eps))
     _check(lib().store_kv_rope(pool, ctypes.byref(batch.c), ctypes.byref(r), _dptr(q), int(num_q_heads),
@@ -274,6 +325,7 @@ def store_kv_rope(pool, batch: Batch, k_ext, v_ext, *, theta: float = 10000.0, r
 
 
 def extend_attention(pool, batch: Batch, q, num_q_heads: int, sm_scale: float, out, lse=None, stream=None) -> None:
+    _suffix_buffers(pool, batch, int(num_q_heads), q=q, out=out, lse=lse)
     _check(lib().extend_attention(pool, ctypes.byref(batch.c), _dptr(q), int(num_q_heads), float(sm_scale),
                                   _dptr(out), _dptr(lse), _stream(stream)), "extend_attention")
 

@@ -77,6 +77,19 @@ def test_hot_path_argument_errors_before_any_device_work():
     assert _err(kvx.extend_attention_plan, bad0, 4, 2, 128) == kvx.KVX_EINVAL
 
 
+def test_binding_rejects_short_buffers_and_ragged_lengths():
+    import torch
+    kvx._need(torch.empty(8, dtype=torch.int16), 16, "x")  # exactly enough
+    with pytest.raises(ValueError):
+        kvx._need(torch.empty(7, dtype=torch.int16), 16, "x")
+    kvx._need(0x1000, 1 << 40, "raw address")  # raw addresses are not checked
+    kvx._need(None, 16, "absent")
+    with pytest.raises(ValueError):
+        kvx.Batch([16, 0], [4], [0, 2, 2], 0x1000)  # extend_lens one short
+    with pytest.raises(ValueError):
+        kvx.Batch([16], [4], [0, 2, 2], 0x1000)  # page_indptr one too long
+
+
 def _check_plan(w, split=0):
     kvx.kvx_set_split_keys(split)
     try:

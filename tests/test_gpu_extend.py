@@ -201,7 +201,7 @@ def test_empty_batches_are_no_ops():
     pool = kvx.kv_pool_create(8, 16, 2, 64)
     try:
         out = torch.full((4, 4, 64), 7.0, dtype=torch.bfloat16, device=DEV)
-        ids = torch.zeros(1, dtype=torch.int32, device=DEV)
+        ids = torch.zeros(2, dtype=torch.int32, device=DEV)
         b0 = kvx.Batch([], [], [0], ids)
         kvx.extend_attention(pool, b0, out, 4, 0.125, out)
         b1 = kvx.Batch([16, 3], [0, 0], [0, 1, 2], ids)
@@ -227,5 +227,35 @@ def test_validation_mode_rejects_out_of_range_pages(monkeypatch):
         with pytest.raises(kvx.KvxError) as e:
             kvx.extend_attention(pool, b, q, 2, 0.125, q)
         assert e.value.status == kvx.KVX_ERANGE
+    finally:
+        kvx.kv_pool_destroy(pool)
+
+
+def test_binding_rejects_buffers_smaller_than_the_call():
+    """The Python binding checks tensor sizes against the batch and the pool before
+    the C call, so an undersized tensor raises instead of reaching a kernel."""
+    pool = kvx.kv_pool_create(8, 16, 2, 64)
+    try:
+        ids = torch.arange(2, dtype=torch.int32, device=DEV)
+        b = kvx.Batch([16], [4], [0, 2], ids)
+        q = torch.zeros((4, 4, 64), dtype=torch.bfloat16, device=DEV)
+        kv = torch.zeros((4, 2, 64), dtype=torch.bfloat16, device=DEV)
+        with pytest.raises(ValueError):
+            kvx.extend_attention(pool, b, q[:3], 4, 0.125, q)
+        with pytest.raises(ValueError):
+            kvx.extend_attention(pool, b, q, 4, 0.125, q, lse=torch.zeros(15, device=DEV))
+        with pytest.raises(ValueError):
+            kvx.store_kv(pool, b, kv, kv[:3])
+        with pytest.raises(ValueError):
+            kvx.store_kv_rope(pool, b, kv, kv, rotary_dim=64, q=q, num_q_heads=4, q_out=q[:2])
+        with pytest.raises(ValueError):
+            kvx.kv_pool_read_pages(pool, [0, 1], torch.zeros((1, 2, 16, 64), dtype=torch.int16, device=DEV),
+                                   torch.zeros((2, 2, 16, 64), dtype=torch.int16, device=DEV))
+        with pytest.raises(ValueError):
+            kvx.Batch([16], [4], [0, 2], ids[:1])
+        # the same calls with whole buffers go through
+        kvx.store_kv(pool, b, kv, kv)
+        kvx.extend_attention(pool, b, q, 4, 0.125, torch.empty_like(q), lse=torch.zeros(16, device=DEV))
+        torch.cuda.synchronize()
     finally:
         kvx.kv_pool_destroy(pool)

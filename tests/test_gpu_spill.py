@@ -92,8 +92,36 @@ def test_spill_argument_errors():
         assert err(kvx.kv_pool_spill, [0, 1], [2, 2]) == kvx.KVX_EINVAL
         assert err(kvx.kv_pool_reload, [3, 3], [0, 1]) == kvx.KVX_EINVAL
         assert err(kvx.kv_pool_spill, [0], [0], pinned.data_ptr() + 8) == kvx.KVX_EINVAL  # alignment
+        with pytest.raises(ValueError):  # the tensor holds 4 records, not 5
+            kvx.kv_pool_spill(pool, [0], [0], pinned, 5)
         kvx.kv_pool_spill(pool, [0, 0], [0, 1], pinned, 4)   # reading a page twice is fine
         kvx.kv_pool_reload(pool, [5, 6], [0, 0], pinned, 4)  # so is reading a record twice
         torch.cuda.synchronize()
+    finally:
+        kvx.kv_pool_destroy(pool)
+
+
+def test_host_pointer_inside_a_pinned_allocation():
+    """A host buffer that starts inside a larger pinned allocation (a tensor view)
+    addresses its records from its own start."""
+    print("[spill] host view at a record offset", flush=True)
+    pool, k, v = _pool_with_random_pages(8, 2, 64, kvx.KVX_KV_BF16, seed=7)
+    try:
+        rb = kvx.kv_pool_record_bytes(pool)
+        whole = torch.zeros(6 * rb, dtype=torch.uint8, pin_memory=True)
+        view = whole[2 * rb:]  # 4 records, starting at the allocation's third record
+        kvx.kv_pool_spill(pool, [5, 1], [0, 3], view, 4)
+        torch.cuda.synchronize()
+        hb = whole.numpy().reshape(6, 2, -1)
+        kc = k.cpu().numpy().view(np.uint16)
+        assert np.array_equal(hb[2, 0].view(np.uint16).reshape(2, 16, 64), kc[5])
+        assert np.array_equal(hb[5, 0].view(np.uint16).reshape(2, 16, 64), kc[1])
+        assert (hb[[0, 1, 3, 4]] == 0).all()
+        kvx.kv_pool_reload(pool, [6, 7], [3, 0], view, 4)
+        k2 = torch.empty((2, 2, 16, 64), dtype=k.dtype, device=DEV)
+        v2 = torch.empty_like(k2)
+        kvx.kv_pool_read_pages(pool, [6, 7], k2, v2)
+        torch.cuda.synchronize()
+        assert torch.equal(k2, k[[1, 5]]) and torch.equal(v2, v[[1, 5]])
     finally:
         kvx.kv_pool_destroy(pool)
