@@ -28,6 +28,8 @@ def brute_force(q: np.ndarray, k: np.ndarray, v: np.ndarray, prefix_len: int, sm
     n, hkv, _ = k.shape
     assert n == prefix_len + e
     g = hq // hkv
+    if e == 0:  # no suffix rows (the request may have no keys at all)
+        return np.zeros((0, hq, d)), np.zeros((0, hq))
     kx = np.repeat(k, g, axis=1)  # [L, Hq, d]: query head h reads kv head h // g
     vx = np.repeat(v, g, axis=1)
     s = np.einsum("ihc,jhc->hij", q, kx) * sm_scale  # [Hq, E, L]

@@ -7,6 +7,7 @@ import re
 
 import numpy as np
 import pytest
+from hypothesis import assume, given, settings, strategies as st
 
 from paper_2609_32278_amd import kvx
 from paper_2609_32278_amd import workloads as wl
@@ -133,6 +134,22 @@ def _check_plan(w, split=0):
     assert not seen
     # longest first within an XCD, by request then by tile
     return items
+
+
+@settings(max_examples=40, deadline=None, derandomize=True)
+@given(st.data())
+def test_plan_covers_drawn_batches(data):
+    """The coverage check of the work plan on ragged batches hypothesis draws, with
+    and without forced key splits."""
+    r = data.draw(st.integers(1, 6), label="requests")
+    prefix = data.draw(st.lists(st.integers(0, 3000), min_size=r, max_size=r), label="prefix_lens")
+    extend = data.draw(st.lists(st.integers(0, 600), min_size=r, max_size=r), label="extend_lens")
+    assume(sum(extend) > 0)
+    hkv = data.draw(st.sampled_from([1, 2, 3, 8]), label="kv_heads")
+    g = data.draw(st.sampled_from([1, 4, 8]), label="group")
+    split = data.draw(st.sampled_from([0, 0, 64, 1024]), label="split_keys")
+    w = wl.make_custom(prefix, extend, hkv * g, hkv, 128, seed=1)
+    _check_plan(w, split)
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama8b", "tail_outlier", "rr_partial", "wide70b", "decode_llama8b",

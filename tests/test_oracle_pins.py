@@ -21,6 +21,7 @@ import numpy as np
 import pytest
 import torch
 import torch.nn.functional as F
+from hypothesis import assume, given, settings, strategies as st
 
 import oracle
 from helpers import (brute_force, brute_force_all, fp8_dequant_torch, oracle_all_rows,
@@ -43,6 +44,26 @@ def test_brute_force_tiny_config():
     (out, lse), _, _ = _oracle_outputs(w, want_lse=True)
     ref, ref_lse = brute_force_all(w)
     assert out.shape == ref.shape == (156, 4, 64)
+    assert np.abs(out - ref).max() <= TOL
+    assert np.abs(lse - ref_lse).max() <= TOL
+
+
+@settings(max_examples=30, deadline=None, derandomize=True)
+@given(st.data())
+def test_brute_force_on_drawn_shapes(data):
+    """(a) on shapes hypothesis draws: ragged prefixes and suffixes (empty ones too),
+    one to four KV heads, GQA groups of 1-4, random page placement and pool slack."""
+    r = data.draw(st.integers(1, 4), label="requests")
+    prefix = data.draw(st.lists(st.integers(0, 70), min_size=r, max_size=r), label="prefix_lens")
+    extend = data.draw(st.lists(st.integers(0, 40), min_size=r, max_size=r), label="extend_lens")
+    assume(sum(extend) > 0)
+    hkv = data.draw(st.integers(1, 4), label="kv_heads")
+    g = data.draw(st.sampled_from([1, 2, 4]), label="group")
+    d = data.draw(st.sampled_from([8, 16, 32]), label="head_dim")
+    w = wl.make_custom(prefix, extend, hkv * g, hkv, d, seed=data.draw(st.integers(0, 9999), label="seed"),
+                       pool_factor=data.draw(st.sampled_from([1.0, 1.5, 3.0]), label="pool_factor"))
+    (out, lse), _, _ = _oracle_outputs(w, want_lse=True)
+    ref, ref_lse = brute_force_all(w)
     assert np.abs(out - ref).max() <= TOL
     assert np.abs(lse - ref_lse).max() <= TOL
 
