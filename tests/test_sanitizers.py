@@ -1,8 +1,10 @@
 """AddressSanitizer and UndefinedBehaviorSanitizer builds of the host code (no GPU):
 the prefix cache (csrc/kvx_cache.cpp) under random turn sequences of both
-policies with host tiers, recency tiers and shared-prefix groups, and the C
-oracle under random ragged batches stored into NaN-filled pools.  The drivers
-also check ownership and finiteness invariants; see tests/sanitize/."""
+policies with host tiers, recency tiers and shared-prefix groups; the work
+planners of csrc/kvx_host.cpp under random ragged batches (kernel launchers
+stubbed out); and the C oracle under random ragged batches stored into
+NaN-filled pools.  The drivers also check ownership, coverage and finiteness
+invariants; see tests/sanitize/."""
 
 import os
 import shutil
@@ -43,6 +45,20 @@ def test_oracle_under_sanitizers(tmp_path):
     exe = str(tmp_path / "oracle_stress")
     cmd = ["gcc", "-std=c11", *SAN, "-fopenmp", os.path.join(ROOT, "oracle", "oracle.c"),
            os.path.join(ROOT, "tests", "sanitize", "oracle_stress.c"), "-lm", "-o", exe]
+    out = _build_and_run(cmd, exe, ["300"], tmp_path)
+    assert "passed" in out
+    print(out)
+
+
+@pytest.mark.skipif(shutil.which("g++") is None or not os.path.exists("/opt/rocm/lib/libamdhip64.so"),
+                    reason="g++ or the HIP runtime library not installed")
+def test_planner_under_sanitizers(tmp_path):
+    exe = str(tmp_path / "plan_stress")
+    cmd = ["g++", "-std=c++17", *SAN, "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+           "-I" + os.path.join(ROOT, "include"), "-I" + os.path.join(ROOT, "paper_2609_32278_amd", "csrc"),
+           os.path.join(ROOT, "paper_2609_32278_amd", "csrc", "kvx_host.cpp"),
+           os.path.join(ROOT, "tests", "sanitize", "plan_stress.cpp"),
+           "-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib", "-o", exe]
     out = _build_and_run(cmd, exe, ["300"], tmp_path)
     assert "passed" in out
     print(out)
