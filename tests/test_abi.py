@@ -196,3 +196,22 @@ def test_plan_balances_xcds_for_eight_kv_heads():
     cost = np.zeros(8)
     np.add.at(cost, real["xcd"], (real["key_end"] - real["key_begin"]).astype(np.float64))
     assert cost.max() / cost.min() < 1.0001
+
+
+def test_headers_compile_as_c99_and_work_from_c(tmp_path):
+    """A C99 program (tests/c_abi/consumer.c) includes both public headers with
+    -pedantic -Werror, links libkvx.so and calls the host-only entry points."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not installed")
+    exe = str(tmp_path / "consumer")
+    lib_dir = os.path.dirname(kvx.LIB_PATH)
+    cmd = ["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror", "-I" + os.path.join(ROOT, "include"),
+           os.path.join(ROOT, "tests", "c_abi", "consumer.c"), "-L" + lib_dir, "-l:libkvx.so",
+           "-Wl,-rpath," + lib_dir, "-o", exe]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-3000:]
+    run = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    assert run.returncode == 0, run.stdout + run.stderr
+    assert "cache cycle ok" in run.stdout
