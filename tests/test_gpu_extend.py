@@ -59,6 +59,14 @@ CASES = {
     "decode_g16_d64": ([700, 16, 0, 4100], [1, 1, 1, 0], 32, 2, 64, wl.KV_BF16),
     "decode_fp8_d64": ([9000, 33], [1, 1], 8, 4, 64, wl.KV_FP8_E4M3),
     "long_causal": ([0], [1000], 4, 1, 128, wl.KV_BF16),
+    # wide groups: 32 and the maximum 256 query heads per KV head (8 and 1 tokens per
+    # tile); a one-token batch above the decode kernel's group limit (prefill path)
+    "g32_d128": ([100, 3, 0], [40, 9, 17], 32, 1, 128, wl.KV_BF16),
+    "g256_d64": ([50, 0], [5, 3], 256, 1, 64, wl.KV_BF16),
+    "decode_g32_fp8": ([500, 20], [1, 1], 64, 2, 128, wl.KV_FP8_E4M3),
+    # KV head counts off the XCD count: 3 (greedy XCD binding) and 16
+    "hkv3_fp8_d128": ([129, 40, 0, 700], [60, 1, 33, 90], 6, 3, 128, wl.KV_FP8_E4M3),
+    "hkv16_d64": ([16, 250], [70, 31], 32, 16, 64, wl.KV_BF16),
 }
 
 
