@@ -25,6 +25,10 @@
  *     for the first one's calls before queuing more on the pool.  Calls on one
  *     pool that overlap on two streams race on those buffers.  Separate pools
  *     are independent.
+ *   - Calls build their work plan on the host and upload it through a pinned
+ *     staging buffer, waiting on the host for that buffer's previous copy, and
+ *     may allocate device scratch the first time a size is seen: they are not
+ *     meant to be captured into a HIP graph.
  *   - "host" pointers are ordinary CPU memory read during the call;
  *     "device" pointers are GPU memory (hipMalloc / torch CUDA tensors).
  *   - bf16 means IEEE binary32 truncated to its upper 16 bits (2 bytes).
