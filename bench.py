@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6  # 256 CUs x 2.4 GHz x 4096 dense bf16 flop/clk/CU
 PEAK_HBM_GBPS = 8000.0
+CPU_SAMPLE_TRIPLES = 330_000_000  # oracle sample size in (row, query head, key) triples
 
 DESCRIPTIONS = {
     "tiny": "4 requests, P {0,64,208,512}, E {32,16,100,8}, Hq 4 / Hkv 2, d 64, page 16, bf16 K/V",
@@ -129,8 +130,10 @@ def run_gpu(config: str, steps: int, warmup: int, rope: bool = False):
     import torch
     from paper_2609_32278_amd import kvx
 
+    print(f"[bench] setup {config}", file=sys.stderr, flush=True)
     s = setup(config, rope=rope)
     w, pool, batch = s["w"], s["pool"], s["batch"]
+    print(f"[bench] timing {warmup} + {steps} steps", file=sys.stderr, flush=True)
     q, k_ext, v_ext, out = s["q"], s["k_ext"], s["v_ext"], s["out"]
     q_rot = torch.empty_like(q) if rope else q
 
@@ -173,6 +176,21 @@ def run_cpu_baseline(config: str, rows_per_req: int, max_reqs: int):
 
     w = wl.make_workload(config)
     reqs = list(range(min(w.num_reqs, max_reqs)))
+    if rows_per_req <= 0:
+        # about CPU_SAMPLE_TRIPLES (row, query head, key) triples, ~15 s of the oracle on 16 cores; an fp8
+        # pool's keys cost the oracle 2.3x (it decodes every code).  Each request contributes at least its
+        # first, last and page-boundary rows, so the largest configs also sample fewer requests.
+        weight = 2.3 if w.kv_dtype != 0 else 1.0
+        cost = [weight * w.num_q_heads * (int(w.prefix_lens[r]) + int(w.extend_lens[r]) / 2) for r in reqs]
+        rows_per_req = int(min(32, max(4, CPU_SAMPLE_TRIPLES // max(sum(cost), 1))))
+        if rows_per_req == 4:
+            keep, total = 0, 0.0
+            while keep < len(reqs) and (keep < 2 or total + 4 * cost[keep] <= CPU_SAMPLE_TRIPLES):
+                total += 4 * cost[keep]
+                keep += 1
+            reqs = reqs[:keep]
+    print(f"[bench] cpu baseline: {rows_per_req} rows per request of {len(reqs)} requests", file=sys.stderr,
+          flush=True)
     sub = w.subset(reqs)
     t = wl.batch_tensors(sub, device="cuda")
     t = {k: v.cpu() for k, v in t.items()}
@@ -218,7 +236,8 @@ def main():
     ap.add_argument("--rope", action="store_true",
                     help="the step's store also RMS-normalises and rotates Q and K (store_kv_rope)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=32)
+    ap.add_argument("--cpu-rows", type=int, default=0,
+                    help="oracle sample rows per request (0: sized to about 15 s of oracle work, at most 32)")
     ap.add_argument("--cpu-reqs", type=int, default=16)
     ap.add_argument("--calib-copy", action="store_true",
                     help="run only a plain 1 GiB device copy kernel (HBM counter calibration)")
