@@ -319,6 +319,8 @@ def main(argv=None) -> int:
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--capacity", type=float, default=0.5,
                     help="pool size as a fraction of the summed final contexts of all agents")
+    ap.add_argument("--pool-tokens", type=int, default=0,
+                    help="pool size in tokens (overrides --capacity; a fixed pool for concurrency sweeps)")
     ap.add_argument("--chunk-tokens", type=int, default=1024)
     ap.add_argument("--decode-ticks", type=int, default=2)
     ap.add_argument("--heads", default="32,8,128", help="Hq,Hkv,head_dim")
@@ -336,7 +338,7 @@ def main(argv=None) -> int:
     tr = wl.make_agent_trace(args.agents, args.turns, seed=args.seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
                              shared=args.shared)
     total = sum(tr.max_context(i) for i in range(tr.num_agents))
-    num_pages = int(args.capacity * total) // wl.PAGE_SIZE
+    num_pages = (args.pool_tokens if args.pool_tokens > 0 else int(args.capacity * total)) // wl.PAGE_SIZE
     for pol in (["lru", "rr"] if args.policy == "both" else [args.policy]):
         host_pages = int(args.host_pages * num_pages)
         r = replay(tr, pol, num_pages, chunk_tokens=args.chunk_tokens, decode_ticks=args.decode_ticks,

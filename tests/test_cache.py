@@ -235,6 +235,20 @@ def test_round_robin_spreads_the_loss_on_a_replay():
     assert s["rr"]["uncached_p99"] < s["lru"]["uncached_p99"]
 
 
+def test_replay_cli_fixed_pool(capsys):
+    """--pool-tokens fixes the pool across a concurrency sweep: the CLI reports that
+    pool, and once 28 agents overflow 200k tokens round robin keeps the P99 tail
+    below LRU's (seed 0: 7454 vs 12399 uncached tokens)."""
+    import json
+    from paper_2609_32278_amd import agent_replay
+    assert agent_replay.main(["--no-gpu", "--agents", "28", "--turns", "8", "--pool-tokens", "200000"]) == 0
+    rows = [json.loads(x) for x in capsys.readouterr().out.splitlines() if x.startswith("{")]
+    by = {r["policy"]: r for r in rows}
+    assert by["lru"]["num_pages"] == by["rr"]["num_pages"] == 200000 // PAGE
+    assert by["rr"]["uncached_p99"] < 0.7 * by["lru"]["uncached_p99"]
+    assert by["rr"]["full_misses"] < by["lru"]["full_misses"]
+
+
 # ------------------------------------------------------------------ host tier
 
 class _TieredPair(_Pair):
