@@ -80,3 +80,24 @@ def test_full_config_parity(name):
         assert np.array_equal(gv, ref_pool.v[sub.page_ids]), f"{name}: V pages differ"
     finally:
         run.close()
+
+
+def test_row_offsets_past_two_to_the_31():
+    """Q and O of 300,000 suffix tokens x 64 query heads x 128 dims hold 2.46e9 elements,
+    so the last rows' offsets pass 2^31: rows at both ends of both requests must
+    match the oracle (64-bit row indexing in the kernel, the binding and the plan)."""
+    w = wl.make_custom([0, 4096], [150000, 150000], 64, 8, 128, seed=31, name="offsets64")
+    assert w.total_extend * w.num_q_heads * w.head_dim > 2 ** 31
+    rows = np.array([[0, 0], [0, 149999], [1, 0], [1, 77777], [1, 149998], [1, 149999]], np.int32)
+    print(f"[config] offsets64: T={w.total_extend} pages={w.num_pages} rows={len(rows)}", flush=True)
+    run = GpuRun(w)
+    try:
+        run.store()
+        out = run.attend()
+        assert not torch.isnan(out[-1]).any() and not torch.isnan(out[0]).any()
+        print("[config] offsets64: GPU done, running the oracle", flush=True)
+        ref, gidx = oracle_rows(w, run.q, rows)
+        got = out[torch.from_numpy(gidx).to(out.device)].float().cpu().numpy().astype(np.float64)
+        compare(got, ref, "offsets64")
+    finally:
+        run.close()
