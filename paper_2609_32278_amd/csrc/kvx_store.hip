@@ -6,7 +6,9 @@
 // from the pool.  HBM-bound: each element is read once and written once.
 //
 // Pool layout: K [page][kv_head][slot][dim], V [page][kv_head][dim][slot].
-// One workgroup handles one page of one request (all KV heads): K rows are
+// One workgroup handles one page of one request (all KV heads), in passes of
+// 4 heads (head_dim 128) or 8 (head_dim 64) whose loads are all issued before any
+// is used (four K and four V 16-byte loads in flight per thread): K rows are
 // copied with 16-byte accesses, V rows are staged in LDS and written out
 // transposed, one 16-slot column (32 bytes bf16 / 16 bytes fp8) per dim.
 // fp8 pool: code = e4m3_rne(clamp(x * inv_scale_h, -448, 448)) with the
@@ -80,28 +82,41 @@ __device__ __forceinline__ void write_vt(const uint16_t (&vs)[kPageSize][D + 8],
 
 template <int D, bool FP8>
 __global__ __launch_bounds__(kStoreThreads) void store_kv_kernel(StoreParams p) {
-  // V rows of this page for one head, staged for the transpose: [16 slots][D] bf16
-  __shared__ __attribute__((aligned(16))) uint16_t vs[kPageSize][D + 8];
+  constexpr int CPR = D / 8;                          // 16-byte chunks per bf16 row
+  constexpr int CHUNKS = kPageSize * CPR;             // per head
+  constexpr int HB = 4 * kStoreThreads / CHUNKS;      // heads per pass: 4 (D = 128), 8 (D = 64)
+  constexpr int PER = HB * CHUNKS / kStoreThreads;    // chunks per thread and pass
+  static_assert(PER == 4, "four K and four V loads in flight per thread");
+  // V rows of this page for the pass's heads, staged for the transpose: [head][16 slots][D] bf16
+  __shared__ __attribute__((aligned(16))) uint16_t vs[HB][kPageSize][D + 8];
   const StoreUnit su = p.units[blockIdx.x];
   const int page = p.page_ids[su.page_pos];
   const int H = p.num_kv_heads;
-  constexpr int CPR = D / 8;                // 16-byte chunks per bf16 row
-  constexpr int CHUNKS = kPageSize * CPR;   // per head
 
-  for (int hd = 0; hd < H; hd++) {
-    const float kinv = FP8 ? p.k_inv_scale[hd] : 1.0f;
-    const float vinv = FP8 ? p.v_inv_scale[hd] : 1.0f;
-    const size_t blk = ((size_t)page * H + hd) * (size_t)(kPageSize * D);
-    for (int c = threadIdx.x; c < CHUNKS; c += kStoreThreads) {
-      const int slot = c / CPR, cc = c % CPR;
-      uint4 kx = make_uint4(0, 0, 0, 0), vx = make_uint4(0, 0, 0, 0);
-      const bool live = slot >= su.slot_begin && slot < su.slot_end;
-      if (live) {
+  for (int h0 = 0; h0 < H; h0 += HB) {
+    // every load of the pass is issued before any of them is used
+    uint4 kx[PER], vx[PER];
+#pragma unroll
+    for (int j = 0; j < PER; j++) {
+      const int i = threadIdx.x + j * kStoreThreads;
+      const int hd = h0 + i / CHUNKS, slot = (i % CHUNKS) / CPR, cc = i % CPR;
+      kx[j] = vx[j] = make_uint4(0, 0, 0, 0);
+      if (hd < H && slot >= su.slot_begin && slot < su.slot_end) {
         const size_t src = ((size_t)(su.row_slot0 + slot) * H + hd) * D + cc * 8;
-        kx = *(const uint4*)(p.k_ext + src);
-        vx = *(const uint4*)(p.v_ext + src);
+        kx[j] = *(const uint4*)(p.k_ext + src);
+        vx[j] = *(const uint4*)(p.v_ext + src);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < PER; j++) {
+      const int i = threadIdx.x + j * kStoreThreads;
+      const int hb = i / CHUNKS, hd = h0 + hb, slot = (i % CHUNKS) / CPR, cc = i % CPR;
+      if (hd >= H) continue;
+      if (slot >= su.slot_begin && slot < su.slot_end) {
+        const size_t blk = ((size_t)page * H + hd) * (size_t)(kPageSize * D);
         if constexpr (FP8) {
-          const uint16_t* ke = (const uint16_t*)&kx;
+          const float kinv = p.k_inv_scale[hd];
+          const uint16_t* ke = (const uint16_t*)&kx[j];
           uint2 code;
           code.x = e4m3x4(bf16_to_f32(ke[0]) * kinv, bf16_to_f32(ke[1]) * kinv,
                           bf16_to_f32(ke[2]) * kinv, bf16_to_f32(ke[3]) * kinv);
@@ -109,13 +124,17 @@ __global__ __launch_bounds__(kStoreThreads) void store_kv_kernel(StoreParams p) 
                           bf16_to_f32(ke[6]) * kinv, bf16_to_f32(ke[7]) * kinv);
           *(uint2*)((uint8_t*)p.k_pool + blk + (size_t)slot * D + cc * 8) = code;
         } else {
-          *(uint4*)((uint16_t*)p.k_pool + blk + (size_t)slot * D + cc * 8) = kx;
+          *(uint4*)((uint16_t*)p.k_pool + blk + (size_t)slot * D + cc * 8) = kx[j];
         }
       }
-      *(uint4*)(&vs[slot][cc * 8]) = vx;
+      *(uint4*)(&vs[hb][slot][cc * 8]) = vx[j];
     }
     __syncthreads();
-    write_vt<D, FP8>(vs, p.v_pool, blk, su.slot_begin, su.slot_end, vinv);
+    for (int hb = 0; hb < HB && h0 + hb < H; hb++) {
+      const int hd = h0 + hb;
+      const size_t blk = ((size_t)page * H + hd) * (size_t)(kPageSize * D);
+      write_vt<D, FP8>(vs[hb], p.v_pool, blk, su.slot_begin, su.slot_end, FP8 ? p.v_inv_scale[hd] : 1.0f);
+    }
     __syncthreads();
   }
 }
