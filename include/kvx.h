@@ -23,8 +23,9 @@
  *     every call on it.  Work on one pool must therefore be ordered: issue its
  *     calls on one stream, or make a second stream wait (hipStreamWaitEvent)
  *     for the first one's calls before queuing more on the pool.  Calls on one
- *     pool that overlap on two streams race on those buffers.  Separate pools
- *     are independent.
+ *     pool that overlap on two streams race on those buffers, and calls on one
+ *     pool must come from one host thread at a time.  Separate pools are
+ *     independent.
  *   - Calls build their work plan on the host and upload it through a pinned
  *     staging buffer, waiting on the host for that buffer's previous copy, and
  *     may allocate device scratch the first time a size is seen: they are not
