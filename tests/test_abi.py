@@ -215,3 +215,14 @@ def test_headers_compile_as_c99_and_work_from_c(tmp_path):
     run = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert run.returncode == 0, run.stdout + run.stderr
     assert "cache cycle ok" in run.stdout
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """With no built libkvx.so the binding raises KvxNotBuilt on first use: there
+    is no CPU or torch fallback on the product path."""
+    monkeypatch.setattr(kvx, "_lib", None)
+    monkeypatch.setattr(kvx, "LIB_PATH", str(tmp_path / "libkvx.so"))
+    with pytest.raises(kvx.KvxNotBuilt):
+        kvx.lib()
+    with pytest.raises(kvx.KvxNotBuilt):
+        kvx.extend_attention_plan(kvx.Batch([0], [4], [0, 1], 0x1000), 4, 2, 128)
