@@ -194,6 +194,8 @@ class Batch:
             raise ValueError("prefix_lens and extend_lens need one entry per request, page_indptr one more")
         if len(self.page_indptr):
             _need(page_ids_dev, 4 * int(self.page_indptr[-1]), "page_ids")
+        if page_ids_dev is not None and not isinstance(page_ids_dev, int) and page_ids_dev.element_size() != 4:
+            raise ValueError(f"page_ids must hold 4-byte (int32) page ids, got {page_ids_dev.dtype}")
         self.c = kvx_batch(len(self.prefix_lens), self.prefix_lens.ctypes.data,
                            self.extend_lens.ctypes.data, self.page_indptr.ctypes.data,
                            _dptr(page_ids_dev) if page_ids_dev is not None else None)

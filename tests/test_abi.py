@@ -89,6 +89,8 @@ def test_binding_rejects_short_buffers_and_ragged_lengths():
         kvx.Batch([16, 0], [4], [0, 2, 2], 0x1000)  # extend_lens one short
     with pytest.raises(ValueError):
         kvx.Batch([16], [4], [0, 2, 2], 0x1000)  # page_indptr one too long
+    with pytest.raises(ValueError, match="int32"):
+        kvx.Batch([16], [4], [0, 2], torch.zeros(2, dtype=torch.int64))  # int64 page ids
 
 
 def _check_plan(w, split=0):
