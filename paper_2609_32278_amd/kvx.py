@@ -298,6 +298,8 @@ def _suffix_buffers(pool, batch: Batch, num_q_heads: int, **bufs) -> None:
     rows = {"k_ext": t * hkv, "v_ext": t * hkv, "q": t * num_q_heads, "q_out": t * num_q_heads,
             "out": t * num_q_heads}
     for name, buf in bufs.items():
+        if buf is not None and not isinstance(buf, int) and buf.element_size() != (4 if name == "lse" else 2):
+            raise ValueError(f"{name}: {buf.dtype} elements; expected {'float32' if name == 'lse' else 'bf16'}")
         if name == "lse":
             _need(buf, 4 * t * num_q_heads, name)
         elif name in ("q_norm", "k_norm"):

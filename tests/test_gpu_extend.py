@@ -261,6 +261,8 @@ def test_binding_rejects_buffers_smaller_than_the_call():
                                    torch.zeros((2, 2, 16, 64), dtype=torch.int16, device=DEV))
         with pytest.raises(ValueError):
             kvx.Batch([16], [4], [0, 2], ids[:1])
+        with pytest.raises(ValueError, match="bf16"):  # float32 Q of enough bytes is still refused
+            kvx.extend_attention(pool, b, q.float(), 4, 0.125, q)
         # the same calls with whole buffers go through
         kvx.store_kv(pool, b, kv, kv)
         kvx.extend_attention(pool, b, q, 4, 0.125, torch.empty_like(q), lse=torch.zeros(16, device=DEV))
