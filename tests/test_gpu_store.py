@@ -25,10 +25,19 @@ def _case(name):
     if name == "ragged_fp8_d128":
         return wl.make_custom([0, 5, 16, 37, 100, 3, 1000], [7, 0, 1, 29, 18, 40, 200], 8, 2, 128,
                               kv_dtype=wl.KV_FP8_E4M3, seed=5)
+    # KV head counts that leave a partial pass of the store's head batches (4 per pass at
+    # head_dim 128, 8 at 64)
+    if name == "hkv5_d128":
+        return wl.make_custom([0, 21, 300], [40, 17, 33], 10, 5, 128, seed=6)
+    if name == "hkv9_fp8_d64":
+        return wl.make_custom([7, 0], [50, 16], 9, 9, 64, kv_dtype=wl.KV_FP8_E4M3, seed=7)
+    if name == "hkv3_d64":
+        return wl.make_custom([16, 3], [64, 13], 6, 3, 64, seed=8)
     raise KeyError(name)
 
 
-@pytest.mark.parametrize("name", ["tiny", "tiny_fp8", "ragged_d128", "ragged_fp8_d128"])
+@pytest.mark.parametrize("name", ["tiny", "tiny_fp8", "ragged_d128", "ragged_fp8_d128", "hkv5_d128", "hkv9_fp8_d64",
+                                  "hkv3_d64"])
 def test_store_kv_pool_bit_exact(name):
     print(f"[store] {name}", flush=True)
     w = _case(name)
