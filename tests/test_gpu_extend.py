@@ -269,3 +269,29 @@ def test_binding_rejects_buffers_smaller_than_the_call():
         torch.cuda.synchronize()
     finally:
         kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_seeded_random_batches(seed):
+    """Seeded random small batches (1-5 requests, ragged and empty suffixes, prefixes
+    up to 700 tokens, GQA groups 1-8, head_dim 64/128, bf16 or fp8 pools, optional
+    forced splits), every row against the oracle with LSE."""
+    rng = np.random.default_rng([17, seed])
+    r = int(rng.integers(1, 6))
+    prefix = rng.integers(0, 700, r).tolist()
+    extend = [int(x) if rng.random() > 0.15 else 0 for x in rng.integers(1, 260, r)]
+    if sum(extend) == 0:
+        extend[0] = 1
+    hkv = int(rng.choice([1, 2, 3, 4]))
+    g = int(rng.choice([1, 2, 4, 8]))
+    d = int(rng.choice([64, 128]))
+    dt = wl.KV_FP8_E4M3 if rng.random() < 0.3 else wl.KV_BF16
+    split = int(rng.choice([0, 0, 64, 256]))
+    w = wl.make_custom(prefix, extend, hkv * g, hkv, d, kv_dtype=dt, seed=100 + seed)
+    print(f"[random] seed={seed} P={prefix} E={extend} Hq={hkv * g} Hkv={hkv} d={d} fp8={dt} split={split}",
+          flush=True)
+    kvx.kvx_set_split_keys(split)
+    try:
+        _run_and_compare(w, f"random{seed}", want_lse=True)
+    finally:
+        kvx.kvx_set_split_keys(0)
