@@ -144,3 +144,33 @@ def test_replay_with_a_shared_system_prompt_matches_brute_force(policy):
     assert o.evictions == res.stats["evictions"] > 0
     # first turns after the node exists reuse the shared pages
     assert any(t.turn == 0 and t.prefix >= 160 for t in checked)
+
+
+@pytest.mark.parametrize("policy", ["lru", "rr"])
+def test_replay_with_every_feature_at_once(policy):
+    """A shared system prompt, a host tier, no completion signals and (round robin)
+    recency tiers in one replay: every batch against brute force over the agent's
+    logical context, whatever mix of reused, reloaded, shared and recomputed pages
+    its prefix came from."""
+    tr = wl.make_agent_trace(8, 4, seed=9, first=(200, 700), new=(20, 300), reply=(10, 80), idle=(1, 4),
+                             spread=3, num_q_heads=8, num_kv_heads=2, head_dim=64, shared=96)
+    total = sum(tr.max_context(i) for i in range(tr.num_agents))
+    num_pages = int(0.35 * total) // 16
+    print(f"[replay-all] policy={policy} pages={num_pages} host={num_pages // 2}", flush=True)
+    checked = []
+
+    def on_batch(reqs, q, out):
+        row = 0
+        for r in reqs:
+            k, v = wl.agent_kv(tr, r.agent, r.prompt, "cuda")
+            ref, _ = brute_force(to_f64(q[row:row + r.uncached]), to_f64(k), to_f64(v), r.prefix, tr.sm_scale)
+            got = out[row:row + r.uncached].float().cpu().numpy()
+            compare(got, ref, f"{policy}+all agent {r.agent} turn {r.turn} P={r.prefix} E={r.uncached}")
+            row += r.uncached
+            checked.append(r)
+
+    res = agent_replay.replay(tr, policy, num_pages, chunk_tokens=64, on_batch=on_batch, host_pages=num_pages // 2,
+                              completion_signals=False, tier_width=6 if policy == "rr" else 0)
+    torch.cuda.synchronize()
+    assert len(checked) == tr.num_agents * len(tr.new[0])
+    assert res.stats["evictions"] > 0 and res.stats["spilled_pages"] > 0
