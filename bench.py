@@ -12,7 +12,10 @@ Prints one JSON line: algorithmic TFLOP/s of the step (4*d*Hq per visible causal
 the attention kernel's roofline entry, and the CPU oracle timed on a bounded
 sample of the same workload.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config llama8b]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config wide70b]
+
+The default workload is the largest single-GPU one, the 70B-shaped layer
+(48 requests, 64 query / 8 KV heads, 6.3e14 FLOP per step).
 """
 
 from __future__ import annotations
@@ -160,16 +163,17 @@ def run_gpu(config: str, steps: int, warmup: int, rope: bool = False):
         step(evs[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    store_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    store_t = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    attn_t = np.array([e[1].elapsed_time(e[2]) for e in evs])
     ms_step = (t1 - t0) * 1e3 / steps
     assert torch.isfinite(out.float()).all(), "non-finite attention output"
     kvx.kv_pool_destroy(pool)
-    return w, ms_step, store_ms, attn_ms
+    return w, ms_step, store_t, attn_t, out
 
 
-def run_cpu_baseline(config: str, rows_per_req: int, max_reqs: int):
-    """The oracle as it stands, on a bounded sample of the same workload."""
+def run_cpu_baseline(config: str, rows_per_req: int, max_reqs: int, gpu_out=None):
+    """The oracle as it stands, on a bounded sample of the same workload.  With the
+    GPU's output of the timed steps, also the parity of the sampled rows."""
     import torch
     import oracle
     from paper_2609_32278_amd import workloads as wl
@@ -208,13 +212,23 @@ def run_cpu_baseline(config: str, rows_per_req: int, max_reqs: int):
     if os.environ.get("OMP_NUM_THREADS", "").isdigit():
         cores = min(cores, int(os.environ["OMP_NUM_THREADS"]))
     t0 = time.perf_counter()
-    oracle.extend_attention(pool, sub.prefix_lens, sub.extend_lens, sub.page_indptr, sub.page_ids, q_rows,
-                            rows[:, 0], rows[:, 1], w.num_q_heads, w.sm_scale, num_threads=cores)
+    ref = oracle.extend_attention(pool, sub.prefix_lens, sub.extend_lens, sub.page_indptr, sub.page_ids, q_rows,
+                                  rows[:, 0], rows[:, 1], w.num_q_heads, w.sm_scale, num_threads=cores)
     dt = time.perf_counter() - t0
     used = oracle.max_threads()
     visible = int(sum(int(sub.prefix_lens[r]) + int(i) + 1 for r, i in rows))
     flops = 4.0 * w.head_dim * w.num_q_heads * visible
-    return {
+    parity = None
+    if gpu_out is not None:
+        # the sampled requests are the batch's first ones, so their rows sit at the same offsets
+        gidx = torch.from_numpy(np.array([qo[r] + i for r, i in rows], dtype=np.int64))
+        got = gpu_out[gidx.to(gpu_out.device)].float().cpu().numpy().astype(np.float64)
+        err = np.abs(got - ref)
+        parity = {"rows": int(len(rows)), "max_abs_err": float(err.max()), "mean_abs_err": float(err.mean()),
+                  "rel_rms_err": float(np.sqrt((err ** 2).mean()) / max(np.sqrt((ref ** 2).mean()), 1e-300)),
+                  "gate": "max <= 2e-2, mean <= 2e-3 (fp64 oracle)",
+                  "pass": bool(err.max() <= 2e-2 and err.mean() <= 2e-3)}
+    return parity, {
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
         "cores": used,
@@ -232,7 +246,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="llama8b", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--config", default="wide70b", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--rope", action="store_true",
                     help="the step's store also RMS-normalises and rotates Q and K (store_kv_rope)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -266,7 +280,10 @@ def main():
         print(json.dumps({"calib_copy_bytes_read": 4 * n, "calib_copy_bytes_written": 4 * n, "launches": 3}))
         return
 
-    w, ms_step, store_ms, attn_ms = run_gpu(args.config, args.steps, args.warmup, args.rope)
+    w, ms_step, store_t, attn_t, gpu_out = run_gpu(args.config, args.steps, args.warmup, args.rope)
+    # the roofline entry takes the kernel's average launch time; medians are reported beside it
+    store_ms, attn_ms = float(store_t.mean()), float(attn_t.mean())
+    store_med, attn_med = float(np.median(store_t)), float(np.median(attn_t))
     flops = w.flops()
     T = w.total_extend
     tflops_step = flops / (ms_step * 1e-3) / 1e12
@@ -304,11 +321,17 @@ def main():
         "pct_bf16_peak": round(100.0 * tflops_step / PEAK_BF16_TFLOPS, 2),
         "uncached_tokens_per_s": round(T / (ms_step * 1e-3), 1),
         "attn_ms": round(attn_ms, 4),
+        "attn_ms_median": round(attn_med, 4),
+        "attn_ms_min_max": [round(float(attn_t.min()), 4), round(float(attn_t.max()), 4)],
         "attn_tflops": round(tflops_attn, 2),
-        "uncached_tokens_per_s_attn_only": round(T / (attn_ms * 1e-3), 1),
+        "attn_tflops_median": round(flops / (attn_med * 1e-3) / 1e12, 2),
+        "pct_bf16_peak_attn_median": round(100.0 * flops / (attn_med * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+        "uncached_tokens_per_s_attn_only": round(T / (attn_med * 1e-3), 1),
         "store_kernel": "store_kv_rope_kernel" if args.rope else "store_kv_kernel",
         "store_ms": round(store_ms, 4),
-        "store_GBps": round(store_bytes / (store_ms * 1e-3) / 1e9, 1),
+        "store_ms_median": round(store_med, 4),
+        "store_GBps": round(store_bytes / (store_med * 1e-3) / 1e9, 1),
+        "store_roofline_frac": round(store_bytes / (store_med * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
         "roofline": {
             "kernel": "extend_attn_kernel",
             "bound": "mfma",
@@ -326,9 +349,13 @@ def main():
         gbps = attn_alg_bytes / (attn_ms * 1e-3) / 1e9
         result["roofline"].update({"kernel": "decode_kernel", "bound": "hbm", "achieved": round(gbps, 1),
                                    "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4)})
+    if traffic is not None:
+        result["roofline"]["traffic_GBps"] = round(traffic / (attn_ms * 1e-3) / 1e9, 1)
+        result["roofline"]["traffic_over_algorithmic"] = round(traffic / attn_alg_bytes, 2)
     if not args.no_cpu_baseline:
-        cb = run_cpu_baseline(args.config, args.cpu_rows, args.cpu_reqs)
+        parity, cb = run_cpu_baseline(args.config, args.cpu_rows, args.cpu_reqs, gpu_out)
         result["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v) for k, v in cb.items()}
+        result["parity"] = parity
     print(json.dumps(result), flush=True)
 
 

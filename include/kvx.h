@@ -29,7 +29,9 @@
  *   - Calls build their work plan on the host and upload it through a pinned
  *     staging buffer, waiting on the host for that buffer's previous copy, and
  *     may allocate device scratch the first time a size is seen: they are not
- *     meant to be captured into a HIP graph.
+ *     meant to be captured into a HIP graph.  Scratch grows with the
+ *     stream-ordered allocator (hipMallocAsync / hipFreeAsync): growing never
+ *     waits for the device on the host.
  *   - "host" pointers are ordinary CPU memory read during the call;
  *     "device" pointers are GPU memory (hipMalloc / torch CUDA tensors).
  *   - bf16 means IEEE binary32 truncated to its upper 16 bits (2 bytes).
@@ -95,9 +97,9 @@ typedef struct {
 } kvx_pool_layout;
 
 /*
- * Allocate a KV pool of `num_pages` pages of `page_size` tokens (the shared
- * cache pool of fixed-size pages, Section 2, "Modern serving systems manage
- * reusable KV tensors in a shared cache pool").
+ * Allocate a KV pool of `num_pages` pages of `page_size` tokens: the one pool of
+ * fixed-size pages from which every request's reusable KV is served (Section 2,
+ * on how serving systems keep cached KV).
  *   page_size     must be 16.
  *   num_kv_heads  >= 1.
  *   head_dim      64 or 128.
@@ -241,8 +243,8 @@ int store_kv_rope(kvx_pool *pool, const kvx_batch *batch, const kvx_rope *rope, 
  * A decode step -- every request has at most one suffix token, and at most 16
  * query heads share a KV head -- runs a dedicated decode kernel (key chunks of
  * each request and KV head streamed from HBM); the result is the same operation.
- * Uses a library-owned device workspace (grown with hipMalloc when a batch needs
- * more than any earlier one).  Errors: EINVAL, EUNSUPPORTED, ERANGE (validation
+ * Uses a library-owned device workspace (grown with hipMallocAsync when a batch
+ * needs more than any earlier one; at most 2 GiB of partial results).  Errors: EINVAL, EUNSUPPORTED, ERANGE (validation
  * mode), ENOMEM, EHIP.  R = 0 or T = 0: no-op.
  */
 int extend_attention(kvx_pool *pool, const kvx_batch *batch, const void *q, int32_t num_q_heads,
@@ -272,17 +274,21 @@ typedef struct {
  * every (request, KV head), longest first (tok_count 1).  Writes at most `cap` items to
  * `items` (may be NULL) and the total count to *count.
  *   num_kv_heads, num_q_heads, head_dim as for extend_attention.
+ *   split_keys   as set by kv_pool_set_split_keys (0 = automatic).
  * Errors: EINVAL, EUNSUPPORTED.
  */
 int extend_attention_plan(const kvx_batch *batch, int32_t num_q_heads, int32_t num_kv_heads,
-                          int32_t head_dim, kvx_work_item *items, int64_t cap, int64_t *count);
+                          int32_t head_dim, int32_t split_keys, kvx_work_item *items, int64_t cap,
+                          int64_t *count);
 
 /*
- * Key-range split length for extend_attention (tokens, a multiple of 64, or 0 =
- * automatic, the default).  A non-zero value splits every key range longer
- * than it; used to exercise the split path.  Process-wide.  Errors: EINVAL.
+ * Key-range split length of extend_attention on this pool (tokens, a multiple
+ * of 64, or 0 = automatic, the default).  A non-zero value splits every key
+ * range longer than it (a decode step: chunks of that many keys); used to
+ * exercise the split path.  A setting of the pool: takes effect for calls queued
+ * after it, from the pool's one host thread.  Errors: EINVAL.
  */
-int kvx_set_split_keys(int32_t keys);
+int kv_pool_set_split_keys(kvx_pool *pool, int32_t keys);
 
 /* Message describing the last non-OK status on this thread ("" if none). */
 const char *kvx_last_error(void);

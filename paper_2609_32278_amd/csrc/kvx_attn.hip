@@ -520,8 +520,9 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   __syncthreads();  // every wave has read K(0) before iteration 0 refills its slot with K(4)
 
   // One pipelined iteration: consumes S(t) (scores in s_cur, maximum in mx), produces
-  // S(t+1) into s_nxt with its maximum, accumulates P(t) V(t).  Issues K(t+3) and
-  // V(t+2) into the ring and waits for K(t+2) and V(t+1), issued one iteration ago.
+  // S(t+1) into s_nxt with its maximum, accumulates P(t) V(t).  Issues K(t+4) and
+  // V(t+3) into the ring and, before its barrier, waits for K(t+2) and V(t+1),
+  // which were issued two iterations earlier.
   // In the unmasked variant tile t+1 exists and needs no mask, so the compute part
   // is one branch-free block in which MFMA and the softmax VALU work interleave.
   // lazy rescale before the scores of the tile whose maximum is mx are exponentiated:

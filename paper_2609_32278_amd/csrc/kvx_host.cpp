@@ -63,30 +63,38 @@ bool validate_mode() {
   return v != nullptr && v[0] != '\0' && v[0] != '0';
 }
 
-// Pinned host buffer + device buffer + event: a reusable upload channel.  The host
-// side is rewritten only after the previous copy out of it has completed.
+// Pinned host buffer + device buffer + events: a reusable upload channel.  The
+// host side is rewritten only after the previous copy out of it has completed.
+// The device buffer grows with the stream-ordered allocator: the old buffer is
+// freed in stream order behind `used` (recorded after the last kernels that read
+// it), so growing never waits on the host for the device.
 struct Staging {
   void* host = nullptr;
   size_t host_cap = 0;
   void* dev = nullptr;
   size_t dev_cap = 0;
-  hipEvent_t ev = nullptr;
+  hipEvent_t ev = nullptr;    // after the last copy out of `host`
+  hipEvent_t used = nullptr;  // after the last kernels that read `dev`
   bool pending = false;
 
+  // Only after the device has gone idle (pool destruction).
   void release() {
     if (ev) {
       (void)hipEventSynchronize(ev);
       (void)hipEventDestroy(ev);
     }
+    if (used) (void)hipEventDestroy(used);
     if (host) (void)hipHostFree(host);
-    if (dev) (void)hipFree(dev);
+    if (dev) (void)hipFreeAsync(dev, nullptr);
     *this = Staging();
   }
 
   // Copy `bytes` from `src` to device memory ordered on `stream`; *out receives the
   // device address (valid until the next upload on this channel is ordered after it).
+  // The caller records done() on the stream after the kernels that read it.
   int upload(const void* src, size_t bytes, hipStream_t stream, void** out) {
     if (!ev) KVX_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+    if (!used) KVX_HIP(hipEventCreateWithFlags(&used, hipEventDisableTiming));
     if (pending) {
       KVX_HIP(hipEventSynchronize(ev));
       pending = false;
@@ -99,14 +107,15 @@ struct Staging {
       host_cap = cap;
     }
     if (bytes > dev_cap) {
-      // earlier kernels on any stream may still read the old buffer
       if (dev) {
-        KVX_HIP(hipDeviceSynchronize());
-        KVX_HIP(hipFree(dev));
+        // earlier kernels (on any stream) that read the old buffer precede `used`
+        KVX_HIP(hipStreamWaitEvent(stream, used, 0));
+        KVX_HIP(hipFreeAsync(dev, stream));
       }
       dev = nullptr;
+      dev_cap = 0;
       size_t cap = std::max<size_t>(bytes + bytes / 2, 4096);
-      KVX_HIP(hipMalloc(&dev, cap));
+      KVX_HIP(hipMallocAsync(&dev, cap, stream));
       dev_cap = cap;
     }
     std::memcpy(host, src, bytes);
@@ -116,35 +125,51 @@ struct Staging {
     *out = dev;
     return KVX_OK;
   }
+
+  int done(hipStream_t stream) {
+    KVX_HIP(hipEventRecord(used, stream));
+    return KVX_OK;
+  }
 };
 
-// Device scratch that only grows.
+// Device scratch that only grows, with the same stream-ordered replacement.
 struct Workspace {
   void* ptr = nullptr;
   size_t cap = 0;
-  int ensure(size_t bytes) {
+  hipEvent_t used = nullptr;  // after the last kernels that used `ptr`
+  int ensure(size_t bytes, hipStream_t stream) {
+    if (!used) KVX_HIP(hipEventCreateWithFlags(&used, hipEventDisableTiming));
     if (bytes <= cap) return KVX_OK;
     if (ptr) {
-      KVX_HIP(hipDeviceSynchronize());
-      KVX_HIP(hipFree(ptr));
+      KVX_HIP(hipStreamWaitEvent(stream, used, 0));
+      KVX_HIP(hipFreeAsync(ptr, stream));
       ptr = nullptr;
       cap = 0;
     }
-    size_t c = std::max<size_t>(bytes + bytes / 4, 1 << 20);
-    KVX_HIP(hipMalloc(&ptr, c));
+    // headroom of a quarter for small sizes; past 1 GiB exactly what is asked
+    size_t c = bytes > ((size_t)1 << 30) ? bytes : std::max<size_t>(bytes + bytes / 4, 1 << 20);
+    KVX_HIP(hipMallocAsync(&ptr, c, stream));
     cap = c;
     return KVX_OK;
   }
+  int done(hipStream_t stream) {
+    if (used) KVX_HIP(hipEventRecord(used, stream));
+    return KVX_OK;
+  }
+  // Only after the device has gone idle (pool destruction).
   void release() {
-    if (ptr) (void)hipFree(ptr);
+    if (ptr) (void)hipFreeAsync(ptr, nullptr);
+    if (used) (void)hipEventDestroy(used);
     ptr = nullptr;
     cap = 0;
+    used = nullptr;
   }
 };
 
-constexpr int kPlanSlots = 256;       // 256 CUs x 1 resident attention workgroup
-constexpr int64_t kMaxParts = 32768;  // bound on split partial results (2 GiB at head_dim 128)
-int32_t g_split_keys = 0;             // 0 = automatic
+constexpr int kPlanSlots = 256;  // 256 CUs x 1 resident attention workgroup
+// Bound on the partial results of split key ranges: 16384 parts x 256 rows x 128
+// dims x 4 B = 2 GiB (+16 MiB of LSE) at head_dim 128, allocated exactly.
+constexpr int64_t kMaxParts = 16384;
 
 }  // namespace
 
@@ -161,6 +186,7 @@ struct kvx_pool {
   float* scales_d = nullptr;  // [k_scale | v_scale | k_inv | v_inv], each num_kv_heads
   Staging st_store, st_attn, st_io, st_move;
   Workspace parts;
+  int32_t split_keys = 0;  // key-range split length of extend_attention; 0 = automatic
 };
 
 namespace {
@@ -242,7 +268,8 @@ struct Plan {
 //     head count is a multiple of 8, else greedy by cost), so the workgroups that
 //     stream the same K/V pages share one L2;
 //   * within an XCD, requests go longest first and a request's tiles longest first.
-int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, int32_t Hkv, Plan& plan) {
+int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, int32_t Hkv, int32_t split_keys,
+              int64_t max_parts, Plan& plan) {
   const int G = Hq / Hkv;
   const int tile_tok = kvx::kTileRows / G;
   const int BN = kvx::kTileKeys;
@@ -266,8 +293,8 @@ int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, in
 
   // split length in keys (a multiple of BN), 0 = no split
   int64_t split = 0;
-  if (g_split_keys > 0) {
-    split = g_split_keys;
+  if (split_keys > 0) {
+    split = split_keys;
   } else if (!tiles.empty()) {
     const int64_t avg = total_cost / kPlanSlots;            // tiles of keys per slot
     const int64_t allowed = std::max<int64_t>(avg / 2, 16);  // at least 1024 keys per part
@@ -281,7 +308,7 @@ int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, in
         const int64_t nb = t.qpos0 / split;  // boundaries split, 2 split, ... <= qpos0
         if (nb > 0) parts += nb + 1;
       }
-      if (parts <= kMaxParts) break;
+      if (parts <= max_parts) break;
       split *= 2;
     }
   }
@@ -414,14 +441,15 @@ bool is_decode_batch(const kvx_batch* b, int32_t Hq, int32_t Hkv) {
 // about 2048 chunks (8 per workgroup slot at two resident workgroups per CU), at
 // least 512 keys each; a range of more than one chunk becomes parts merged by
 // log-sum-exp.  Chunks are dispatched longest first.
-int make_decode_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hkv, DecodePlan& plan) {
+int make_decode_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hkv, int32_t split_keys,
+                     int64_t max_parts, DecodePlan& plan) {
   const int64_t A = kvx::kDecodeChunkAlign;
   int64_t total = 0;
   for (int r = 0; r < b->num_reqs; r++)
     if (b->extend_lens[r] == 1) total += (int64_t)Hkv * ((int64_t)b->prefix_lens[r] + 1);
   int64_t chunk;
-  if (g_split_keys > 0) {
-    chunk = g_split_keys;
+  if (split_keys > 0) {
+    chunk = split_keys;
   } else {
     chunk = std::max<int64_t>(512, (total + 2047) / 2048);
     chunk = (chunk + A - 1) / A * A;
@@ -433,7 +461,7 @@ int make_decode_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t
       const int64_t n = ((int64_t)b->prefix_lens[r] + 1 + chunk - 1) / chunk;
       if (n > 1) parts += n * Hkv;
     }
-    if (parts <= kMaxParts) break;
+    if (parts <= max_parts) break;
     chunk *= 2;
   }
   for (int r = 0; r < b->num_reqs; r++) {
@@ -480,11 +508,11 @@ int check_heads(int32_t Hq, int32_t Hkv, int32_t D) {
 int decode_attention(kvx_pool* pool, const kvx_batch* batch, const std::vector<int64_t>& qo, const void* q,
                      int32_t num_q_heads, float sm_scale, void* out, float* lse, hipStream_t s) {
   DecodePlan plan;
-  if (int rc = make_decode_plan(batch, qo, pool->num_kv_heads, plan)) return rc;
+  if (int rc = make_decode_plan(batch, qo, pool->num_kv_heads, pool->split_keys, kMaxParts, plan)) return rc;
   const int D = pool->head_dim;
   constexpr int R = kvx::kDecodeMaxGroup;
   if (plan.n_parts > 0)
-    if (int rc = pool->parts.ensure((size_t)plan.n_parts * R * (D + 1) * sizeof(float))) return rc;
+    if (int rc = pool->parts.ensure((size_t)plan.n_parts * R * (D + 1) * sizeof(float), s)) return rc;
   const size_t ub = plan.units.size() * sizeof(DecodeUnit), mb = plan.merges.size() * sizeof(DecodeMerge);
   std::vector<uint8_t> blob(ub + mb);
   if (ub) std::memcpy(blob.data(), plan.units.data(), ub);
@@ -521,7 +549,8 @@ int decode_attention(kvx_pool* pool, const kvx_batch* batch, const std::vector<i
     e = kvx::launch_decode_merge(m, (int64_t)plan.merges.size(), D, s);
     if (e != hipSuccess) return hip_fail(e, "decode merge kernel launch");
   }
-  return KVX_OK;
+  if (int rc = pool->st_attn.done(s)) return rc;
+  return pool->parts.done(s);
 }
 
 }  // namespace
@@ -530,10 +559,12 @@ extern "C" {
 
 const char* kvx_last_error(void) { return g_last_error.c_str(); }
 
-int kvx_set_split_keys(int32_t keys) {
+int kv_pool_set_split_keys(kvx_pool* pool, int32_t keys) {
+  g_last_error.clear();
+  if (int rc = check_pool(pool)) return rc;
   if (keys < 0 || keys % kvx::kTileKeys != 0)
     return fail(KVX_EINVAL, "split keys %d: must be 0 or a positive multiple of %d", keys, kvx::kTileKeys);
-  g_split_keys = keys;
+  pool->split_keys = keys;
   return KVX_OK;
 }
 
@@ -672,7 +703,7 @@ static int page_io(kvx_pool* pool, const int32_t* page_ids, int64_t n, void* k_l
   p.to_pool = to_pool;
   hipError_t e = kvx::launch_page_io(p, n, pool->head_dim, pool->elem_bytes, s);
   if (e != hipSuccess) return hip_fail(e, "page io kernel launch");
-  return KVX_OK;
+  return pool->st_io.done(s);
 }
 
 int kv_pool_write_pages(kvx_pool* pool, const int32_t* page_ids, int64_t n, const void* k_src, const void* v_src,
@@ -745,7 +776,7 @@ static int page_move(kvx_pool* pool, const int32_t* page_ids, const int32_t* slo
   p.to_host = to_host;
   hipError_t e = kvx::launch_page_move(p, n, s);
   if (e != hipSuccess) return hip_fail(e, "page move kernel launch");
-  return KVX_OK;
+  return pool->st_move.done(s);
 }
 
 int kv_pool_spill(const kvx_pool* pool, const int32_t* page_ids, const int32_t* slots, int64_t n, void* host,
@@ -802,7 +833,7 @@ int store_kv(kvx_pool* pool, const kvx_batch* batch, const void* k_ext, const vo
   p.num_kv_heads = pool->num_kv_heads;
   hipError_t e = kvx::launch_store_kv(p, (int64_t)units.size(), pool->head_dim, pool->kv_dtype == KVX_KV_FP8_E4M3, s);
   if (e != hipSuccess) return hip_fail(e, "store_kv kernel launch");
-  return KVX_OK;
+  return pool->st_store.done(s);
 }
 
 int store_kv_rope(kvx_pool* pool, const kvx_batch* batch, const kvx_rope* rope, const void* q, int32_t num_q_heads,
@@ -886,15 +917,17 @@ int store_kv_rope(kvx_pool* pool, const kvx_batch* batch, const kvx_rope* rope, 
   hipError_t e = kvx::launch_store_kv_rope(p, (int64_t)units.size(), D, pool->kv_dtype == KVX_KV_FP8_E4M3,
                                            rope->style == KVX_ROPE_INTERLEAVED, s);
   if (e != hipSuccess) return hip_fail(e, "store_kv_rope kernel launch");
-  return KVX_OK;
+  return pool->st_store.done(s);
 }
 
 int extend_attention_plan(const kvx_batch* batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                          kvx_work_item* items, int64_t cap, int64_t* count) {
+                          int32_t split_keys, kvx_work_item* items, int64_t cap, int64_t* count) {
   g_last_error.clear();
   if (count == nullptr) return fail(KVX_EINVAL, "count is NULL");
   *count = 0;
   if (int rc = check_heads(num_q_heads, num_kv_heads, head_dim)) return rc;
+  if (split_keys < 0 || split_keys % kvx::kTileKeys != 0)
+    return fail(KVX_EINVAL, "split keys %d: must be 0 or a positive multiple of %d", split_keys, kvx::kTileKeys);
   std::vector<int64_t> qo;
   if (int rc = check_batch(batch, qo, false)) return rc;
   if (cap < 0) return fail(KVX_EINVAL, "cap < 0");
@@ -902,11 +935,11 @@ int extend_attention_plan(const kvx_batch* batch, int32_t num_q_heads, int32_t n
   if (qo.back() > 0) {
     if (is_decode_batch(batch, num_q_heads, num_kv_heads)) {
       DecodePlan dp;
-      if (int rc = make_decode_plan(batch, qo, num_kv_heads, dp)) return rc;
+      if (int rc = make_decode_plan(batch, qo, num_kv_heads, split_keys, kMaxParts, dp)) return rc;
       out_items = std::move(dp.items);
     } else {
       Plan plan;
-      if (int rc = make_plan(batch, qo, num_q_heads, num_kv_heads, plan)) return rc;
+      if (int rc = make_plan(batch, qo, num_q_heads, num_kv_heads, split_keys, kMaxParts, plan)) return rc;
       out_items = std::move(plan.items);
     }
   }
@@ -940,12 +973,12 @@ int extend_attention(kvx_pool* pool, const kvx_batch* batch, const void* q, int3
     return decode_attention(pool, batch, qo, q, num_q_heads, sm_scale, out, lse, s);
 
   Plan plan;
-  if (int rc = make_plan(batch, qo, num_q_heads, pool->num_kv_heads, plan)) return rc;
+  if (int rc = make_plan(batch, qo, num_q_heads, pool->num_kv_heads, pool->split_keys, kMaxParts, plan)) return rc;
   const int D = pool->head_dim;
   if (plan.n_parts > 0) {
     const size_t obytes = (size_t)plan.n_parts * kvx::kTileRows * D * sizeof(float);
     const size_t lbytes = (size_t)plan.n_parts * kvx::kTileRows * sizeof(float);
-    if (int rc = pool->parts.ensure(obytes + lbytes)) return rc;
+    if (int rc = pool->parts.ensure(obytes + lbytes, s)) return rc;
   }
   // one upload: units, then merges
   const size_t ub = plan.units.size() * sizeof(AttnUnit), mb = plan.merges.size() * sizeof(MergeUnit);
@@ -986,7 +1019,8 @@ int extend_attention(kvx_pool* pool, const kvx_batch* batch, const void* q, int3
     e = kvx::launch_merge(m, (int64_t)plan.merges.size(), D, s);
     if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
   }
-  return KVX_OK;
+  if (int rc = pool->st_attn.done(s)) return rc;
+  return pool->parts.done(s);
 }
 
 }  // extern "C"

@@ -29,7 +29,7 @@ KVX_ROPE_HALF, KVX_ROPE_INTERLEAVED = 0, 1
 # Every symbol include/kvx.h and include/kvx_cache.h declare.
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_layout", "kv_pool_write_pages",
            "kv_pool_read_pages", "kv_pool_record_bytes", "kv_pool_spill", "kv_pool_reload", "store_kv", "store_kv_rope", "extend_attention", "extend_attention_plan",
-           "kvx_set_split_keys", "kvx_last_error",
+           "kv_pool_set_split_keys", "kvx_last_error",
            "kvx_cache_create", "kvx_cache_create_tiered", "kvx_cache_set_recency_tiers", "kvx_cache_destroy", "kvx_cache_begin_turn",
            "kvx_cache_begin_turn_tiered", "kvx_cache_end_turn", "kvx_cache_complete", "kvx_cache_agent",
            "kvx_cache_agent_host", "kvx_cache_join", "kvx_cache_group", "kvx_cache_stats"]
@@ -112,8 +112,8 @@ def lib():
             "store_kv": [P, ctypes.POINTER(kvx_batch), P, P, P],
             "store_kv_rope": [P, ctypes.POINTER(kvx_batch), ctypes.POINTER(kvx_rope), P, i32, P, P, P, P],
             "extend_attention": [P, ctypes.POINTER(kvx_batch), P, i32, f32, P, P, P],
-            "extend_attention_plan": [ctypes.POINTER(kvx_batch), i32, i32, i32, P, i64, ctypes.POINTER(i64)],
-            "kvx_set_split_keys": [i32],
+            "extend_attention_plan": [ctypes.POINTER(kvx_batch), i32, i32, i32, i32, P, i64, ctypes.POINTER(i64)],
+            "kv_pool_set_split_keys": [P, i32],
             "kvx_cache_create": [i64, i32, i32, i32, ctypes.POINTER(P)],
             "kvx_cache_create_tiered": [i64, i64, i32, i32, i32, ctypes.POINTER(P)],
             "kvx_cache_set_recency_tiers": [P, i64],
@@ -334,19 +334,20 @@ def extend_attention(pool, batch: Batch, q, num_q_heads: int, sm_scale: float, o
                                   _dptr(out), _dptr(lse), _stream(stream)), "extend_attention")
 
 
-def extend_attention_plan(batch: Batch, num_q_heads: int, num_kv_heads: int, head_dim: int) -> np.ndarray:
+def extend_attention_plan(batch: Batch, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                          split_keys: int = 0) -> np.ndarray:
     count = ctypes.c_int64()
-    _check(lib().extend_attention_plan(ctypes.byref(batch.c), num_q_heads, num_kv_heads, head_dim, None, 0,
-                                       ctypes.byref(count)), "extend_attention_plan")
+    _check(lib().extend_attention_plan(ctypes.byref(batch.c), num_q_heads, num_kv_heads, head_dim, int(split_keys),
+                                       None, 0, ctypes.byref(count)), "extend_attention_plan")
     items = np.zeros(count.value, dtype=WORK_ITEM_DTYPE)
-    _check(lib().extend_attention_plan(ctypes.byref(batch.c), num_q_heads, num_kv_heads, head_dim,
+    _check(lib().extend_attention_plan(ctypes.byref(batch.c), num_q_heads, num_kv_heads, head_dim, int(split_keys),
                                        items.ctypes.data, count.value, ctypes.byref(count)),
            "extend_attention_plan")
     return items
 
 
-def kvx_set_split_keys(keys: int) -> None:
-    _check(lib().kvx_set_split_keys(int(keys)), "kvx_set_split_keys")
+def kv_pool_set_split_keys(pool, keys: int) -> None:
+    _check(lib().kv_pool_set_split_keys(pool, int(keys)), "kv_pool_set_split_keys")
 
 
 # ------------------------------------------------------------------ prefix cache (include/kvx_cache.h)

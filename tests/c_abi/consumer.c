@@ -35,15 +35,15 @@ int main(void)
     b.extend_lens = extend;
     b.page_indptr = indptr;
     b.page_ids = NULL;
-    CHECK(extend_attention_plan(&b, 8, 2, 128, items, 64, &count) == KVX_OK);
+    CHECK(extend_attention_plan(&b, 8, 2, 128, 0, items, 64, &count) == KVX_OK);
     CHECK(count > 0 && count <= 64);
     for (i = 0; i < count; i++)
         if (items[i].req >= 0 && items[i].part < 0) rows += items[i].tok_count;
     CHECK(rows == 2 * (100 + 7)); /* every suffix token once per KV head */
 
-    CHECK(extend_attention_plan(&b, 6, 4, 128, NULL, 0, &count) == KVX_EINVAL);
+    CHECK(extend_attention_plan(&b, 6, 4, 128, 0, NULL, 0, &count) == KVX_EINVAL);
     CHECK(strlen(kvx_last_error()) > 0);
-    CHECK(extend_attention_plan(&b, 8, 2, 96, NULL, 0, &count) == KVX_EUNSUPPORTED);
+    CHECK(extend_attention_plan(&b, 8, 2, 96, 0, NULL, 0, &count) == KVX_EUNSUPPORTED);
 
     CHECK(kvx_cache_create(16, 16, 64, KVX_EVICT_RR, &cache) == KVX_OK);
     CHECK(kvx_cache_begin_turn(cache, 7, 50, &pre, table, 8) == KVX_OK);

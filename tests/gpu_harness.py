@@ -31,10 +31,12 @@ class GpuRun:
     """Pool + batch of one workload on the GPU; the cached prefixes are written by
     store_kv of the history turn, request by request."""
 
-    def __init__(self, w: wl.Workload, fill_bits: int | None = None, overrides=None):
+    def __init__(self, w: wl.Workload, fill_bits: int | None = None, overrides=None, split_keys: int = 0):
         self.w = w
         self.pool = kvx.kv_pool_create(w.num_pages, w.page_size, w.num_kv_heads, w.head_dim, w.kv_dtype,
                                        w.k_scale, w.v_scale)
+        if split_keys:
+            kvx.kv_pool_set_split_keys(self.pool, split_keys)
         if fill_bits is not None:
             self.fill_pool(fill_bits)
         self.batch, self._ids = fresh_batch(w, w.page_ids, w.prefix_lens, w.extend_lens, w.page_indptr)

@@ -63,12 +63,11 @@ void one(bool decode_like) {
   kvx_batch b{R, P.data(), E.data(), indptr.data(), nullptr};
   const int32_t splits[] = {0, 0, 64, 1024, 16384};
   const int32_t split = splits[uni(0, 4)];
-  CHECK(kvx_set_split_keys(split) == KVX_OK);
   int64_t count = -1;
-  CHECK(extend_attention_plan(&b, hkv * g, hkv, D, nullptr, 0, &count) == KVX_OK);
+  CHECK(extend_attention_plan(&b, hkv * g, hkv, D, split, nullptr, 0, &count) == KVX_OK);
   std::vector<kvx_work_item> items((size_t)count + 1);
   int64_t count2 = -1;
-  CHECK(extend_attention_plan(&b, hkv * g, hkv, D, items.data(), count, &count2) == KVX_OK);
+  CHECK(extend_attention_plan(&b, hkv * g, hkv, D, split, items.data(), count, &count2) == KVX_OK);
   CHECK(count2 == count);
   items.resize((size_t)count);
   // (req, head, tok_begin) -> key ranges
@@ -124,17 +123,17 @@ int main(int argc, char** argv) {
   int32_t P[1] = {-1}, E[1] = {4}, ip[2] = {0, 1};
   kvx_batch b{1, P, E, ip, nullptr};
   int64_t count = 0;
-  CHECK(extend_attention_plan(&b, 4, 2, 128, nullptr, 0, &count) == KVX_EINVAL);
+  CHECK(extend_attention_plan(&b, 4, 2, 128, 0, nullptr, 0, &count) == KVX_EINVAL);
   P[0] = 16;
   E[0] = 17;
   ip[1] = 2;
-  CHECK(extend_attention_plan(&b, 4, 2, 128, nullptr, 0, &count) == KVX_EINVAL);
+  CHECK(extend_attention_plan(&b, 4, 2, 128, 0, nullptr, 0, &count) == KVX_EINVAL);
   P[0] = 0;
   E[0] = 4;
   ip[0] = 1;
   ip[1] = 2;
-  CHECK(extend_attention_plan(&b, 4, 2, 128, nullptr, 0, &count) == KVX_EINVAL);
-  CHECK(kvx_set_split_keys(0) == KVX_OK);
+  CHECK(extend_attention_plan(&b, 4, 2, 128, 0, nullptr, 0, &count) == KVX_EINVAL);
+  CHECK(extend_attention_plan(&b, 4, 2, 128, 100, nullptr, 0, &count) == KVX_EINVAL);  // not a multiple of 64
   std::printf("planner stress: %d batches passed\n", n);
   return 0;
 }

@@ -57,7 +57,7 @@ def test_pool_argument_errors():
     assert _err(kvx.kv_pool_create, 10, 16, 2, 64, kvx.KVX_KV_FP8_E4M3) == kvx.KVX_EUNSUPPORTED
     assert _err(kvx.kv_pool_create, 10, 16, 2, 64, kvx.KVX_KV_FP8_E4M3, [1.0, 0.0], [1.0, 1.0]) == kvx.KVX_EINVAL
     assert _err(kvx.kv_pool_create, 10, 16, 2, 64, 7) == kvx.KVX_EINVAL
-    assert _err(kvx.kvx_set_split_keys, 100) == kvx.KVX_EINVAL
+    assert _err(kvx.kv_pool_set_split_keys, None, 64) == kvx.KVX_EINVAL
     assert _err(kvx.kv_pool_layout, None) == kvx.KVX_EINVAL
 
 
@@ -76,6 +76,9 @@ def test_hot_path_argument_errors_before_any_device_work():
     assert _err(kvx.extend_attention_plan, neg, 4, 2, 128) == kvx.KVX_EINVAL
     bad0 = kvx.Batch([0], [4], [1, 2], 0x1000)
     assert _err(kvx.extend_attention_plan, bad0, 4, 2, 128) == kvx.KVX_EINVAL
+    ok = kvx.Batch([16], [4], [0, 2], 0x1000)
+    assert _err(kvx.extend_attention_plan, ok, 4, 2, 128, 100) == kvx.KVX_EINVAL  # split not a multiple of 64
+    assert _err(kvx.extend_attention_plan, ok, 4, 2, 128, -64) == kvx.KVX_EINVAL
 
 
 def test_binding_rejects_short_buffers_and_ragged_lengths():
@@ -94,12 +97,8 @@ def test_binding_rejects_short_buffers_and_ragged_lengths():
 
 
 def _check_plan(w, split=0):
-    kvx.kvx_set_split_keys(split)
-    try:
-        b = kvx.Batch(w.prefix_lens, w.extend_lens, w.page_indptr, 0)
-        items = kvx.extend_attention_plan(b, w.num_q_heads, w.num_kv_heads, w.head_dim)
-    finally:
-        kvx.kvx_set_split_keys(0)
+    b = kvx.Batch(w.prefix_lens, w.extend_lens, w.page_indptr, 0)
+    items = kvx.extend_attention_plan(b, w.num_q_heads, w.num_kv_heads, w.head_dim, split)
     g = w.group
     tile_tok = TILE_ROWS // g
     real = items[items["req"] >= 0]

@@ -21,10 +21,10 @@ pytestmark = pytest.mark.gpu
 # name -> (requests sampled, rows per request)
 SAMPLING = {
     "llama8b": (16, 16),
-    "tail_outlier": (4, 8),
-    "rr_partial": (6, 6),
-    "wide70b": (4, 6),
-    "wide70b_fp8": (4, 6),
+    "tail_outlier": (32, 16),
+    "rr_partial": (8, 8),
+    "wide70b": (8, 8),
+    "wide70b_fp8": (8, 8),
     # decode steps (one row per request; the planner splits every long key range)
     "decode_llama8b": (32, 1),
     "decode_long": (12, 1),

@@ -18,10 +18,10 @@ def _f64(t):
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
-def _run_and_compare(w, tag, want_lse=False, fill=None):
+def _run_and_compare(w, tag, want_lse=False, fill=None, split_keys=0):
     print(f"[extend] {tag}: R={w.num_reqs} T={w.total_extend} Hq={w.num_q_heads} Hkv={w.num_kv_heads} "
-          f"d={w.head_dim} fp8={w.kv_dtype}", flush=True)
-    run = GpuRun(w, fill_bits=fill)
+          f"d={w.head_dim} fp8={w.kv_dtype} split={split_keys}", flush=True)
+    run = GpuRun(w, fill_bits=fill, split_keys=split_keys)
     try:
         run.store()
         res = run.attend(want_lse=want_lse)
@@ -85,11 +85,7 @@ def test_sharpened_queries():
 @pytest.mark.parametrize("split", [64, 128, 1024])
 def test_forced_key_split_matches_oracle(split):
     w = wl.make_custom([3000, 129, 0], [70, 200, 300], 8, 2, 128, seed=10)
-    kvx.kvx_set_split_keys(split)
-    try:
-        _run_and_compare(w, f"split{split}", want_lse=True)
-    finally:
-        kvx.kvx_set_split_keys(0)
+    _run_and_compare(w, f"split{split}", want_lse=True, split_keys=split)
 
 
 def test_single_key_returns_value_bits():
@@ -181,18 +177,22 @@ def test_needle_key_dominates(where):
         run.close()
 
 
-def test_split_invariance_across_page_boundaries():
+@pytest.mark.parametrize("kv_dtype", [wl.KV_BF16, wl.KV_FP8_E4M3])
+def test_split_invariance_across_page_boundaries(kv_dtype):
     """One logical sequence, cut into cached prefix + suffix at several page
-    boundaries: the rows past the last cut agree with each other within the gate."""
+    boundaries: the rows past the last cut agree with each other within the gate.
+    On an fp8 pool the suffix is read back dequantised like the prefix, so the cut
+    does not change what any row sees either (one set of per-head scales)."""
     total, hq, hkv, d = 700, 8, 2, 128
-    base = wl.make_custom([0], [total], hq, hkv, d, seed=13)
+    base = wl.make_custom([0], [total], hq, hkv, d, seed=13, kv_dtype=kv_dtype)
     q_all = wl.request_q(base, 0, DEV)
     k_all, v_all = wl.request_kv(base, 0, DEV)
     cuts = [0, 16, 320, 640]
     rows = []
     for cut in cuts:
-        w = wl.make_custom([cut], [total - cut], hq, hkv, d, seed=13 + cut)
-        print(f"[extend] cut {cut}", flush=True)
+        w = wl.make_custom([cut], [total - cut], hq, hkv, d, seed=13 + cut, kv_dtype=kv_dtype,
+                           k_scale=base.k_scale, v_scale=base.v_scale)
+        print(f"[extend] cut {cut} fp8={kv_dtype}", flush=True)
         run = GpuRun(w, overrides={"kv": lambda r: (k_all, v_all), "q": lambda r: q_all[cut:]})
         try:
             run.store()
@@ -290,8 +290,4 @@ def test_seeded_random_batches(seed):
     w = wl.make_custom(prefix, extend, hkv * g, hkv, d, kv_dtype=dt, seed=100 + seed)
     print(f"[random] seed={seed} P={prefix} E={extend} Hq={hkv * g} Hkv={hkv} d={d} fp8={dt} split={split}",
           flush=True)
-    kvx.kvx_set_split_keys(split)
-    try:
-        _run_and_compare(w, f"random{seed}", want_lse=True)
-    finally:
-        kvx.kvx_set_split_keys(0)
+    _run_and_compare(w, f"random{seed}", want_lse=True, split_keys=split)

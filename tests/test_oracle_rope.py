@@ -198,6 +198,70 @@ def test_value_store_equals_bit_store_on_bf16_values(kv_dtype):
     assert np.array_equal(pools[0].k, pools[1].k) and np.array_equal(pools[0].v, pools[1].v)
 
 
+def _e4m3_codes_f32(vals, inv):
+    """torch's float8_e4m3fn cast of float32(float32(x) * inv[h]), pre-clamped to +-448."""
+    y = torch.from_numpy(np.asarray(vals, np.float64).astype(np.float32)) * torch.from_numpy(inv)[None, :, None]
+    return y.clamp(-448.0, 448.0).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+
+
+def _e4m3_codes_f64(vals, inv):
+    """The same code with the product taken in double and rounded to float32 once."""
+    y = torch.from_numpy(np.asarray(vals, np.float64) * inv.astype(np.float64)[None, :, None])
+    return y.clamp(-448.0, 448.0).to(torch.float32).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+
+
+def test_fp8_value_store_matches_torch_cast_on_non_bf16_values():
+    """The fp8 branch of the value store on doubles that are not bf16 values (the
+    rotated keys of the fused store): each stored code must equal torch's
+    float8_e4m3fn cast of float32(float32(x) * float32(1/scale)), pre-clamped to
+    +-448 (the store's fp8 reading), placed through the page table.  Two plausible
+    mistakes must each change some code: rounding x to bf16 before quantising,
+    and scaling in double before the one rounding to float32."""
+    rng = np.random.default_rng(21)
+    P, E = [0, 21, 48], [30, 5, 17]
+    T, H, d = sum(E), 2, 64
+    indptr = np.array([0, 2, 4, 9])
+    ids = rng.permutation(12)[:9].astype(np.int32)
+    k_scale = np.array([0.03, 0.07], np.float32)
+    inv = (np.float32(1.0) / k_scale).astype(np.float32)
+    kd = rng.standard_normal((T, H, d)) * 2.0
+    kd[0, 0, :8] = [5.0, -5.0, 6.0, -7.0, 1e-6, -3e-7, 0.0, 4.6]  # saturating and subnormal codes
+    # keys next to the e4m3 tie points 1.0625 and -2.625 (after scaling): the float32 and
+    # the double product land on opposite sides of the tie for some of them
+    cand = []
+    for tie in (1.0625, -2.625, 0.15625):
+        for h in range(H):
+            base = tie / float(inv[h])
+            for k in range(-400, 400):
+                x = base + k * 2.0 ** -34
+                a = _e4m3_codes_f32(np.full((1, H, 1), x), inv)[0, h, 0]
+                b = _e4m3_codes_f64(np.full((1, H, 1), x), inv)[0, h, 0]
+                if a != b:
+                    cand.append((h, x))
+                    break
+    assert len(cand) >= 4, "no value separates the float32 and double products"
+    for j, (h, x) in enumerate(cand):
+        kd[1 + j, h, 0] = x
+    vb = oracle.bf16_round(rng.standard_normal((T, H, d)))
+    pool = oracle.OraclePool(12, H, d, oracle.KV_FP8_E4M3, fill=0x33, k_scale=k_scale,
+                             v_scale=np.array([0.05, 0.03], np.float32))
+    oracle.store_kv_values(pool, P, E, indptr, ids, kd, vb)
+
+    want = _e4m3_codes_f32(kd, inv)
+    # the placement written out: token P+i of request r -> page ids[indptr[r] + (P+i)//16], slot (P+i)%16
+    got = np.empty_like(want)
+    row = 0
+    for r in range(3):
+        for i in range(E[r]):
+            t = P[r] + i
+            got[row] = pool.k[ids[indptr[r] + t // 16], :, t % 16, :]
+            row += 1
+    assert np.array_equal(got, want)
+    # planted mistakes: a bf16 detour, and the product taken in double
+    assert not np.array_equal(_e4m3_codes_f32(oracle.bf16_value(oracle.bf16_round(kd)), inv), want)
+    assert not np.array_equal(_e4m3_codes_f64(kd, inv), want)
+
+
 # ------------------------------------------------------------------ planted mistakes
 
 @pytest.mark.parametrize("mutant", [m for m in R.MUTANTS if m != "none"])
