@@ -250,6 +250,32 @@ int store_kv_rope(kvx_pool *pool, const kvx_batch *batch, const kvx_rope *rope, 
 int extend_attention(kvx_pool *pool, const kvx_batch *batch, const void *q, int32_t num_q_heads,
                      float sm_scale, void *out, float *lse, kvx_stream_t stream);
 
+/*
+ * extend_attention for callers that cannot allocate device memory during the
+ * call: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, operation, kernels and result as extend_attention
+ * (bit for bit when both split the key ranges alike), but the work plan and the
+ * partial results of split key ranges go into one fixed device array of the
+ * library instead of the pool's staging buffer and workspace; the call makes no
+ * device or pinned allocation (only host containers for the plan).  The plan is
+ * copied from pageable host memory (hipMemcpyAsync, staged before the call
+ * returns).
+ *   The array holds KVX_NOALLOC_PLAN_BYTES of plan (32 B per work item) and
+ *   KVX_NOALLOC_PARTS_BYTES of partial results; the planner splits key ranges
+ *   only into as many parts as fit.  A batch whose plan does not fit is refused
+ *   with EUNSUPPORTED on the host, before any device work.
+ *   Each GPU the library runs on holds its own copy of the array (64 MiB) from
+ *   the first call on it until the process ends.  Every call on one GPU shares
+ *   that copy, and each call leaves its plan and partial results in it: calls
+ *   that may overlap on one GPU (two streams, or two host threads) race and must
+ *   be ordered by the caller, even on different pools.
+ * Errors: EINVAL, EUNSUPPORTED, ERANGE (validation mode), EHIP.
+ */
+#define KVX_NOALLOC_PLAN_BYTES (8u << 20)
+#define KVX_NOALLOC_PARTS_BYTES (56u << 20)
+int extend_attention_noalloc(kvx_pool *pool, const kvx_batch *batch, const void *q, int32_t num_q_heads,
+                             float sm_scale, void *out, float *lse, kvx_stream_t stream);
+
 /* ---------------------------------------------------------- planning, tuning */
 
 /* One work item of extend_attention: a tile of suffix tokens of one request and

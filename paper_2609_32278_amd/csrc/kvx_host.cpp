@@ -505,20 +505,90 @@ int check_heads(int32_t Hq, int32_t Hkv, int32_t D) {
   return KVX_OK;
 }
 
+// Where one attention call keeps its plan and its partial results: the pool's
+// growable buffers, or the caller-independent fixed scratch of the allocation-free
+// entry point (plan region, then partial-result region).
+struct CallBuffers {
+  kvx_pool* pool;
+  const kvx::FixedScratch* fixed;
+  uint8_t* base = nullptr;  // fixed scratch on the pool's device (after bind())
+
+  // Bound on split parts of `per_part` bytes each.
+  int64_t max_parts(size_t per_part) const {
+    if (!fixed) return kMaxParts;
+    return std::min<int64_t>(kMaxParts, (int64_t)(fixed->parts_bytes / per_part));
+  }
+  // Host-only size check of the plan (before any device call).
+  int check_plan(size_t bytes) const {
+    if (fixed && bytes > fixed->plan_bytes)
+      return fail(KVX_EUNSUPPORTED, "work plan of %zu bytes exceeds the fixed scratch's %zu-byte plan region",
+                  bytes, fixed->plan_bytes);
+    return KVX_OK;
+  }
+  // With the pool's device current: the fixed scratch's address on it.
+  int bind() {
+    if (!fixed) return KVX_OK;
+    void* p = nullptr;
+    if (int rc = fixed->address(pool->device, &p)) return rc;
+    base = (uint8_t*)p;
+    return KVX_OK;
+  }
+  int parts(size_t bytes, hipStream_t s, float** out) {
+    if (fixed) {
+      if (bytes > fixed->parts_bytes)
+        return fail(KVX_EUNSUPPORTED, "partial results of %zu bytes exceed the fixed scratch's %zu bytes", bytes,
+                    fixed->parts_bytes);
+      *out = (float*)(base + fixed->plan_bytes);
+      return KVX_OK;
+    }
+    if (int rc = pool->parts.ensure(bytes, s)) return rc;
+    *out = (float*)pool->parts.ptr;
+    return KVX_OK;
+  }
+  int upload(const std::vector<uint8_t>& blob, hipStream_t s, void** out) {
+    if (fixed) {
+      // pageable source: the copy is staged before the call returns
+      KVX_HIP(hipMemcpyAsync(base, blob.data(), blob.size(), hipMemcpyHostToDevice, s));
+      *out = base;
+      return KVX_OK;
+    }
+    return pool->st_attn.upload(blob.data(), blob.size(), s, out);
+  }
+  int done(hipStream_t s) {
+    if (fixed) return KVX_OK;
+    if (int rc = pool->st_attn.done(s)) return rc;
+    return pool->parts.done(s);
+  }
+};
+
+template <typename U, typename M>
+std::vector<uint8_t> plan_blob(const std::vector<U>& units, const std::vector<M>& merges) {
+  const size_t ub = units.size() * sizeof(U), mb = merges.size() * sizeof(M);
+  std::vector<uint8_t> blob(ub + mb);
+  if (ub) std::memcpy(blob.data(), units.data(), ub);
+  if (mb) std::memcpy(blob.data() + ub, merges.data(), mb);
+  return blob;
+}
+
 int decode_attention(kvx_pool* pool, const kvx_batch* batch, const std::vector<int64_t>& qo, const void* q,
-                     int32_t num_q_heads, float sm_scale, void* out, float* lse, hipStream_t s) {
-  DecodePlan plan;
-  if (int rc = make_decode_plan(batch, qo, pool->num_kv_heads, pool->split_keys, kMaxParts, plan)) return rc;
+                     int32_t num_q_heads, float sm_scale, void* out, float* lse, hipStream_t s, CallBuffers& buf) {
   const int D = pool->head_dim;
   constexpr int R = kvx::kDecodeMaxGroup;
+  DecodePlan plan;
+  if (int rc = make_decode_plan(batch, qo, pool->num_kv_heads, pool->split_keys,
+                                buf.max_parts((size_t)R * (D + 1) * sizeof(float)), plan))
+    return rc;
+  const std::vector<uint8_t> blob = plan_blob(plan.units, plan.merges);
+  if (int rc = buf.check_plan(blob.size())) return rc;
+  if (int rc = use_device(pool)) return rc;
+  if (validate_mode())
+    if (int rc = check_page_ids(pool, batch, s)) return rc;
+  if (int rc = buf.bind()) return rc;
+  float* parts = nullptr;
   if (plan.n_parts > 0)
-    if (int rc = pool->parts.ensure((size_t)plan.n_parts * R * (D + 1) * sizeof(float), s)) return rc;
-  const size_t ub = plan.units.size() * sizeof(DecodeUnit), mb = plan.merges.size() * sizeof(DecodeMerge);
-  std::vector<uint8_t> blob(ub + mb);
-  if (ub) std::memcpy(blob.data(), plan.units.data(), ub);
-  if (mb) std::memcpy(blob.data() + ub, plan.merges.data(), mb);
+    if (int rc = buf.parts((size_t)plan.n_parts * R * (D + 1) * sizeof(float), s, &parts)) return rc;
   void* dev = nullptr;
-  if (int rc = pool->st_attn.upload(blob.data(), blob.size(), s, &dev)) return rc;
+  if (int rc = buf.upload(blob, s, &dev)) return rc;
   kvx::DecodeParams p;
   p.q = (const uint16_t*)q;
   p.out = (uint16_t*)out;
@@ -527,8 +597,8 @@ int decode_attention(kvx_pool* pool, const kvx_batch* batch, const std::vector<i
   p.v_pool = pool->v;
   p.page_ids = batch->page_ids;
   p.units = (const DecodeUnit*)dev;
-  p.o_part = plan.n_parts ? (float*)pool->parts.ptr : nullptr;
-  p.lse_part = plan.n_parts ? (float*)pool->parts.ptr + (size_t)plan.n_parts * R * D : nullptr;
+  p.o_part = plan.n_parts ? parts : nullptr;
+  p.lse_part = plan.n_parts ? parts + (size_t)plan.n_parts * R * D : nullptr;
   p.k_scale = pool->scales_d;
   p.v_scale = pool->scales_d ? pool->scales_d + pool->num_kv_heads : nullptr;
   p.num_q_heads = num_q_heads;
@@ -539,7 +609,7 @@ int decode_attention(kvx_pool* pool, const kvx_batch* batch, const std::vector<i
   if (e != hipSuccess) return hip_fail(e, "decode kernel launch");
   if (!plan.merges.empty()) {
     kvx::DecodeMergeParams m;
-    m.merges = (const DecodeMerge*)((const uint8_t*)dev + ub);
+    m.merges = (const DecodeMerge*)((const uint8_t*)dev + plan.units.size() * sizeof(DecodeUnit));
     m.o_part = p.o_part;
     m.lse_part = p.lse_part;
     m.out = (uint16_t*)out;
@@ -549,8 +619,7 @@ int decode_attention(kvx_pool* pool, const kvx_batch* batch, const std::vector<i
     e = kvx::launch_decode_merge(m, (int64_t)plan.merges.size(), D, s);
     if (e != hipSuccess) return hip_fail(e, "decode merge kernel launch");
   }
-  if (int rc = pool->st_attn.done(s)) return rc;
-  return pool->parts.done(s);
+  return buf.done(s);
 }
 
 }  // namespace
@@ -953,6 +1022,13 @@ int extend_attention_plan(const kvx_batch* batch, int32_t num_q_heads, int32_t n
 
 int extend_attention(kvx_pool* pool, const kvx_batch* batch, const void* q, int32_t num_q_heads, float sm_scale,
                      void* out, float* lse, kvx_stream_t stream) {
+  return kvx::attention_call(pool, batch, q, num_q_heads, sm_scale, out, lse, stream, nullptr);
+}
+
+}  // extern "C"
+
+int kvx::attention_call(kvx_pool* pool, const kvx_batch* batch, const void* q, int32_t num_q_heads, float sm_scale,
+                        void* out, float* lse, kvx_stream_t stream, const FixedScratch* fixed) {
   g_last_error.clear();
   if (int rc = check_pool(pool)) return rc;
   if (int rc = check_heads(num_q_heads, pool->num_kv_heads, pool->head_dim)) return rc;
@@ -964,29 +1040,30 @@ int extend_attention(kvx_pool* pool, const kvx_batch* batch, const void* q, int3
   if (int rc = check_align(q, "q")) return rc;
   if (int rc = check_align(out, "out")) return rc;
   if (lse != nullptr && ((uintptr_t)lse & 3u) != 0) return fail(KVX_EINVAL, "lse is not 4-byte aligned");
-  if (int rc = use_device(pool)) return rc;
   hipStream_t s = (hipStream_t)stream;
-  if (validate_mode())
-    if (int rc = check_page_ids(pool, batch, s)) return rc;
+  CallBuffers buf{pool, fixed};
 
   if (is_decode_batch(batch, num_q_heads, pool->num_kv_heads))
-    return decode_attention(pool, batch, qo, q, num_q_heads, sm_scale, out, lse, s);
+    return decode_attention(pool, batch, qo, q, num_q_heads, sm_scale, out, lse, s, buf);
 
-  Plan plan;
-  if (int rc = make_plan(batch, qo, num_q_heads, pool->num_kv_heads, pool->split_keys, kMaxParts, plan)) return rc;
   const int D = pool->head_dim;
-  if (plan.n_parts > 0) {
-    const size_t obytes = (size_t)plan.n_parts * kvx::kTileRows * D * sizeof(float);
-    const size_t lbytes = (size_t)plan.n_parts * kvx::kTileRows * sizeof(float);
-    if (int rc = pool->parts.ensure(obytes + lbytes, s)) return rc;
-  }
+  const size_t part_bytes = (size_t)kvx::kTileRows * (D + 1) * sizeof(float);
+  Plan plan;
+  if (int rc = make_plan(batch, qo, num_q_heads, pool->num_kv_heads, pool->split_keys, buf.max_parts(part_bytes),
+                         plan))
+    return rc;
   // one upload: units, then merges
-  const size_t ub = plan.units.size() * sizeof(AttnUnit), mb = plan.merges.size() * sizeof(MergeUnit);
-  std::vector<uint8_t> blob(ub + mb);
-  if (ub) std::memcpy(blob.data(), plan.units.data(), ub);
-  if (mb) std::memcpy(blob.data() + ub, plan.merges.data(), mb);
+  const std::vector<uint8_t> blob = plan_blob(plan.units, plan.merges);
+  if (int rc = buf.check_plan(blob.size())) return rc;
+  if (int rc = use_device(pool)) return rc;
+  if (validate_mode())
+    if (int rc = check_page_ids(pool, batch, s)) return rc;
+  if (int rc = buf.bind()) return rc;
+  float* parts = nullptr;
+  if (plan.n_parts > 0)
+    if (int rc = buf.parts((size_t)plan.n_parts * part_bytes, s, &parts)) return rc;
   void* dev = nullptr;
-  if (int rc = pool->st_attn.upload(blob.data(), blob.size(), s, &dev)) return rc;
+  if (int rc = buf.upload(blob, s, &dev)) return rc;
 
   kvx::AttnParams p;
   p.q = (const uint16_t*)q;
@@ -996,8 +1073,8 @@ int extend_attention(kvx_pool* pool, const kvx_batch* batch, const void* q, int3
   p.v_pool = pool->v;
   p.page_ids = batch->page_ids;
   p.units = (const AttnUnit*)dev;
-  p.o_part = plan.n_parts ? (float*)pool->parts.ptr : nullptr;
-  p.lse_part = plan.n_parts ? (float*)pool->parts.ptr + (size_t)plan.n_parts * kvx::kTileRows * D : nullptr;
+  p.o_part = plan.n_parts ? parts : nullptr;
+  p.lse_part = plan.n_parts ? parts + (size_t)plan.n_parts * kvx::kTileRows * D : nullptr;
   p.k_scale = pool->scales_d;
   p.v_scale = pool->scales_d ? pool->scales_d + pool->num_kv_heads : nullptr;
   p.num_q_heads = num_q_heads;
@@ -1009,7 +1086,7 @@ int extend_attention(kvx_pool* pool, const kvx_batch* batch, const void* q, int3
   if (e != hipSuccess) return hip_fail(e, "extend_attention kernel launch");
   if (!plan.merges.empty()) {
     kvx::MergeParams m;
-    m.merges = (const MergeUnit*)((const uint8_t*)dev + ub);
+    m.merges = (const MergeUnit*)((const uint8_t*)dev + plan.units.size() * sizeof(AttnUnit));
     m.o_part = p.o_part;
     m.lse_part = p.lse_part;
     m.out = (uint16_t*)out;
@@ -1019,8 +1096,5 @@ int extend_attention(kvx_pool* pool, const kvx_batch* batch, const void* q, int3
     e = kvx::launch_merge(m, (int64_t)plan.merges.size(), D, s);
     if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
   }
-  if (int rc = pool->st_attn.done(s)) return rc;
-  return pool->parts.done(s);
+  return buf.done(s);
 }
-
-}  // extern "C"

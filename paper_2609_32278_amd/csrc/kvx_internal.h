@@ -197,6 +197,23 @@ hipError_t launch_decode_merge(const DecodeMergeParams& p, int64_t n_merges, int
 // Record a failure for kvx_last_error() and return `code` (host code of any file).
 int report(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 
+// Fixed device scratch of the allocation-free attention entry point: a plan region
+// of plan_bytes followed by a partial-result region of parts_bytes, at an address
+// that `address` gives per device (called with that device current).
+struct FixedScratch {
+  size_t plan_bytes;
+  size_t parts_bytes;
+  int (*address)(int device, void** base);
+};
+
+// extend_attention's whole call: argument checks, plan, upload, launches.  With
+// fixed == nullptr the plan goes through the pool's staging buffer and split
+// parts into its growable workspace; otherwise both go into the fixed scratch,
+// the plan is bounded by its regions (EUNSUPPORTED beyond them, checked on the
+// host before any device call) and nothing is allocated.
+int attention_call(kvx_pool* pool, const kvx_batch* batch, const void* q, int32_t num_q_heads, float sm_scale,
+                   void* out, float* lse, kvx_stream_t stream, const FixedScratch* fixed);
+
 hipError_t launch_extend_attention(const AttnParams& p, int64_t n_units, int head_dim, bool fp8,
                                    hipStream_t stream);
 hipError_t launch_merge(const MergeParams& p, int64_t n_merges, int head_dim, hipStream_t stream);

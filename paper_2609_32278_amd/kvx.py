@@ -25,10 +25,11 @@ STATUS_NAMES = {0: "KVX_OK", 1: "KVX_EINVAL", 2: "KVX_ENOMEM", 3: "KVX_ERANGE",
 
 KVX_EVICT_LRU, KVX_EVICT_RR = 0, 1
 KVX_ROPE_HALF, KVX_ROPE_INTERLEAVED = 0, 1
+NOALLOC_PLAN_BYTES, NOALLOC_PARTS_BYTES = 8 << 20, 56 << 20  # KVX_NOALLOC_* in include/kvx.h
 
 # Every symbol include/kvx.h and include/kvx_cache.h declare.
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_layout", "kv_pool_write_pages",
-           "kv_pool_read_pages", "kv_pool_record_bytes", "kv_pool_spill", "kv_pool_reload", "store_kv", "store_kv_rope", "extend_attention", "extend_attention_plan",
+           "kv_pool_read_pages", "kv_pool_record_bytes", "kv_pool_spill", "kv_pool_reload", "store_kv", "store_kv_rope", "extend_attention", "extend_attention_noalloc", "extend_attention_plan",
            "kv_pool_set_split_keys", "kvx_last_error",
            "kvx_cache_create", "kvx_cache_create_tiered", "kvx_cache_set_recency_tiers", "kvx_cache_destroy", "kvx_cache_begin_turn",
            "kvx_cache_begin_turn_tiered", "kvx_cache_end_turn", "kvx_cache_complete", "kvx_cache_agent",
@@ -112,6 +113,7 @@ def lib():
             "store_kv": [P, ctypes.POINTER(kvx_batch), P, P, P],
             "store_kv_rope": [P, ctypes.POINTER(kvx_batch), ctypes.POINTER(kvx_rope), P, i32, P, P, P, P],
             "extend_attention": [P, ctypes.POINTER(kvx_batch), P, i32, f32, P, P, P],
+            "extend_attention_noalloc": [P, ctypes.POINTER(kvx_batch), P, i32, f32, P, P, P],
             "extend_attention_plan": [ctypes.POINTER(kvx_batch), i32, i32, i32, i32, P, i64, ctypes.POINTER(i64)],
             "kv_pool_set_split_keys": [P, i32],
             "kvx_cache_create": [i64, i32, i32, i32, ctypes.POINTER(P)],
@@ -332,6 +334,15 @@ def extend_attention(pool, batch: Batch, q, num_q_heads: int, sm_scale: float, o
     _suffix_buffers(pool, batch, int(num_q_heads), q=q, out=out, lse=lse)
     _check(lib().extend_attention(pool, ctypes.byref(batch.c), _dptr(q), int(num_q_heads), float(sm_scale),
                                   _dptr(out), _dptr(lse), _stream(stream)), "extend_attention")
+
+
+def extend_attention_noalloc(pool, batch: Batch, q, num_q_heads: int, sm_scale: float, out, lse=None,
+                             stream=None) -> None:
+    """extend_attention without device allocation: plan and split parts go into the
+    library's fixed per-GPU scratch (NOALLOC_PLAN_BYTES + NOALLOC_PARTS_BYTES)."""
+    _suffix_buffers(pool, batch, int(num_q_heads), q=q, out=out, lse=lse)
+    _check(lib().extend_attention_noalloc(pool, ctypes.byref(batch.c), _dptr(q), int(num_q_heads), float(sm_scale),
+                                          _dptr(out), _dptr(lse), _stream(stream)), "extend_attention_noalloc")
 
 
 def extend_attention_plan(batch: Batch, num_q_heads: int, num_kv_heads: int, head_dim: int,
