@@ -26,7 +26,11 @@
 //   * online softmax in base 2: p = exp2(s * scale - m) (one FMA + one exp per
 //     score).  The running maximum m moves only when a row's maximum grows by
 //     more than 2^8, so O is rarely rescaled (the final division cancels the
-//     reference point);
+//     reference point).  On an fp8 pool the FMA goes away: Q is multiplied by
+//     scale * k_scale when it is loaded (one more bf16 rounding, 2^-9 relative,
+//     far below the pool's own e4m3 rounding of K), and the first MFMA of every
+//     score tile takes -m (a 16-register block) as its accumulator input, so the
+//     tile comes out as s * scale - m and p is exp2 of it directly;
 //   * O^T += V^T(t) P^T(t): V^T from LDS is the A operand, P stays in registers
 //     as bf16 pairs, and the row sums are taken over those bf16 values (v_dot2).
 // Software pipeline: the MFMAs of S(t+1) are issued among the exp / pack of tile
@@ -57,12 +61,19 @@ static_assert(kTileKeys % kBN == 0, "split boundaries must fall on tile boundari
 // compile-time flags passed to the pipelined iteration
 struct False { static constexpr bool value = false; };
 struct True { static constexpr bool value = true; };
+template <int N>
+struct Stage { static constexpr int value = N; };  // ring slot of tile t, or -1: computed from t
+using AnyStage = Stage<-1>;
 
 __device__ __forceinline__ float pair_max(float x) {
   // v_permlane32_swap(x, x): r[0] holds the low half's value, r[1] the high half's,
-  // in every lane, so the combination is identical in lanes l and l ^ 32.
+  // in every lane, so the combination is identical in lanes l and l ^ 32.  The
+  // inputs are scores (never signalling NaNs), so a plain v_max_f32 does, without
+  // the canonicalising copies fmaxf would add.
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  float m;
+  asm("v_max_f32 %0, %1, %2" : "=v"(m) : "v"(__uint_as_float(r[0])), "v"(__uint_as_float(r[1])));
+  return m;
 }
 
 __device__ __forceinline__ float pair_sum(float x) {
@@ -230,19 +241,19 @@ __device__ __forceinline__ void wait_issued(int n) {
 // at the same offsets shifted by 32 rows).
 // between(i) runs after k-step group i of the PER_WAVE groups (used to spread
 // this wave's loads of later tiles over the product).
+// The first k-step accumulates onto c0: zero, or (folded softmax) the negated
+// running maxima of the lanes' rows.
 template <int D, typename F>
 __device__ __forceinline__ void qk_tile(f32x16 (&s)[kKB], const uint8_t* kt, const int (&koff)[Geom<D>::KSTEPS],
-                                        const bf16x8 (&qf)[Geom<D>::KSTEPS], F&& between) {
+                                        const bf16x8 (&qf)[Geom<D>::KSTEPS], const f32x16& c0, F&& between) {
   using G = Geom<D>;
   constexpr int STEP = G::KSTEPS / G::PER_WAVE;
-#pragma unroll
-  for (int kb = 0; kb < kKB; kb++) s[kb] = f32x16{};
 #pragma unroll
   for (int st = 0; st < G::KSTEPS; st++) {
 #pragma unroll
     for (int kb = 0; kb < kKB; kb++) {
       const bf16x8 a = *(const bf16x8*)(kt + kb * 32 * D * 2 + koff[st]);
-      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], s[kb], 0, 0, 0);
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], st == 0 ? c0 : s[kb], 0, 0, 0);
     }
     if ((st + 1) % STEP == 0) between((st + 1) / STEP - 1);
   }
@@ -250,8 +261,8 @@ __device__ __forceinline__ void qk_tile(f32x16 (&s)[kKB], const uint8_t* kt, con
 
 template <int D>
 __device__ __forceinline__ void qk_tile(f32x16 (&s)[kKB], const uint8_t* kt, const int (&koff)[Geom<D>::KSTEPS],
-                                        const bf16x8 (&qf)[Geom<D>::KSTEPS]) {
-  qk_tile<D>(s, kt, koff, qf, [](int) {});
+                                        const bf16x8 (&qf)[Geom<D>::KSTEPS], const f32x16& c0) {
+  qk_tile<D>(s, kt, koff, qf, c0, [](int) {});
 }
 
 // Raw row maximum of a tile (optionally causally masked in place), combined over
@@ -278,17 +289,20 @@ __device__ __forceinline__ float row_max(f32x16 (&s)[kKB], int k0, int qpos, int
 
 // p = exp2(s * scale - m) as bf16 pairs (the P^T B operands, one per page of the
 // tile); returns the row sum over those bf16 values added to l.
+// FOLDED: the tile is already s * scale - m, and p = exp2 of it.
+template <bool FOLDED>
 __device__ __forceinline__ float exp_pack(const f32x16 (&s)[kKB], bf16x8 (&pb)[2 * kKB], float l, float m_run,
                                           float scale) {
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   const float neg = -m_run;
+  auto arg = [&](float x) { return FOLDED ? x : __builtin_fmaf(x, scale, neg); };
 #pragma unroll
   for (int pg = 0; pg < 2 * kKB; pg++) {
     uint32_t w[4];
 #pragma unroll
     for (int e = 0; e < 4; e++) {
-      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[pg / 2][8 * (pg % 2) + 2 * e], scale, neg));
-      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[pg / 2][8 * (pg % 2) + 2 * e + 1], scale, neg));
+      const float p0 = __builtin_amdgcn_exp2f(arg(s[pg / 2][8 * (pg % 2) + 2 * e]));
+      const float p1 = __builtin_amdgcn_exp2f(arg(s[pg / 2][8 * (pg % 2) + 2 * e + 1]));
       w[e] = pack_bf16(p0, p1);
       l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, l, false);
     }
@@ -349,12 +363,34 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   const bool valid = tok < ntok;
   const int qpos = u.q_pos0 + tok;
 
-  // Q^T operand: k-slot (h, j) of k-step s holds dim h*D/2 + 8s + j
+  // softmax scale of the scores in log2 units (with the pool's k_scale on fp8)
+  constexpr bool FOLD = FP8;  // scale and running maximum folded into the products
+  float scale = p.scale_log2;
+  float vscale = 1.0f;
+  if constexpr (FP8) {
+    scale *= p.k_scale[kv_head];
+    vscale = p.v_scale[kv_head];
+  }
+
+  // Q^T operand: k-slot (h, j) of k-step s holds dim h*D/2 + 8s + j; folded: times
+  // scale, rounded once to bf16
   bf16x8 qf[G::KSTEPS];
   {
     const uint4* src = (const uint4*)(p.q + ((size_t)(u.qo_row0 + tok) * p.num_q_heads + hq) * D + h * (D / 2));
 #pragma unroll
-    for (int s = 0; s < G::KSTEPS; s++) qf[s] = __builtin_bit_cast(bf16x8, valid ? src[s] : make_uint4(0, 0, 0, 0));
+    for (int s = 0; s < G::KSTEPS; s++) {
+      const uint4 raw = valid ? src[s] : make_uint4(0, 0, 0, 0);
+      if constexpr (FOLD) {
+        const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+        uint32_t o4[4];
+#pragma unroll
+        for (int e = 0; e < 4; e++)
+          o4[e] = pack_bf16(__uint_as_float(w[e] << 16) * scale, __uint_as_float(w[e] & 0xFFFF0000u) * scale);
+        qf[s] = __builtin_bit_cast(bf16x8, make_uint4(o4[0], o4[1], o4[2], o4[3]));
+      } else {
+        qf[s] = __builtin_bit_cast(bf16x8, raw);
+      }
+    }
   }
 
   // LDS read offsets.  K: MFMA row n holds key row_key(n); k-step st reads dims
@@ -371,17 +407,13 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
 #pragma unroll
   for (int it = 0; it < G::PER_WAVE; it++) slot[it].init(it * kWaves + wave, lane);
 
-  float scale = p.scale_log2;
-  float vscale = 1.0f;
-  if constexpr (FP8) {
-    scale *= p.k_scale[kv_head];
-    vscale = p.v_scale[kv_head];
-  }
-
   f32x16 o[G::DB];
 #pragma unroll
   for (int b = 0; b < G::DB; b++) o[b] = f32x16{};
-  float m_run = -1e30f, l_run = 0.0f, mx;
+  // running maximum m of the lane's row (log2 units); folded: -m is also the score
+  // tiles' accumulator input, and m starts at the first tile's row maximum
+  float m_run = FOLD ? 0.0f : -1e30f, l_run = 0.0f, mx;
+  f32x16 cneg = f32x16{};
 
   const int kb0 = u.key_begin;
   const int n_tiles = (u.key_end - kb0 + kBN - 1) / kBN;
@@ -515,8 +547,16 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
 
   f32x16 sa[kKB], sb[kKB];
   bf16x8 pb[2 * kKB];
-  qk_tile<D>(sa, k_lds[0], koff, qf);
+  qk_tile<D>(sa, k_lds[0], koff, qf, cneg);
   mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
+  if constexpr (FOLD) {
+    // the first tile's row maximum is finite (its first key is visible to every row)
+    m_run = mx;
+#pragma unroll
+    for (int kb = 0; kb < kKB; kb++) sa[kb] -= mx;
+    cneg = -mx;
+    mx = 0.0f;
+  }
   __syncthreads();  // every wave has read K(0) before iteration 0 refills its slot with K(4)
 
   // One pipelined iteration: consumes S(t) (scores in s_cur, maximum in mx), produces
@@ -527,21 +567,44 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   // is one branch-free block in which MFMA and the softmax VALU work interleave.
   // lazy rescale before the scores of the tile whose maximum is mx are exponentiated:
   // the reference maximum moves only when a row outgrows it by 2^8
-  auto rescale = [&]() {
-    if (__any(mx * scale > m_run + kRescaleThreshold)) {
-      const float m_new = fmaxf(m_run, mx * scale);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
+  // (folded: mx and the tile st are relative to m, and st moves with m)
+  auto rescale = [&](f32x16 (&st)[kKB]) {
+    if constexpr (FOLD) {
+      if (__any(mx > kRescaleThreshold)) {
+        const float d = fmaxf(mx, 0.0f);
+        const float alpha = __builtin_amdgcn_exp2f(-d);
+        l_run *= alpha;
 #pragma unroll
-      for (int b = 0; b < G::DB; b++) o[b] *= alpha;
-      m_run = m_new;
+        for (int b = 0; b < G::DB; b++) o[b] *= alpha;
+#pragma unroll
+        for (int kb = 0; kb < kKB; kb++) st[kb] -= d;
+        m_run += d;
+        mx -= d;
+        cneg = -m_run;
+      }
+    } else {
+      if (__any(mx * scale > m_run + kRescaleThreshold)) {
+        const float m_new = fmaxf(m_run, mx * scale);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int b = 0; b < G::DB; b++) o[b] *= alpha;
+        m_run = m_new;
+      }
     }
   };
-  if constexpr (FP8) rescale();
+  if constexpr (FP8 && !FOLD) rescale(sa);
 
-  auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole) {
+  auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole, auto stage) {
     constexpr bool MASKED = decltype(masked)::value;
     constexpr bool WHOLE = decltype(whole)::value;
+    constexpr int ST = decltype(stage)::value;
+    // ring slot of tile t + d: a constant when the caller knows t's slot, so every
+    // LDS operand address is a register plus an immediate offset
+    auto ring = [&](int d) -> int {
+      if constexpr (ST >= 0) return (ST + d) % G::NSTAGE;
+      else return (t + d) % G::NSTAGE;
+    };
     const int k0 = kb0 + t * kBN;
     const bool has_next = MASKED ? t + 1 < n_tiles : true;
     const int tk = WHOLE || t + 4 < n_tiles ? t + 4 : -1;
@@ -560,32 +623,33 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
 
     // bf16 pool: the check for S(t) comes here; the fp8 kernel, tighter on
     // registers, takes it at the end of the previous iteration instead
-    if constexpr (!FP8) rescale();
+    if constexpr (!FP8) rescale(s_cur);
 
     if constexpr (MASKED) {
-      if (has_next) qk_tile<D>(s_nxt, k_lds[(t + 1) % G::NSTAGE], koff, qf);
-      l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
-      pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
+      if (has_next) qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, cneg);
+      l_run = exp_pack<FOLD>(s_cur, pb, l_run, m_run, scale);
+      pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
       if (has_next) mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
     } else if constexpr (SPREAD) {
-      qk_tile<D>(s_nxt, k_lds[(t + 1) % G::NSTAGE], koff, qf, [&](int i) {
+      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, cneg, [&](int i) {
         const int it = G::PER_WAVE - 1 - i;
         const bool is_v = it >= G::K_SLOTS;
-        const int tt = is_v ? tv : tk;
         if constexpr (FP8) fresh[it] = *(const uint2*)(blk[it] + slot[it].off / 2);
-        else issue_direct<D>(slot[it], blk[it], is_v ? v_lds[tt % G::NSTAGE] : k_lds[tt % G::NSTAGE]);
+        else issue_direct<D>(slot[it], blk[it], is_v ? v_lds[ring(3)] : k_lds[ring(4)]);  // V(t+3), K(t+4)
       });
-      l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
-      pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
+      l_run = exp_pack<FOLD>(s_cur, pb, l_run, m_run, scale);
+      pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
       mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     } else {
-      qk_tile<D>(s_nxt, k_lds[(t + 1) % G::NSTAGE], koff, qf);
-      l_run = exp_pack(s_cur, pb, l_run, m_run, scale);
-      pv_tile<D>(o, v_lds[t % G::NSTAGE], vbase, pb);
+      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, cneg);
+      l_run = exp_pack<FOLD>(s_cur, pb, l_run, m_run, scale);
+      pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
       mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     }
 
-    if constexpr (FP8) rescale();  // for S(t+1), exponentiated in the next iteration
+    if constexpr (FP8) {
+      if (!MASKED || has_next) rescale(s_nxt);  // for S(t+1), exponentiated in the next iteration
+    }
     if constexpr (SPREAD) {
       // next page ids, read after this iteration's last LDS operand read so that no
       // operand wait has to cover an outstanding scalar load
@@ -609,24 +673,31 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   // prologue issued K(3) and V(2) in full whenever that holds for t = 0.
   {
     const int whole_end = (last_whole - 3 < n_tiles - 4 ? last_whole - 3 : n_tiles - 4);
+    // four tiles per trip (t % 4 == 0 at its top): every ring slot is a constant
+    for (; t + 4 < n_full && t + 3 < whole_end; t += 4) {
+      iteration(sa, sb, t, False{}, True{}, Stage<0>{});
+      iteration(sb, sa, t + 1, False{}, True{}, Stage<1>{});
+      iteration(sa, sb, t + 2, False{}, True{}, Stage<2>{});
+      iteration(sb, sa, t + 3, False{}, True{}, Stage<3>{});
+    }
     for (; t + 2 < n_full && t + 1 < whole_end; t += 2) {
-      iteration(sa, sb, t, False{}, True{});
-      iteration(sb, sa, t + 1, False{}, True{});
+      iteration(sa, sb, t, False{}, True{}, AnyStage{});
+      iteration(sb, sa, t + 1, False{}, True{}, AnyStage{});
     }
   }
   for (; t + 2 < n_full; t += 2) {
-    iteration(sa, sb, t, False{}, False{});
-    iteration(sb, sa, t + 1, False{}, False{});
+    iteration(sa, sb, t, False{}, False{}, AnyStage{});
+    iteration(sb, sa, t + 1, False{}, False{}, AnyStage{});
   }
   if (t + 1 < n_full) {
-    iteration(sa, sb, t, False{}, False{});
+    iteration(sa, sb, t, False{}, False{}, AnyStage{});
     t++;
 #pragma unroll
     for (int kb = 0; kb < kKB; kb++) sa[kb] = sb[kb];
   }
   for (; t < n_tiles; t += 2) {
-    iteration(sa, sb, t, True{}, False{});
-    if (t + 1 < n_tiles) iteration(sb, sa, t + 1, True{}, False{});
+    iteration(sa, sb, t, True{}, False{}, AnyStage{});
+    if (t + 1 < n_tiles) iteration(sb, sa, t + 1, True{}, False{}, AnyStage{});
   }
 
   wait_vmcnt<0>();  // no load into this workgroup's LDS may outlive it
