@@ -33,7 +33,9 @@ EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_layout", "kv_pool_write
            "kv_pool_set_split_keys", "kvx_last_error",
            "kvx_cache_create", "kvx_cache_create_tiered", "kvx_cache_set_recency_tiers", "kvx_cache_destroy", "kvx_cache_begin_turn",
            "kvx_cache_begin_turn_tiered", "kvx_cache_end_turn", "kvx_cache_complete", "kvx_cache_agent",
-           "kvx_cache_agent_host", "kvx_cache_join", "kvx_cache_group", "kvx_cache_stats"]
+           "kvx_cache_agent_host", "kvx_cache_join", "kvx_cache_group", "kvx_cache_stats",
+           "kvx_radix_create", "kvx_radix_destroy", "kvx_radix_begin", "kvx_radix_end", "kvx_radix_complete",
+           "kvx_radix_match", "kvx_radix_stats"]
 
 
 class KvxNotBuilt(ImportError):
@@ -75,6 +77,13 @@ class kvx_work_item(ctypes.Structure):
 
 
 WORK_ITEM_DTYPE = np.dtype([(n, np.int32) for n, _ in kvx_work_item._fields_])
+
+
+class kvx_radix_counters(ctypes.Structure):
+    _fields_ = [("num_pages", ctypes.c_int64), ("free_pages", ctypes.c_int64), ("cached_pages", ctypes.c_int64),
+                ("temp_pages", ctypes.c_int64), ("nodes", ctypes.c_int64), ("leaves", ctypes.c_int64),
+                ("evicted_pages", ctypes.c_int64), ("evictions", ctypes.c_int64), ("active", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class kvx_cache_stats_t(ctypes.Structure):
@@ -129,6 +138,13 @@ def lib():
             "kvx_cache_complete": [P, i64],
             "kvx_cache_agent": [P, i64, ctypes.POINTER(i32), P, i64],
             "kvx_cache_stats": [P, ctypes.POINTER(kvx_cache_stats_t)],
+            "kvx_radix_create": [i64, i32, i32, i32, ctypes.POINTER(P)],
+            "kvx_radix_destroy": [P],
+            "kvx_radix_begin": [P, i64, P, i32, ctypes.POINTER(i32), P, i64],
+            "kvx_radix_end": [P, i64],
+            "kvx_radix_complete": [P, i64],
+            "kvx_radix_match": [P, P, i32, ctypes.POINTER(i32), P, i64],
+            "kvx_radix_stats": [P, ctypes.POINTER(kvx_radix_counters)],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -471,3 +487,58 @@ def kvx_cache_stats(cache) -> dict:
     st = kvx_cache_stats_t()
     _check(lib().kvx_cache_stats(cache, ctypes.byref(st)), "kvx_cache_stats")
     return {n: getattr(st, n) for n, _ in st._fields_}
+
+
+# ------------------------------------------------------------------ token-content radix tree (include/kvx_radix.h)
+
+def _tokens(tokens) -> np.ndarray:
+    t = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32))
+    if t.ndim != 1:
+        raise ValueError("tokens must be one-dimensional")
+    return t
+
+
+def kvx_radix_create(num_pages: int, page_size: int = 16, chunk_tokens: int = 1024, policy: int = KVX_EVICT_RR):
+    out = ctypes.c_void_p()
+    _check(lib().kvx_radix_create(int(num_pages), int(page_size), int(chunk_tokens), int(policy), ctypes.byref(out)),
+           "kvx_radix_create")
+    return out
+
+
+def kvx_radix_destroy(tree) -> None:
+    _check(lib().kvx_radix_destroy(tree), "kvx_radix_destroy")
+
+
+def kvx_radix_begin(tree, agent: int, tokens, page_size: int = 16):
+    """Start a request of `agent` over `tokens`; returns (prefix_len, page table)."""
+    t = _tokens(tokens)
+    n = len(t)
+    table = np.zeros(max(1, (n + page_size - 1) // page_size), dtype=np.int32)
+    prefix = ctypes.c_int32()
+    _check(lib().kvx_radix_begin(tree, int(agent), t.ctypes.data, n, ctypes.byref(prefix), table.ctypes.data,
+                                 len(table)), "kvx_radix_begin")
+    return prefix.value, table
+
+
+def kvx_radix_end(tree, agent: int) -> None:
+    _check(lib().kvx_radix_end(tree, int(agent)), "kvx_radix_end")
+
+
+def kvx_radix_complete(tree, agent: int) -> None:
+    _check(lib().kvx_radix_complete(tree, int(agent)), "kvx_radix_complete")
+
+
+def kvx_radix_match(tree, tokens, page_size: int = 16):
+    """Longest cached whole-page prefix of `tokens`: (matched tokens, its pages)."""
+    t = _tokens(tokens)
+    m = ctypes.c_int32()
+    pages = np.zeros(max(1, len(t) // page_size), dtype=np.int32)
+    _check(lib().kvx_radix_match(tree, t.ctypes.data, len(t), ctypes.byref(m), pages.ctypes.data, len(pages)),
+           "kvx_radix_match")
+    return m.value, pages[: m.value // page_size].copy()
+
+
+def kvx_radix_stats(tree) -> dict:
+    st = kvx_radix_counters()
+    _check(lib().kvx_radix_stats(tree, ctypes.byref(st)), "kvx_radix_stats")
+    return {n: getattr(st, n) for n, _ in st._fields_ if n != "reserved"}

@@ -457,3 +457,37 @@ def agent_q(tr: AgentTrace, agent: int, turn: int, rows: int, device="cpu") -> t
     """Queries of the uncached rows of one turn: bf16 [rows, Hq, d]."""
     return _randn_bf16((rows, tr.num_q_heads, tr.head_dim), tr.sigma,
                        _torch_seed(AGENT_CONFIG_ID, 1, tr.seed, 0, agent * 4096 + turn), device)
+
+
+# ----------------------------------------------------------------------------- token content
+
+TOKEN_CONFIG_ID = 11  # seed domain of the token-keyed K/V below
+_HASH_MOD = (1 << 61) - 1
+
+
+def prefix_hashes(tokens) -> list:
+    """Rolling hash of every prefix: h_t = (h_{t-1} * 1000003 + token_t + 1) mod (2^61 - 1)."""
+    h, out = 0, []
+    for x in tokens:
+        h = (h * 1_000_003 + int(x) + 1) % _HASH_MOD
+        out.append(h)
+    return out
+
+
+def content_kv(tokens, num_kv_heads: int, head_dim: int, sigma: float = 1.0, device="cpu", _memo={}):
+    """K and V [n, Hkv, d] (bf16) of a token sequence in which row t depends only on
+    tokens[0 .. t] -- the way a model's KV depends on the context so far -- drawn
+    N(0, sigma^2) from a generator seeded by the prefix's hash.  Sequences that share
+    a prefix share its rows, whichever request computes them."""
+    rows = []
+    per = 2 * num_kv_heads * head_dim
+    for h in prefix_hashes(tokens):
+        key = (h, per, sigma)
+        r = _memo.get(key)
+        if r is None:
+            r = np.random.default_rng([TOKEN_CONFIG_ID, h & 0xFFFFFFFF, h >> 32]).standard_normal(per) * sigma
+            _memo[key] = r
+        rows.append(r)
+    x = torch.from_numpy(np.asarray(rows, dtype=np.float32).reshape(len(rows), 2, num_kv_heads, head_dim))
+    x = x.to(torch.bfloat16).to(device)
+    return x[:, 0].contiguous(), x[:, 1].contiguous()

@@ -1,6 +1,7 @@
 """AddressSanitizer and UndefinedBehaviorSanitizer builds of the host code (no GPU):
 the prefix cache (csrc/kvx_cache.cpp) under random turn sequences of both
-policies with host tiers, recency tiers and shared-prefix groups; the work
+policies with host tiers, recency tiers and shared-prefix groups; the radix
+tree (csrc/kvx_radix.cpp) under random branching request sequences; the work
 planners of csrc/kvx_host.cpp under random ragged batches (kernel launchers
 stubbed out); and the C oracle under random ragged batches stored into
 NaN-filled pools.  The drivers also check ownership, coverage and finiteness
@@ -36,6 +37,18 @@ def test_cache_under_sanitizers(tmp_path):
            os.path.join(ROOT, "paper_2609_32278_amd", "csrc", "kvx_cache.cpp"),
            os.path.join(ROOT, "tests", "sanitize", "cache_stress.cpp"), "-o", exe]
     out = _build_and_run(cmd, exe, ["1000"], tmp_path)
+    assert "passed" in out
+    print(out)
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not installed")
+def test_radix_tree_under_sanitizers(tmp_path):
+    exe = str(tmp_path / "radix_stress")
+    cmd = ["g++", "-std=c++17", *SAN, "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+           "-I" + os.path.join(ROOT, "include"), "-I" + os.path.join(ROOT, "paper_2609_32278_amd", "csrc"),
+           os.path.join(ROOT, "paper_2609_32278_amd", "csrc", "kvx_radix.cpp"),
+           os.path.join(ROOT, "tests", "sanitize", "radix_stress.cpp"), "-o", exe]
+    out = _build_and_run(cmd, exe, ["200"], tmp_path)
     assert "passed" in out
     print(out)
 
