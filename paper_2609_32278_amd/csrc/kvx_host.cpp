@@ -570,6 +570,32 @@ std::vector<uint8_t> plan_blob(const std::vector<U>& units, const std::vector<M>
   return blob;
 }
 
+// The requests of a store batch in the kernel arguments when there are few enough
+// (returns false otherwise: the unit list is uploaded instead).  Workgroup order
+// matches the unit lists below: request by request, logical page by page.
+bool inline_store_reqs(const kvx_batch* b, const std::vector<int64_t>& qo, kvx::StoreReqs& rq) {
+  rq.n = 0;
+  int32_t wg = 0;
+  for (int r = 0; r < b->num_reqs; r++) {
+    const int64_t P = b->prefix_lens[r], E = b->extend_lens[r];
+    if (E == 0) continue;
+    if (rq.n == kvx::kStoreInlineReqs) {
+      rq.n = 0;
+      return false;
+    }
+    const int64_t pages = (P + E - 1) / kvx::kPageSize - P / kvx::kPageSize + 1;
+    rq.first[rq.n] = wg;
+    rq.qo[rq.n] = (int32_t)qo[(size_t)r];
+    rq.prefix[rq.n] = (int32_t)P;
+    rq.end[rq.n] = (int32_t)(P + E);
+    rq.page_base[rq.n] = b->page_indptr[r];
+    wg += (int32_t)pages;
+    rq.n++;
+  }
+  rq.first[rq.n] = wg;
+  return rq.n > 0;
+}
+
 int decode_attention(kvx_pool* pool, const kvx_batch* batch, const std::vector<int64_t>& qo, const void* q,
                      int32_t num_q_heads, float sm_scale, void* out, float* lse, hipStream_t s, CallBuffers& buf) {
   const int D = pool->head_dim;
@@ -888,9 +914,10 @@ int store_kv(kvx_pool* pool, const kvx_batch* batch, const void* k_ext, const vo
       units.push_back(u);
     }
   }
-  void* units_d = nullptr;
-  if (int rc = pool->st_store.upload(units.data(), units.size() * sizeof(StoreUnit), s, &units_d)) return rc;
   kvx::StoreParams p;
+  void* units_d = nullptr;
+  if (!inline_store_reqs(batch, qo, p.reqs))
+    if (int rc = pool->st_store.upload(units.data(), units.size() * sizeof(StoreUnit), s, &units_d)) return rc;
   p.k_ext = (const uint16_t*)k_ext;
   p.v_ext = (const uint16_t*)v_ext;
   p.k_pool = pool->k;
@@ -902,7 +929,7 @@ int store_kv(kvx_pool* pool, const kvx_batch* batch, const void* k_ext, const vo
   p.num_kv_heads = pool->num_kv_heads;
   hipError_t e = kvx::launch_store_kv(p, (int64_t)units.size(), pool->head_dim, pool->kv_dtype == KVX_KV_FP8_E4M3, s);
   if (e != hipSuccess) return hip_fail(e, "store_kv kernel launch");
-  return pool->st_store.done(s);
+  return p.reqs.n > 0 ? KVX_OK : pool->st_store.done(s);
 }
 
 int store_kv_rope(kvx_pool* pool, const kvx_batch* batch, const kvx_rope* rope, const void* q, int32_t num_q_heads,
@@ -966,7 +993,8 @@ int store_kv_rope(kvx_pool* pool, const kvx_batch* batch, const kvx_rope* rope, 
     }
   }
   void* units_d = nullptr;
-  if (int rc = pool->st_store.upload(units.data(), units.size() * sizeof(kvx::RopeUnit), s, &units_d)) return rc;
+  if (!inline_store_reqs(batch, qo, p.reqs))
+    if (int rc = pool->st_store.upload(units.data(), units.size() * sizeof(kvx::RopeUnit), s, &units_d)) return rc;
   p.q = (const uint16_t*)q;
   p.q_out = (uint16_t*)q_out;
   p.k_ext = (const uint16_t*)k_ext;
@@ -986,7 +1014,7 @@ int store_kv_rope(kvx_pool* pool, const kvx_batch* batch, const kvx_rope* rope, 
   hipError_t e = kvx::launch_store_kv_rope(p, (int64_t)units.size(), D, pool->kv_dtype == KVX_KV_FP8_E4M3,
                                            rope->style == KVX_ROPE_INTERLEAVED, s);
   if (e != hipSuccess) return hip_fail(e, "store_kv_rope kernel launch");
-  return pool->st_store.done(s);
+  return p.reqs.n > 0 ? KVX_OK : pool->st_store.done(s);
 }
 
 int extend_attention_plan(const kvx_batch* batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,

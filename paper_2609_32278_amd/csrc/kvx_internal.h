@@ -74,6 +74,19 @@ struct MergeParams {
   int32_t group;
 };
 
+// The requests of a small store batch, passed by value in the kernel arguments so
+// that no unit list is uploaded: request r's pages are the workgroups
+// [first[r], first[r + 1]), logical pages prefix[r] / 16 onwards.
+constexpr int kStoreInlineReqs = 96;
+struct StoreReqs {
+  int32_t n;                            // requests with work; 0: use the uploaded unit list
+  int32_t first[kStoreInlineReqs + 1];  // first workgroup of each request; first[n] = all
+  int32_t qo[kStoreInlineReqs];         // suffix row of the request's first suffix token
+  int32_t prefix[kStoreInlineReqs];     // P
+  int32_t end[kStoreInlineReqs];        // P + E
+  int32_t page_base[kStoreInlineReqs];  // page_indptr[r]
+};
+
 struct StoreParams {
   const uint16_t* k_ext;  // bf16 [T, Hkv, D]
   const uint16_t* v_ext;
@@ -84,6 +97,7 @@ struct StoreParams {
   const float* k_inv_scale;  // fp8 pool: device [Hkv], fp32 1/scale
   const float* v_inv_scale;
   int32_t num_kv_heads;
+  StoreReqs reqs;            // reqs.n > 0: the units come from here instead
 };
 
 // One fused-store workgroup: a StoreUnit plus the absolute position of slot 0.
@@ -115,6 +129,7 @@ struct RopeParams {
   int32_t rotary_dim;        // multiple of 16, <= D
   float norm_eps;
   double rev_freq[kRopeMaxPlanes];  // plane rate in revolutions per position: f_j / (2 pi)
+  StoreReqs reqs;                   // reqs.n > 0: the units come from here instead
 };
 
 struct PageIoParams {

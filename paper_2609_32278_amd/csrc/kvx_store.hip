@@ -6,11 +6,12 @@
 // from the pool.  HBM-bound: each element is read once and written once.
 //
 // Pool layout: K [page][kv_head][slot][dim], V [page][kv_head][dim][slot].
-// One workgroup handles one page of one request (all KV heads), in passes of
-// 4 heads (head_dim 128) or 8 (head_dim 64) whose loads are all issued before any
-// is used (four K and four V 16-byte loads in flight per thread): K rows are
-// copied with 16-byte accesses, V rows are staged in LDS and written out
-// transposed, one 16-slot column (32 bytes bf16 / 16 bytes fp8) per dim.
+// One workgroup handles one page of one request for one group of 4 KV heads
+// (head_dim 128) or 8 (head_dim 64) -- grid x = the page, y = the head group, so
+// that a batch touching few pages still fills the chip -- and issues all of its
+// loads before using any (four K and four V 16-byte loads in flight per thread):
+// K rows are copied with 16-byte accesses, V rows are staged in LDS and written
+// out transposed, one 16-slot column (32 bytes bf16 / 16 bytes fp8) per dim.
 // fp8 pool: code = e4m3_rne(clamp(x * inv_scale_h, -448, 448)) with the
 // hardware converter v_cvt_pk_fp8_f32 (OCP e4m3 on gfx950).
 
@@ -80,6 +81,25 @@ __device__ __forceinline__ void write_vt(const uint16_t (&vs)[kPageSize][D + 8],
   }
 }
 
+// The unit of workgroup b of a small batch (see StoreReqs); uniform.
+__device__ __forceinline__ RopeUnit inline_unit(const StoreReqs& rq, int b) {
+  int lo = 0, hi = rq.n;  // request r with first[r] <= b < first[r + 1]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) / 2;
+    if (rq.first[mid] <= b) lo = mid;
+    else hi = mid;
+  }
+  const int P = rq.prefix[lo], L = rq.end[lo];
+  const int lp = P / kPageSize + (b - rq.first[lo]);
+  RopeUnit u;
+  u.pos_slot0 = lp * kPageSize;
+  u.row_slot0 = rq.qo[lo] + u.pos_slot0 - P;
+  u.page_pos = rq.page_base[lo] + lp;
+  u.slot_begin = (P > u.pos_slot0 ? P : u.pos_slot0) - u.pos_slot0;
+  u.slot_end = (L < u.pos_slot0 + kPageSize ? L : u.pos_slot0 + kPageSize) - u.pos_slot0;
+  return u;
+}
+
 template <int D, bool FP8>
 __global__ __launch_bounds__(kStoreThreads) void store_kv_kernel(StoreParams p) {
   constexpr int CPR = D / 8;                          // 16-byte chunks per bf16 row
@@ -89,11 +109,18 @@ __global__ __launch_bounds__(kStoreThreads) void store_kv_kernel(StoreParams p) 
   static_assert(PER == 4, "four K and four V loads in flight per thread");
   // V rows of this page for the pass's heads, staged for the transpose: [head][16 slots][D] bf16
   __shared__ __attribute__((aligned(16))) uint16_t vs[HB][kPageSize][D + 8];
-  const StoreUnit su = p.units[blockIdx.x];
+  StoreUnit su;
+  if (p.reqs.n > 0) {
+    const RopeUnit u = inline_unit(p.reqs, blockIdx.x);
+    su = StoreUnit{u.row_slot0, u.page_pos, u.slot_begin, u.slot_end};
+  } else {
+    su = p.units[blockIdx.x];
+  }
   const int page = p.page_ids[su.page_pos];
   const int H = p.num_kv_heads;
 
-  for (int h0 = 0; h0 < H; h0 += HB) {
+  {
+    const int h0 = blockIdx.y * HB;
     // every load of the pass is issued before any of them is used
     uint4 kx[PER], vx[PER];
 #pragma unroll
@@ -135,7 +162,6 @@ __global__ __launch_bounds__(kStoreThreads) void store_kv_kernel(StoreParams p) 
       const size_t blk = ((size_t)page * H + hd) * (size_t)(kPageSize * D);
       write_vt<D, FP8>(vs[hb], p.v_pool, blk, su.slot_begin, su.slot_end, FP8 ? p.v_inv_scale[hd] : 1.0f);
     }
-    __syncthreads();
   }
 }
 
@@ -275,7 +301,7 @@ template <int D, bool FP8, bool INTERLEAVED>
 __global__ __launch_bounds__(kStoreThreads) void store_kv_rope_kernel(RopeParams p) {
   __shared__ float2 cs[kPageSize][kRopeMaxPlanes];  // (cos, sin) of every live slot and plane
   __shared__ __attribute__((aligned(16))) uint16_t vs[kPageSize][D + 8];
-  const RopeUnit u = p.units[blockIdx.x];
+  const RopeUnit u = p.reqs.n > 0 ? inline_unit(p.reqs, blockIdx.x) : p.units[blockIdx.x];
   const int page = p.page_ids[u.page_pos];
   const int planes = p.rotary_dim / 2;
   const int ntok = u.slot_end - u.slot_begin;
@@ -411,7 +437,8 @@ __global__ __launch_bounds__(256) void page_io_kernel(PageIoParams p) {
 hipError_t launch_store_kv(const StoreParams& p, int64_t n_units, int head_dim, bool fp8,
                            hipStream_t stream) {
   if (n_units <= 0) return hipSuccess;
-  dim3 grid((unsigned)n_units), block(kStoreThreads);
+  const int hb = head_dim == 128 ? 4 : 8;  // heads per workgroup (HB of the kernel)
+  dim3 grid((unsigned)n_units, (unsigned)((p.num_kv_heads + hb - 1) / hb)), block(kStoreThreads);
   if (head_dim == 128) {
     if (fp8) hipLaunchKernelGGL((store_kv_kernel<128, true>), grid, block, 0, stream, p);
     else hipLaunchKernelGGL((store_kv_kernel<128, false>), grid, block, 0, stream, p);
