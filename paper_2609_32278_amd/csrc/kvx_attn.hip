@@ -326,83 +326,144 @@ __device__ __forceinline__ void pv_tile(f32x16 (&o)[Geom<D>::DB], const uint8_t*
   }
 }
 
-template <int D, bool FP8>
+// ---------------------------------------------------------------- shared by both kernels
+
+// The work item of this workgroup (scalar loads: every index derived from it stays
+// uniform) and the lane's query row within it.
+struct Rows {
+  AttnUnit u;
+  int lane, wave;
+  int n;        // query row within the wave's block / MFMA row
+  int h;        // half of the wave
+  int kv_head, ntok;
+  int rho;      // row of the unit: token * group + head-in-group
+  int tok, hq, qpos;
+  bool valid;   // the row is a real query (its token exists)
+};
+
+__device__ __forceinline__ Rows rows_of(const AttnParams& p) {
+  Rows r;
+  const const_i32_ptr w = (const_i32_ptr)(p.units + blockIdx.x);
+  r.u.qo_row0 = w[0];
+  r.u.q_pos0 = w[1];
+  r.u.page_base = w[2];
+  r.u.key_begin = w[3];
+  r.u.key_end = w[4];
+  r.u.head_ntok = w[5];
+  r.u.part = w[6];
+  r.u.req = w[7];
+  r.lane = threadIdx.x & 63;
+  r.wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  r.n = r.lane & 31;
+  r.h = r.lane >> 5;
+  r.kv_head = r.u.head_ntok >> 16;
+  r.ntok = r.u.head_ntok & 0xFFFF;
+  r.rho = r.wave * 32 + r.n;
+  r.tok = r.rho / p.group;
+  r.hq = r.kv_head * p.group + (r.rho - r.tok * p.group);
+  r.valid = r.tok < r.ntok;
+  r.qpos = r.u.q_pos0 + r.tok;
+  return r;
+}
+
+// Q^T operand: k-slot (h, j) of k-step s holds dim h*D/2 + 8s + j.  SCALED: times
+// `scale`, rounded once to bf16.
+template <int D, bool SCALED>
+__device__ __forceinline__ void load_q(bf16x8 (&qf)[Geom<D>::KSTEPS], const AttnParams& p, const Rows& r,
+                                       float scale) {
+  const uint4* src = (const uint4*)(p.q + ((size_t)(r.u.qo_row0 + r.tok) * p.num_q_heads + r.hq) * D + r.h * (D / 2));
+#pragma unroll
+  for (int s = 0; s < Geom<D>::KSTEPS; s++) {
+    const uint4 raw = r.valid ? src[s] : make_uint4(0, 0, 0, 0);
+    if constexpr (SCALED) {
+      const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+      uint32_t o4[4];
+#pragma unroll
+      for (int e = 0; e < 4; e++)
+        o4[e] = pack_bf16(__uint_as_float(w[e] << 16) * scale, __uint_as_float(w[e] & 0xFFFF0000u) * scale);
+      qf[s] = __builtin_bit_cast(bf16x8, make_uint4(o4[0], o4[1], o4[2], o4[3]));
+    } else {
+      qf[s] = __builtin_bit_cast(bf16x8, raw);
+    }
+  }
+}
+
+// LDS read offsets of the MFMA operands.  K: MFMA row n holds key row_key(n); k-step
+// st reads dims h*D/2 + 8st .. +8, i.e. chunk h*CPR/2 + st, stored swizzled.
+template <int D>
+__device__ __forceinline__ void k_offsets(int (&koff)[Geom<D>::KSTEPS], int n, int h) {
+  const int r = row_key(n);
+#pragma unroll
+  for (int st = 0; st < Geom<D>::KSTEPS; st++)
+    koff[st] = r * (D * 2) + (((h * (Geom<D>::CPR / 2) + st) ^ (r % Geom<D>::CPR)) * 16);
+}
+
+// V^T: dim 32b + n, slots 8h..8h+7 of a page.
+__device__ __forceinline__ int v_offset(int n, int h) { return n * 32 + ((h ^ ((n >> 3) & 1)) * 16); }
+
+// Epilogue: lane (n, h) holds dims 32*b + 8*(i/4) + 4*h + i%4 of its row; O = o * vscale / l
+// rounded to bf16 with the LSE, or the fp32 partial result of a split part.
+template <int D>
+__device__ __forceinline__ void write_result(const AttnParams& p, const Rows& r, const f32x16 (&o)[Geom<D>::DB],
+                                             float l_run, float m_run, float vscale) {
+  using G = Geom<D>;
+  const float l_tot = pair_sum(l_run);
+  const float inv = l_tot > 0.0f ? vscale / l_tot : 0.0f;
+  const float lse_val = l_tot > 0.0f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+  if (r.u.part < 0) {
+    if (r.valid) {
+      uint16_t* dst = p.out + ((size_t)(r.u.qo_row0 + r.tok) * p.num_q_heads + r.hq) * D;
+#pragma unroll
+      for (int b = 0; b < G::DB; b++) {
+#pragma unroll
+        for (int g4 = 0; g4 < 4; g4++) {
+          uint2 w;
+          w.x = pack_bf16(o[b][4 * g4 + 0] * inv, o[b][4 * g4 + 1] * inv);
+          w.y = pack_bf16(o[b][4 * g4 + 2] * inv, o[b][4 * g4 + 3] * inv);
+          *(uint2*)(dst + 32 * b + 8 * g4 + 4 * r.h) = w;
+        }
+      }
+      if (p.lse != nullptr && r.h == 0) p.lse[(size_t)(r.u.qo_row0 + r.tok) * p.num_q_heads + r.hq] = lse_val;
+    }
+  } else {
+    float* dst = p.o_part + ((size_t)r.u.part * kTileRows + r.rho) * D;
+#pragma unroll
+    for (int b = 0; b < G::DB; b++) {
+#pragma unroll
+      for (int g4 = 0; g4 < 4; g4++) {
+        f32x4 w;
+        w[0] = o[b][4 * g4 + 0] * inv;
+        w[1] = o[b][4 * g4 + 1] * inv;
+        w[2] = o[b][4 * g4 + 2] * inv;
+        w[3] = o[b][4 * g4 + 3] * inv;
+        *(f32x4*)(dst + 32 * b + 8 * g4 + 4 * r.h) = w;
+      }
+    }
+    if (r.h == 0) p.lse_part[(size_t)r.u.part * kTileRows + r.rho] = lse_val;
+  }
+}
+
+// ---------------------------------------------------------------- bf16 pool
+
+template <int D>
 __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams p) {
   using G = Geom<D>;
   __shared__ __attribute__((aligned(1024))) uint8_t k_lds[G::NSTAGE][G::TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t v_lds[G::NSTAGE][G::TILE_BYTES];
 
-  // the work item, read with scalar loads: every index derived from it stays uniform
-  AttnUnit u;
-  {
-    const const_i32_ptr w = (const_i32_ptr)(p.units + blockIdx.x);
-    u.qo_row0 = w[0];
-    u.q_pos0 = w[1];
-    u.page_base = w[2];
-    u.key_begin = w[3];
-    u.key_end = w[4];
-    u.head_ntok = w[5];
-    u.part = w[6];
-    u.req = w[7];
-  }
+  const Rows r = rows_of(p);
+  const AttnUnit& u = r.u;
   if (u.key_end <= u.key_begin) return;  // padding entry: uniform exit
-
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int n = lane & 31;  // query row within the wave's block / MFMA row
-  const int h = lane >> 5;  // half of the wave
-  const int kv_head = u.head_ntok >> 16;
-  const int ntok = u.head_ntok & 0xFFFF;
+  const int lane = r.lane, wave = r.wave, h = r.h, qpos = r.qpos;
   const Ctx c{(const_i32_ptr)p.page_ids + u.page_base, p.k_pool, p.v_pool, p.num_kv_heads, u.page_base, u.key_end,
-              kv_head};
+              r.kv_head};
+  const float scale = p.scale_log2;  // softmax scale of the scores in log2 units
 
-  // this lane's query row: row rho = token * group + head-in-group
-  const int rho = wave * 32 + n;
-  const int tok = rho / p.group;
-  const int hq = kv_head * p.group + (rho - tok * p.group);
-  const bool valid = tok < ntok;
-  const int qpos = u.q_pos0 + tok;
-
-  // softmax scale of the scores in log2 units (with the pool's k_scale on fp8)
-  constexpr bool FOLD = FP8;  // scale and running maximum folded into the products
-  float scale = p.scale_log2;
-  float vscale = 1.0f;
-  if constexpr (FP8) {
-    scale *= p.k_scale[kv_head];
-    vscale = p.v_scale[kv_head];
-  }
-
-  // Q^T operand: k-slot (h, j) of k-step s holds dim h*D/2 + 8s + j; folded: times
-  // scale, rounded once to bf16
   bf16x8 qf[G::KSTEPS];
-  {
-    const uint4* src = (const uint4*)(p.q + ((size_t)(u.qo_row0 + tok) * p.num_q_heads + hq) * D + h * (D / 2));
-#pragma unroll
-    for (int s = 0; s < G::KSTEPS; s++) {
-      const uint4 raw = valid ? src[s] : make_uint4(0, 0, 0, 0);
-      if constexpr (FOLD) {
-        const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-        uint32_t o4[4];
-#pragma unroll
-        for (int e = 0; e < 4; e++)
-          o4[e] = pack_bf16(__uint_as_float(w[e] << 16) * scale, __uint_as_float(w[e] & 0xFFFF0000u) * scale);
-        qf[s] = __builtin_bit_cast(bf16x8, make_uint4(o4[0], o4[1], o4[2], o4[3]));
-      } else {
-        qf[s] = __builtin_bit_cast(bf16x8, raw);
-      }
-    }
-  }
-
-  // LDS read offsets.  K: MFMA row n holds key row_key(n); k-step st reads dims
-  // h*D/2 + 8st .. +8, i.e. chunk h*CPR/2 + st, stored swizzled.  V^T: dim 32b + n,
-  // slots 8h..8h+7 of page hf.
+  load_q<D, false>(qf, p, r, scale);
   int koff[G::KSTEPS];
-  {
-    const int r = row_key(n);
-#pragma unroll
-    for (int st = 0; st < G::KSTEPS; st++) koff[st] = r * (D * 2) + (((h * (G::CPR / 2) + st) ^ (r % G::CPR)) * 16);
-  }
-  const int vbase = n * 32 + ((h ^ ((n >> 3) & 1)) * 16);
+  k_offsets<D>(koff, r.n, h);
+  const int vbase = v_offset(r.n, h);
   LoadSlot<D> slot[G::PER_WAVE];
 #pragma unroll
   for (int it = 0; it < G::PER_WAVE; it++) slot[it].init(it * kWaves + wave, lane);
@@ -410,10 +471,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   f32x16 o[G::DB];
 #pragma unroll
   for (int b = 0; b < G::DB; b++) o[b] = f32x16{};
-  // running maximum m of the lane's row (log2 units); folded: -m is also the score
-  // tiles' accumulator input, and m starts at the first tile's row maximum
-  float m_run = FOLD ? 0.0f : -1e30f, l_run = 0.0f, mx;
-  f32x16 cneg = f32x16{};
+  float m_run = -1e30f, l_run = 0.0f, mx;  // running maximum (log2 units) and sum of the lane's row
+  const f32x16 zero = f32x16{};
 
   const int kb0 = u.key_begin;
   const int n_tiles = (u.key_end - kb0 + kBN - 1) / kBN;
@@ -422,26 +481,18 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   n_full = n_full < 0 ? 0 : (n_full > n_tiles ? n_tiles : n_full);
   const int last_whole = (u.key_end - kb0) / kBN;  // tiles [0, last_whole) lie inside [kb0, key_end)
 
-  // Issue this wave's pieces of K(tk) and V(tv) into the ring (tk / tv < 0: skip).
-  // bf16 pool: direct loads, except for a V tile reaching past key_end, which is
-  // loaded, zeroed and written synchronously (V pieces go first, so that wait only
-  // covers older loads).  Returns the direct loads issued.
-  // fp8 pool: every piece is loaded as 8 raw codes into registers (`fresh`); they
-  // are converted to bf16 and written to the ring at the end of the next iteration
-  // (`held`), so each load has a whole iteration to arrive.
+  // Issue this wave's pieces of K(tk) and V(tv) into the ring (tk / tv < 0: skip):
+  // direct loads, except for a V tile reaching past key_end, which is loaded, zeroed
+  // and written synchronously (V pieces go first, so that wait only covers older
+  // loads).  Returns the direct loads issued.
   // Per slot: the pool base of this KV head, and the page id of the tile the slot
   // loads next (read one iteration ahead, so the scalar load is off the critical path).
-  constexpr int EBYTES = FP8 ? 1 : 2;
-  const uint32_t page_bytes = (uint32_t)p.num_kv_heads * (kPageSize * D * EBYTES);
+  const uint32_t page_bytes = (uint32_t)p.num_kv_heads * (kPageSize * D * 2);
   const char* head_base[G::PER_WAVE];
   uint32_t pid[G::PER_WAVE];
-  uint2 fresh[G::PER_WAVE], held[G::PER_WAVE];
-  int held_tk = -1, held_tv = -1;
 #pragma unroll
-  for (int it = 0; it < G::PER_WAVE; it++) {
-    head_base[it] = (const char*)(it >= G::K_SLOTS ? p.v_pool : p.k_pool) + (size_t)kv_head * (kPageSize * D * EBYTES);
-    fresh[it] = held[it] = make_uint2(0, 0);
-  }
+  for (int it = 0; it < G::PER_WAVE; it++)
+    head_base[it] = (const char*)(it >= G::K_SLOTS ? p.v_pool : p.k_pool) + (size_t)r.kv_head * (kPageSize * D * 2);
   const int lp0 = (int)((uint32_t)kb0 / kPageSize);
   auto page_for = [&](int it, int t) -> uint32_t {
     return (uint32_t)page_of(c, lp0 + t * (kBN / kPageSize) + slot[it].page_sel);
@@ -455,109 +506,53 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       const int t = is_v ? tv : tk;
       if (t < 0) continue;
       const char* block = page_block(head_base[it], pid[it], page_bytes);
-      if constexpr (FP8) {
-        fresh[it] = *(const uint2*)(block + s.off / 2);
+      uint8_t* tile = is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
+      if (is_v && t >= last_whole) {
+        *(uint4*)(tile + s.j * 1024 + lane * 16) = mask_v_tail<D>(*(const uint4*)(block + s.off), s, kb0 + t * kBN, u.key_end);
       } else {
-        uint8_t* tile = is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
-        if (is_v && t >= last_whole) {
-          *(uint4*)(tile + s.j * 1024 + lane * 16) = mask_v_tail<D>(*(const uint4*)(block + s.off), s, kb0 + t * kBN, u.key_end);
-        } else {
-          issue_direct<D>(s, block, tile);
-          direct++;
-        }
+        issue_direct<D>(s, block, tile);
+        direct++;
       }
       pid[it] = page_for(it, t + 1);  // next iteration's tile for this slot
     }
     return direct;
   };
-  // Steady state (K(tk) and V(tv) both lie inside [kb0, key_end)): nothing is
-  // conditional.
-  auto issue_whole = [&](int tk, int tv) {
-#pragma unroll
-    for (int it = G::PER_WAVE - 1; it >= 0; it--) {
-      const LoadSlot<D>& s = slot[it];
-      const bool is_v = it >= G::K_SLOTS;
-      const int t = is_v ? tv : tk;
-      const char* block = page_block(head_base[it], pid[it], page_bytes);
-      if constexpr (FP8) {
-        fresh[it] = *(const uint2*)(block + s.off / 2);
-      } else {
-        issue_direct<D>(s, block, is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE]);
-      }
-      pid[it] = page_for(it, t + 1);
-    }
-  };
-  // fp8: convert the codes in `codes` for K(tk), V(tv) and write them to the ring.
-  auto store_codes = [&](const uint2 (&codes)[G::PER_WAVE], int tk, int tv, auto whole) {
-    constexpr bool WHOLE = decltype(whole)::value;
-#pragma unroll
-    for (int it = 0; it < G::PER_WAVE; it++) {
-      const bool is_v = it >= G::K_SLOTS;
-      const int t = is_v ? tv : tk;
-      if (!WHOLE && t < 0) continue;
-      uint4 x = fp8x8_to_bf16x8(codes[it]);
-      if (!WHOLE && is_v && t >= last_whole) x = mask_v_tail<D>(x, slot[it], kb0 + t * kBN, u.key_end);
-      uint8_t* tile = is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
-      *(uint4*)(tile + slot[it].j * 1024 + lane * 16) = x;
-    }
-  };
-  // end of an iteration that issued K(tk), V(tv): the fp8 codes held since the
-  // previous iteration go to the ring, this iteration's become the held ones
-  auto finish = [&](int tk, int tv, auto whole) {
-    if constexpr (FP8) {
-      store_codes(held, held_tk, held_tv, whole);
-#pragma unroll
-      for (int it = 0; it < G::PER_WAVE; it++) held[it] = fresh[it];
-      held_tk = tk;
-      held_tv = tv;
-    }
-  };
 
-  // ---- prologue.  bf16: K(0), K(1), V(0) resident; K(2), V(1) and then K(3), V(2)
-  // in flight (they play the loads of iterations -2 and -1).  fp8: K(0..2), V(0..1)
-  // resident, the codes of K(3), V(2) held.
+  // ---- prologue: K(0), K(1), V(0) resident; K(2), V(1) and then K(3), V(2) in flight
+  // (they play the loads of iterations -2 and -1)
   auto tile_or_none = [&](int t) { return t < n_tiles ? t : -1; };
   int issued_prev = 0;
 #pragma unroll
   for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 0);
-  if constexpr (FP8) {
-    issue(0, 0);
-    store_codes(fresh, 0, 0, False{});
-    issue(tile_or_none(1), tile_or_none(1));
-    store_codes(fresh, tile_or_none(1), tile_or_none(1), False{});
-    issue(tile_or_none(2), -1);
-    store_codes(fresh, tile_or_none(2), -1, False{});
-    issue(tile_or_none(3), tile_or_none(2));
-    held_tk = tile_or_none(3);
-    held_tv = tile_or_none(2);
+  issue(0, 0);
 #pragma unroll
-    for (int it = 0; it < G::PER_WAVE; it++) held[it] = fresh[it];
-  } else {
-    issue(0, 0);
+  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 1);
+  issue(tile_or_none(1), -1);
+  wait_vmcnt<0>();
 #pragma unroll
-    for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 1);
-    issue(tile_or_none(1), -1);
-    wait_vmcnt<0>();
-#pragma unroll
-    for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, it >= G::K_SLOTS ? 1 : 2);
-    issue(tile_or_none(2), tile_or_none(1));
-    issued_prev = issue(tile_or_none(3), tile_or_none(2));  // pid already advanced to K(3), V(2)
-  }
+  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, it >= G::K_SLOTS ? 1 : 2);
+  issue(tile_or_none(2), tile_or_none(1));
+  issued_prev = issue(tile_or_none(3), tile_or_none(2));  // pid already advanced to K(3), V(2)
   __syncthreads();
 
   f32x16 sa[kKB], sb[kKB];
   bf16x8 pb[2 * kKB];
-  qk_tile<D>(sa, k_lds[0], koff, qf, cneg);
+  qk_tile<D>(sa, k_lds[0], koff, qf, zero);
   mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
-  if constexpr (FOLD) {
-    // the first tile's row maximum is finite (its first key is visible to every row)
-    m_run = mx;
-#pragma unroll
-    for (int kb = 0; kb < kKB; kb++) sa[kb] -= mx;
-    cneg = -mx;
-    mx = 0.0f;
-  }
   __syncthreads();  // every wave has read K(0) before iteration 0 refills its slot with K(4)
+
+  // lazy rescale before the scores of the tile whose maximum is mx are exponentiated:
+  // the reference maximum moves only when a row outgrows it by 2^8
+  auto rescale = [&]() {
+    if (__any(mx * scale > m_run + kRescaleThreshold)) {
+      const float m_new = fmaxf(m_run, mx * scale);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < G::DB; b++) o[b] *= alpha;
+      m_run = m_new;
+    }
+  };
 
   // One pipelined iteration: consumes S(t) (scores in s_cur, maximum in mx), produces
   // S(t+1) into s_nxt with its maximum, accumulates P(t) V(t).  Issues K(t+4) and
@@ -565,36 +560,6 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   // which were issued two iterations earlier.
   // In the unmasked variant tile t+1 exists and needs no mask, so the compute part
   // is one branch-free block in which MFMA and the softmax VALU work interleave.
-  // lazy rescale before the scores of the tile whose maximum is mx are exponentiated:
-  // the reference maximum moves only when a row outgrows it by 2^8
-  // (folded: mx and the tile st are relative to m, and st moves with m)
-  auto rescale = [&](f32x16 (&st)[kKB]) {
-    if constexpr (FOLD) {
-      if (__any(mx > kRescaleThreshold)) {
-        const float d = fmaxf(mx, 0.0f);
-        const float alpha = __builtin_amdgcn_exp2f(-d);
-        l_run *= alpha;
-#pragma unroll
-        for (int b = 0; b < G::DB; b++) o[b] *= alpha;
-#pragma unroll
-        for (int kb = 0; kb < kKB; kb++) st[kb] -= d;
-        m_run += d;
-        mx -= d;
-        cneg = -m_run;
-      }
-    } else {
-      if (__any(mx * scale > m_run + kRescaleThreshold)) {
-        const float m_new = fmaxf(m_run, mx * scale);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        l_run *= alpha;
-#pragma unroll
-        for (int b = 0; b < G::DB; b++) o[b] *= alpha;
-        m_run = m_new;
-      }
-    }
-  };
-  if constexpr (FP8 && !FOLD) rescale(sa);
-
   auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole, auto stage) {
     constexpr bool MASKED = decltype(masked)::value;
     constexpr bool WHOLE = decltype(whole)::value;
@@ -615,55 +580,43 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
     if constexpr (SPREAD) {
 #pragma unroll
       for (int it = 0; it < G::PER_WAVE; it++) blk[it] = page_block(head_base[it], pid[it], page_bytes);
-    } else if constexpr (WHOLE) {
-      issue_whole(tk, tv);
     } else {
       issued = issue(tk, tv);
     }
 
-    // bf16 pool: the check for S(t) comes here; the fp8 kernel, tighter on
-    // registers, takes it at the end of the previous iteration instead
-    if constexpr (!FP8) rescale(s_cur);
+    rescale();
 
     if constexpr (MASKED) {
-      if (has_next) qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, cneg);
-      l_run = exp_pack<FOLD>(s_cur, pb, l_run, m_run, scale);
+      if (has_next) qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, zero);
+      l_run = exp_pack<false>(s_cur, pb, l_run, m_run, scale);
       pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
       if (has_next) mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
     } else if constexpr (SPREAD) {
-      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, cneg, [&](int i) {
+      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, zero, [&](int i) {
         const int it = G::PER_WAVE - 1 - i;
         const bool is_v = it >= G::K_SLOTS;
-        if constexpr (FP8) fresh[it] = *(const uint2*)(blk[it] + slot[it].off / 2);
-        else issue_direct<D>(slot[it], blk[it], is_v ? v_lds[ring(3)] : k_lds[ring(4)]);  // V(t+3), K(t+4)
+        issue_direct<D>(slot[it], blk[it], is_v ? v_lds[ring(3)] : k_lds[ring(4)]);  // V(t+3), K(t+4)
       });
-      l_run = exp_pack<FOLD>(s_cur, pb, l_run, m_run, scale);
+      l_run = exp_pack<false>(s_cur, pb, l_run, m_run, scale);
       pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
       mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     } else {
-      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, cneg);
-      l_run = exp_pack<FOLD>(s_cur, pb, l_run, m_run, scale);
+      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, zero);
+      l_run = exp_pack<false>(s_cur, pb, l_run, m_run, scale);
       pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
       mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     }
 
-    if constexpr (FP8) {
-      if (!MASKED || has_next) rescale(s_nxt);  // for S(t+1), exponentiated in the next iteration
-    }
     if constexpr (SPREAD) {
       // next page ids, read after this iteration's last LDS operand read so that no
       // operand wait has to cover an outstanding scalar load
 #pragma unroll
       for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, (it >= G::K_SLOTS ? tv : tk) + 1);
     }
-    if constexpr (FP8) {
-      finish(tk, tv, whole);
-    } else {
-      // K(t+2), V(t+1) (issued two iterations ago) must be in LDS before the barrier
-      if constexpr (WHOLE) wait_vmcnt<2 * G::PER_WAVE>();
-      else wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
-      issued_prev = issued;
-    }
+    // K(t+2), V(t+1) (issued two iterations ago) must be in LDS before the barrier
+    if constexpr (WHOLE) wait_vmcnt<2 * G::PER_WAVE>();
+    else wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
+    issued_prev = issued;
     __syncthreads();
   };
 
@@ -701,42 +654,331 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   }
 
   wait_vmcnt<0>();  // no load into this workgroup's LDS may outlive it
+  write_result<D>(p, r, o, l_run, m_run, 1.0f);
+}
 
-  // ---- epilogue: lane (n, h) holds dims 32*b + 8*(i/4) + 4*h + i%4 of its row
-  const float l_tot = pair_sum(l_run);
-  const float inv = l_tot > 0.0f ? vscale / l_tot : 0.0f;
-  const float lse_val = l_tot > 0.0f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
-  if (u.part < 0) {
-    if (valid) {
-      uint16_t* dst = p.out + ((size_t)(u.qo_row0 + tok) * p.num_q_heads + hq) * D;
-#pragma unroll
-      for (int b = 0; b < G::DB; b++) {
-#pragma unroll
-        for (int g4 = 0; g4 < 4; g4++) {
-          uint2 w;
-          w.x = pack_bf16(o[b][4 * g4 + 0] * inv, o[b][4 * g4 + 1] * inv);
-          w.y = pack_bf16(o[b][4 * g4 + 2] * inv, o[b][4 * g4 + 3] * inv);
-          *(uint2*)(dst + 32 * b + 8 * g4 + 4 * h) = w;
-        }
-      }
-      if (p.lse != nullptr && h == 0) p.lse[(size_t)(u.qo_row0 + tok) * p.num_q_heads + hq] = lse_val;
+// ---------------------------------------------------------------- fp8 pool
+//
+// The e4m3 codes of K(t) and V(t) come straight from the pool into a 4-slot LDS
+// staging ring (global_load_lds_dwordx4, 1 KiB of codes per wave-wide load, half
+// the loads of a bf16 tile), in the pool's own order: a K tile as 64 rows of D
+// codes, a V tile as [page][dim][16 slots].  Staging slot s holds the "pair"
+// s = {K(s+1), V(s)} (K runs one tile ahead, as in the products).  Every CU
+// converts each code once: iteration t converts pair t+1 -- K(t+2) into bf16 K
+// buffer t % 2 and V(t+1) into V^T buffer (t+1) % 2, in the layouts the bf16
+// kernel uses -- while it multiplies K(t+1) and V(t) from the other buffers, so
+// two bf16 buffers of each suffice.  Pair t+3 is loaded in iteration t and waited
+// for at the end of iteration t+1, two iterations before its conversion reads it
+// (loads stay in flight for one iteration and a barrier).  The conversion is exact
+// (every e4m3 value is a bf16 value); k_scale is folded into Q with the softmax
+// scale, v_scale into the epilogue.
+
+template <int D>
+struct Geom8 {
+  static constexpr int TILE_CODES = kBN * D;              // bytes of codes of one K (or V) tile
+  static constexpr int PAIR = 2 * TILE_CODES;             // a staging slot: K codes, then V codes
+  static constexpr int KINSTR = TILE_CODES / 1024;        // 1 KiB direct loads per tile
+  static constexpr int NDMA = 2 * KINSTR / kWaves;        // direct loads per wave and pair
+  static constexpr int CONV = PAIR / 16 / kAttnThreads;   // 16-code chunks converted per lane and pair
+  static constexpr int KCHUNKS = TILE_CODES / 16;         // 16-code chunks of a K tile
+  static constexpr int CPR16 = D / 16;                    // 16-code chunks per K row
+  static constexpr int NSTG = 4;                          // staging slots
+  static constexpr int NBUF = 2;                          // bf16 buffers of K and of V^T
+  static_assert(NDMA >= 1 && (2 * KINSTR) % kWaves == 0, "direct loads must spread evenly over waves");
+  static_assert(CONV >= 1 && PAIR % (16 * kAttnThreads) == 0, "conversion must spread evenly over lanes");
+};
+
+// One wave's direct load of a pair: load g = wave + 8 * it is K load g (g < KINSTR)
+// or V load g - KINSTR; lane l of load j moves 16 codes to staging byte
+// 1024 j + 16 l of the tile's region.
+template <int D>
+struct CodeLoad {
+  bool is_v;
+  int j;
+  int off;       // byte offset of the lane's 16 codes inside the (page, head) block
+  int page_sel;  // page of the tile
+  __device__ __forceinline__ void init(int g, int lane) {
+    using G8 = Geom8<D>;
+    is_v = g >= G8::KINSTR;
+    j = is_v ? g - G8::KINSTR : g;
+    const int q = 64 * j + lane;
+    if (is_v) {  // [page][dim][16 slots]: chunk q = (page q / D, dim q % D)
+      page_sel = q / D;
+      off = (q % D) * kPageSize;
+    } else {     // 64 rows of D codes: chunk q = (key q / CPR16, 16 dims q % CPR16)
+      const int key = q / G8::CPR16;
+      page_sel = key / kPageSize;
+      off = (key % kPageSize) * D + (q % G8::CPR16) * 16;
     }
-  } else {
-    float* dst = p.o_part + ((size_t)u.part * kTileRows + rho) * D;
-#pragma unroll
-    for (int b = 0; b < G::DB; b++) {
-#pragma unroll
-      for (int g4 = 0; g4 < 4; g4++) {
-        f32x4 w;
-        w[0] = o[b][4 * g4 + 0] * inv;
-        w[1] = o[b][4 * g4 + 1] * inv;
-        w[2] = o[b][4 * g4 + 2] * inv;
-        w[3] = o[b][4 * g4 + 3] * inv;
-        *(f32x4*)(dst + 32 * b + 8 * g4 + 4 * h) = w;
-      }
-    }
-    if (h == 0) p.lse_part[(size_t)u.part * kTileRows + rho] = lse_val;
+    // a load's 64 chunks lie in one page (D >= 64): the same for every lane, which
+    // keeps the page-id lookups scalar
+    page_sel = __builtin_amdgcn_readfirstlane(page_sel);
   }
+};
+
+// One lane's conversion of a pair: chunk q = i * 512 + wave * 64 + lane of the
+// staging slot (K chunks first), at staging byte 16 q, becomes two bf16 chunks at
+// dst and dst ^ 16 of its tile (the two 16-byte halves of a 32-byte-aligned pair
+// of chunks, in the order the swizzle gives).
+//   K chunk (key, c16), 16 dims from 16 c16: bf16 chunks 2 c16, 2 c16 + 1 of row key.
+//   V chunk (page pg, dim d), 16 slots: slots 0..7 and 8..15 of dim row d of page pg.
+template <int D>
+__device__ __forceinline__ int conv_dst(int q) {
+  using G8 = Geom8<D>;
+  using G = Geom<D>;
+  if (q >= G8::KCHUNKS) {
+    const int qv = q - G8::KCHUNKS, pg = qv / D, d = qv % D;
+    return pg * (D * 32) + d * 32 + ((d >> 3) & 1) * 16;
+  }
+  const int key = q / G8::CPR16, c16 = q % G8::CPR16;
+  return key * (D * 2) + ((2 * c16) ^ (key % G::CPR)) * 16;
+}
+
+// Zero the bf16 values of V^T slots at or past key_end (8 slots starting at key).
+__device__ __forceinline__ uint4 zero_past(uint4 x, int key, int key_end) {
+  uint32_t* xw = (uint32_t*)&x;
+#pragma unroll
+  for (int e = 0; e < 4; e++) {
+    const uint32_t lo = (key + 2 * e < key_end) ? 0xFFFFu : 0u;
+    const uint32_t hi = (key + 2 * e + 1 < key_end) ? 0xFFFF0000u : 0u;
+    xw[e] &= (lo | hi);
+  }
+  return x;
+}
+
+template <int D>
+__global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_fp8_kernel(AttnParams p) {
+  using G = Geom<D>;
+  using G8 = Geom8<D>;
+  // one block, bf16 buffers first: every MFMA operand read and conversion write then
+  // lies below 64 KiB and addresses with an immediate offset
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * G8::NBUF * G::TILE_BYTES + G8::NSTG * G8::PAIR];
+  uint8_t(*k_lds)[G::TILE_BYTES] = (uint8_t(*)[G::TILE_BYTES])lds;
+  uint8_t(*v_lds)[G::TILE_BYTES] = (uint8_t(*)[G::TILE_BYTES])(lds + G8::NBUF * G::TILE_BYTES);
+  uint8_t(*stg)[G8::PAIR] = (uint8_t(*)[G8::PAIR])(lds + 2 * G8::NBUF * G::TILE_BYTES);
+
+  const Rows r = rows_of(p);
+  const AttnUnit& u = r.u;
+  if (u.key_end <= u.key_begin) return;  // padding entry: uniform exit
+  const int lane = r.lane, wave = r.wave, h = r.h, qpos = r.qpos;
+  const Ctx c{(const_i32_ptr)p.page_ids + u.page_base, p.k_pool, p.v_pool, p.num_kv_heads, u.page_base, u.key_end,
+              r.kv_head};
+  // Q times softmax scale (log2 units) times k_scale: the products come out in the
+  // exponent's units
+  const float vscale = p.v_scale[r.kv_head];
+  bf16x8 qf[G::KSTEPS];
+  load_q<D, true>(qf, p, r, p.scale_log2 * p.k_scale[r.kv_head]);
+  int koff[G::KSTEPS];
+  k_offsets<D>(koff, r.n, h);
+  const int vbase = v_offset(r.n, h);
+
+  f32x16 o[G::DB];
+#pragma unroll
+  for (int b = 0; b < G::DB; b++) o[b] = f32x16{};
+  // running maximum m of the lane's row (log2 units), -m as the score tiles'
+  // accumulator input; m starts at the first tile's row maximum
+  float m_run = 0.0f, l_run = 0.0f, mx;
+  f32x16 cneg = f32x16{};
+
+  const int kb0 = u.key_begin;
+  const int n_tiles = (u.key_end - kb0 + kBN - 1) / kBN;
+  int n_full = (u.q_pos0 + 1 - kb0) / kBN;
+  n_full = n_full < 0 ? 0 : (n_full > n_tiles ? n_tiles : n_full);
+  const int last_whole = (u.key_end - kb0) / kBN;
+
+  // direct loads: per wave, the pool base of this KV head and the page id of the
+  // tile each load fetches next (read one pair ahead)
+  const uint32_t page_bytes = (uint32_t)p.num_kv_heads * (kPageSize * D);
+  CodeLoad<D> ld[G8::NDMA];
+  const char* head_base[G8::NDMA];
+  uint32_t pid[G8::NDMA];
+#pragma unroll
+  for (int it = 0; it < G8::NDMA; it++) {
+    ld[it].init(wave + kWaves * it, lane);
+    head_base[it] = (const char*)(ld[it].is_v ? p.v_pool : p.k_pool) + (size_t)r.kv_head * (kPageSize * D);
+  }
+  // conversion chunks of this lane: q = i * 512 + wave * 64 + lane
+  int cdst[G8::CONV];
+#pragma unroll
+  for (int i = 0; i < G8::CONV; i++) cdst[i] = conv_dst<D>(i * kAttnThreads + wave * 64 + lane);
+  const int lp0 = (int)((uint32_t)kb0 / kPageSize);
+  // tile of pair s that load `it` fetches: K(s+1) or V(s)
+  auto tile_of = [&](int it, int s) { return ld[it].is_v ? s : s + 1; };
+  auto page_for = [&](int it, int tt) -> uint32_t {  // tt >= 0
+    return (uint32_t)page_of(c, lp0 + tt * (kBN / kPageSize) + ld[it].page_sel);
+  };
+  auto dma = [&](int it, uint8_t* slot, const char* block) {
+    const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)(
+        slot + (ld[it].is_v ? G8::TILE_CODES : 0) + ld[it].j * 1024);
+    lds_dma_16(block, ld[it].off, lds);
+  };
+  // load pair s (tiles that do not exist are skipped); returns the loads issued
+  auto issue = [&](int s) -> int {
+    int n = 0;
+#pragma unroll
+    for (int it = 0; it < G8::NDMA; it++) {
+      const int tt = tile_of(it, s);
+      if (tt < 0 || tt >= n_tiles) continue;
+      dma(it, stg[s & 3], page_block(head_base[it], pid[it], page_bytes));
+      n++;
+      pid[it] = page_for(it, tt + 1);
+    }
+    return n;
+  };
+  // convert pair s from staging slot `src` into the bf16 buffers kdst (K(s+1)) and
+  // vdst (V(s))
+  auto convert = [&](int s, auto whole, const uint8_t* src, uint8_t* kdst, uint8_t* vdst) {
+    constexpr bool WHOLE = decltype(whole)::value;
+#pragma unroll
+    for (int i = 0; i < G8::CONV; i++) {
+      const int q0 = i * kAttnThreads + wave * 64;  // uniform
+      const bool is_v = q0 >= G8::KCHUNKS;
+      const int tt = is_v ? s : s + 1;
+      if (!WHOLE && (tt < 0 || tt >= n_tiles)) continue;
+      const uint4 x = *(const uint4*)(src + (q0 + lane) * 16);
+      uint4 lo = fp8x8_to_bf16x8(make_uint2(x.x, x.y));
+      uint4 hi = fp8x8_to_bf16x8(make_uint2(x.z, x.w));
+      if (!WHOLE && is_v && tt >= last_whole) {
+        // first key of the chunk's 16 slots: page (q - KCHUNKS) / D of tile tt
+        const int key = kb0 + tt * kBN + ((q0 + lane - G8::KCHUNKS) / D) * kPageSize;
+        lo = zero_past(lo, key, u.key_end);
+        hi = zero_past(hi, key + 8, u.key_end);
+      }
+      uint8_t* dst = is_v ? vdst : kdst;
+      *(uint4*)(dst + cdst[i]) = lo;
+      *(uint4*)(dst + (cdst[i] ^ 16)) = hi;
+    }
+  };
+
+  // ---- prologue: pairs -1 = {K(0)}, 0, 1, 2 loaded; -1 and 0 converted (K(0), K(1),
+  // V(0) in bf16), 1 resident, 2 in flight
+#pragma unroll
+  for (int it = 0; it < G8::NDMA; it++) pid[it] = page_for(it, 0);
+  issue(-1);
+  issue(0);
+  issue(1);
+  const int in_flight = issue(2);
+  wait_issued<G8::NDMA>(in_flight);
+  __syncthreads();
+  convert(-1, False{}, stg[3], k_lds[0], v_lds[1]);
+  convert(0, False{}, stg[0], k_lds[1], v_lds[0]);
+  __syncthreads();
+
+  f32x16 sa[kKB], sb[kKB];
+  bf16x8 pb[2 * kKB];
+  qk_tile<D>(sa, k_lds[0], koff, qf, cneg);
+  mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
+  // the reference point: the first tile's row maximum (finite: the tile's first key
+  // is visible to every row of the unit)
+  m_run = mx;
+#pragma unroll
+  for (int kb = 0; kb < kKB; kb++) sa[kb] -= mx;
+  cneg = -mx;
+  mx = 0.0f;
+  __syncthreads();  // every wave has read K(0) before iteration 0 converts K(2) into its buffer
+
+  // lazy rescale before the tile st (its row maximum mx, both relative to m) is
+  // exponentiated: m moves only when a row outgrows it by 2^8, and st moves with it
+  auto rescale = [&](f32x16 (&st)[kKB]) {
+    if (__any(mx > kRescaleThreshold)) {
+      const float d = fmaxf(mx, 0.0f);
+      const float alpha = __builtin_amdgcn_exp2f(-d);
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < G::DB; b++) o[b] *= alpha;
+#pragma unroll
+      for (int kb = 0; kb < kKB; kb++) st[kb] -= d;
+      m_run += d;
+      mx -= d;
+      cneg = -m_run;
+    }
+  };
+
+  // One pipelined iteration: consumes S(t), produces S(t+1) from bf16 K(t+1) with its
+  // maximum, accumulates P(t) V(t), loads pair t+3 and converts pair t+1.  Before the
+  // barrier only this iteration's loads may still be in flight.
+  auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole, auto stage) {
+    constexpr bool MASKED = decltype(masked)::value;
+    constexpr bool WHOLE = decltype(whole)::value;
+    constexpr int ST = decltype(stage)::value;
+    auto buf = [&](int d) -> int {  // bf16 buffer of tile t + d
+      if constexpr (ST >= 0) return (ST + d) % G8::NBUF;
+      else return (t + d) % G8::NBUF;
+    };
+    auto slot_of = [&](int d) -> int {  // staging slot of pair t + d
+      if constexpr (ST >= 0) return (ST + d) % G8::NSTG;
+      else return (t + d) % G8::NSTG;
+    };
+    const int k0 = kb0 + t * kBN;
+    const bool has_next = MASKED ? t + 1 < n_tiles : true;
+    constexpr bool SPREAD = WHOLE && !MASKED;
+    int issued = G8::NDMA;
+    const char* blk[G8::NDMA];
+    if constexpr (SPREAD) {
+#pragma unroll
+      for (int it = 0; it < G8::NDMA; it++) blk[it] = page_block(head_base[it], pid[it], page_bytes);
+    } else {
+      issued = issue(t + 3);
+    }
+    rescale(s_cur);
+    if constexpr (SPREAD) {
+      qk_tile<D>(s_nxt, k_lds[buf(1)], koff, qf, cneg, [&](int i) {
+        if (i < G8::NDMA) dma(i, stg[slot_of(3)], blk[i]);
+      });
+    } else {
+      if (!MASKED || has_next) qk_tile<D>(s_nxt, k_lds[buf(1)], koff, qf, cneg);
+    }
+    convert(t + 1, whole, stg[slot_of(1)], k_lds[buf(2)], v_lds[buf(1)]);
+    l_run = exp_pack<true>(s_cur, pb, l_run, m_run, 0.0f);
+    pv_tile<D>(o, v_lds[buf(0)], vbase, pb);
+    if constexpr (MASKED) {
+      if (has_next) mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
+    } else {
+      mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
+    }
+    if constexpr (SPREAD) {
+#pragma unroll
+      for (int it = 0; it < G8::NDMA; it++) pid[it] = page_for(it, tile_of(it, t + 4));
+    }
+    // pair t+2 (loaded one iteration ago) is converted in the next iteration
+    if constexpr (WHOLE) wait_vmcnt<G8::NDMA>();
+    else wait_issued<G8::NDMA>(issued);
+    __syncthreads();
+  };
+
+  int t = 0;
+  {
+    // steady state: the pair loaded (t+3: K(t+4), V(t+3)) exists and the pair
+    // converted (t+1: K(t+2), V(t+1)) needs no zeroing
+    const int whole_end = (n_tiles - 4 < last_whole - 1 ? n_tiles - 4 : last_whole - 1);
+    for (; t + 4 < n_full && t + 3 < whole_end; t += 4) {
+      iteration(sa, sb, t, False{}, True{}, Stage<0>{});
+      iteration(sb, sa, t + 1, False{}, True{}, Stage<1>{});
+      iteration(sa, sb, t + 2, False{}, True{}, Stage<2>{});
+      iteration(sb, sa, t + 3, False{}, True{}, Stage<3>{});
+    }
+    for (; t + 2 < n_full && t + 1 < whole_end; t += 2) {
+      iteration(sa, sb, t, False{}, True{}, AnyStage{});
+      iteration(sb, sa, t + 1, False{}, True{}, AnyStage{});
+    }
+  }
+  for (; t + 2 < n_full; t += 2) {
+    iteration(sa, sb, t, False{}, False{}, AnyStage{});
+    iteration(sb, sa, t + 1, False{}, False{}, AnyStage{});
+  }
+  if (t + 1 < n_full) {
+    iteration(sa, sb, t, False{}, False{}, AnyStage{});
+    t++;
+#pragma unroll
+    for (int kb = 0; kb < kKB; kb++) sa[kb] = sb[kb];
+  }
+  for (; t < n_tiles; t += 2) {
+    iteration(sa, sb, t, True{}, False{}, AnyStage{});
+    if (t + 1 < n_tiles) iteration(sb, sa, t + 1, True{}, False{}, AnyStage{});
+  }
+
+  wait_vmcnt<0>();  // no load into this workgroup's LDS may outlive it
+  write_result<D>(p, r, o, l_run, m_run, vscale);
 }
 
 // Combine the parts of split tiles: o = sum_p e^{lse_p - M} o_p / sum_p e^{lse_p - M}.
@@ -780,11 +1022,11 @@ hipError_t launch_extend_attention(const AttnParams& p, int64_t n_units, int hea
   if (n_units <= 0) return hipSuccess;
   dim3 grid((unsigned)n_units), block(kAttnThreads);
   if (head_dim == 128) {
-    if (fp8) hipLaunchKernelGGL((extend_attn_kernel<128, true>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((extend_attn_kernel<128, false>), grid, block, 0, stream, p);
+    if (fp8) hipLaunchKernelGGL((extend_attn_fp8_kernel<128>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((extend_attn_kernel<128>), grid, block, 0, stream, p);
   } else {
-    if (fp8) hipLaunchKernelGGL((extend_attn_kernel<64, true>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((extend_attn_kernel<64, false>), grid, block, 0, stream, p);
+    if (fp8) hipLaunchKernelGGL((extend_attn_fp8_kernel<64>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((extend_attn_kernel<64>), grid, block, 0, stream, p);
   }
   return hipGetLastError();
 }
