@@ -333,7 +333,7 @@ def main():
         "store_GBps": round(store_bytes / (store_med * 1e-3) / 1e9, 1),
         "store_roofline_frac": round(store_bytes / (store_med * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
         "roofline": {
-            "kernel": "extend_attn_kernel",
+            "kernel": "extend_attn_fp8_kernel" if w.kv_dtype else "extend_attn_kernel",
             "bound": "mfma",
             "achieved": round(tflops_attn, 2),
             "peak": PEAK_BF16_TFLOPS,
