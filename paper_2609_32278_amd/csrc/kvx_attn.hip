@@ -667,9 +667,10 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
 // converts each code once: iteration t converts pair t+1 -- K(t+2) into bf16 K
 // buffer t % 2 and V(t+1) into V^T buffer (t+1) % 2, in the layouts the bf16
 // kernel uses -- while it multiplies K(t+1) and V(t) from the other buffers, so
-// two bf16 buffers of each suffice.  Pair t+3 is loaded in iteration t and waited
-// for at the end of iteration t+1, two iterations before its conversion reads it
-// (loads stay in flight for one iteration and a barrier).  The conversion is exact
+// two bf16 buffers of each suffice.  Pair t+3 is loaded in iteration t, waited for
+// at the end of iteration t+1 and, after that iteration's barrier, converted in
+// iteration t+2 (each load has the rest of its iteration and the next one to land).
+// The conversion is exact
 // (every e4m3 value is a bf16 value); k_scale is folded into Q with the softmax
 // scale, v_scale into the epilogue.
 

@@ -123,11 +123,16 @@ def test_page_permutation_gives_bitwise_identical_outputs():
     assert torch.equal(outs[0].view(torch.int16), outs[2].view(torch.int16))
 
 
-def test_poisoned_unused_slots_do_not_change_outputs():
+@pytest.mark.parametrize("kv_dtype", [wl.KV_BF16, wl.KV_FP8_E4M3])
+def test_poisoned_unused_slots_do_not_change_outputs(kv_dtype):
+    """Slots past a request's last key (in its last page) hold whatever the pool held;
+    zero, NaN and large values there must leave every output bit unchanged.  On an fp8
+    pool the poison is a code: 0, NaN (0x7F) and the largest finite value (0x7E)."""
     outs = []
-    for fill in (0x0000, 0x7FC0, 0x461C):  # zero, NaN, ~1e4
-        w = wl.make_custom([21, 130], [30, 9], 4, 1, 128, seed=6, num_pages=40)
-        print(f"[extend] poison {fill:#x}", flush=True)
+    fills = (0x0000, 0x7FC0, 0x461C) if kv_dtype == wl.KV_BF16 else (0x00, 0x7F, 0x7E)
+    for fill in fills:
+        w = wl.make_custom([21, 130], [30, 9], 4, 1, 128, kv_dtype=kv_dtype, seed=6, num_pages=40)
+        print(f"[extend] poison {fill:#x} fp8={kv_dtype}", flush=True)
         run = GpuRun(w, fill_bits=fill)
         try:
             run.store()
