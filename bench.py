@@ -129,7 +129,7 @@ def setup(config: str, seed: int = 0, rope: bool = False):
     return dict(w=w, pool=pool, batch=batch, ids=ids, q=q, k_ext=k_ext, v_ext=v_ext, out=out, rope=rk)
 
 
-def run_gpu(config: str, steps: int, warmup: int, rope: bool = False):
+def run_gpu(config: str, steps: int, warmup: int, rope: bool = False, scaled_q_steps: int = 0):
     import torch
     from paper_2609_32278_amd import kvx
 
@@ -167,13 +167,45 @@ def run_gpu(config: str, steps: int, warmup: int, rope: bool = False):
     attn_t = np.array([e[1].elapsed_time(e[2]) for e in evs])
     ms_step = (t1 - t0) * 1e3 / steps
     assert torch.isfinite(out.float()).all(), "non-finite attention output"
+    scaled = None
+    if scaled_q_steps > 0 and w.kv_dtype == 0:
+        # the pool's scaled-Q setting (folded softmax) on the same pool and inputs: the
+        # attention kernel alone, after the exact steps
+        print(f"[bench] scaled-Q mode: {warmup} + {scaled_q_steps} attention launches", file=sys.stderr, flush=True)
+        kvx.kv_pool_set_scaled_q(pool, True)
+        out_sq = torch.empty_like(out)
+        for _ in range(warmup):
+            kvx.extend_attention(pool, batch, q_rot, w.num_q_heads, w.sm_scale, out_sq)
+        ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(scaled_q_steps)]
+        torch.cuda.synchronize()
+        for e in ev2:
+            e[0].record()
+            kvx.extend_attention(pool, batch, q_rot, w.num_q_heads, w.sm_scale, out_sq)
+            e[1].record()
+        torch.cuda.synchronize()
+        kvx.kv_pool_set_scaled_q(pool, False)
+        assert torch.isfinite(out_sq.float()).all(), "non-finite attention output (scaled-Q mode)"
+        scaled = (np.array([e[0].elapsed_time(e[1]) for e in ev2]), out_sq)
     kvx.kv_pool_destroy(pool)
-    return w, ms_step, store_t, attn_t, out
+    return w, ms_step, store_t, attn_t, out, scaled
 
 
-def run_cpu_baseline(config: str, rows_per_req: int, max_reqs: int, gpu_out=None):
+def _parity(gpu_out, qo, rows, ref):
+    """Errors of the GPU output's sampled rows against the oracle's."""
+    import torch
+    gidx = torch.from_numpy(np.array([qo[r] + i for r, i in rows], dtype=np.int64))
+    got = gpu_out[gidx.to(gpu_out.device)].float().cpu().numpy().astype(np.float64)
+    err = np.abs(got - ref)
+    return {"rows": int(len(rows)), "max_abs_err": float(err.max()), "mean_abs_err": float(err.mean()),
+            "rel_rms_err": float(np.sqrt((err ** 2).mean()) / max(np.sqrt((ref ** 2).mean()), 1e-300)),
+            "gate": "max <= 2e-2, mean <= 2e-3 (fp64 oracle)",
+            "pass": bool(err.max() <= 2e-2 and err.mean() <= 2e-3)}
+
+
+def run_cpu_baseline(config: str, rows_per_req: int, max_reqs: int, gpu_out=None, gpu_out_scaled=None):
     """The oracle as it stands, on a bounded sample of the same workload.  With the
-    GPU's output of the timed steps, also the parity of the sampled rows."""
+    GPU's output of the timed steps, also the parity of the sampled rows (and of the
+    scaled-Q mode's output against the oracle's definition of that mode)."""
     import torch
     import oracle
     from paper_2609_32278_amd import workloads as wl
@@ -218,17 +250,16 @@ def run_cpu_baseline(config: str, rows_per_req: int, max_reqs: int, gpu_out=None
     used = oracle.max_threads()
     visible = int(sum(int(sub.prefix_lens[r]) + int(i) + 1 for r, i in rows))
     flops = 4.0 * w.head_dim * w.num_q_heads * visible
-    parity = None
+    parity = parity_sq = None
+    # the sampled requests are the batch's first ones, so their rows sit at the same offsets
     if gpu_out is not None:
-        # the sampled requests are the batch's first ones, so their rows sit at the same offsets
-        gidx = torch.from_numpy(np.array([qo[r] + i for r, i in rows], dtype=np.int64))
-        got = gpu_out[gidx.to(gpu_out.device)].float().cpu().numpy().astype(np.float64)
-        err = np.abs(got - ref)
-        parity = {"rows": int(len(rows)), "max_abs_err": float(err.max()), "mean_abs_err": float(err.mean()),
-                  "rel_rms_err": float(np.sqrt((err ** 2).mean()) / max(np.sqrt((ref ** 2).mean()), 1e-300)),
-                  "gate": "max <= 2e-2, mean <= 2e-3 (fp64 oracle)",
-                  "pass": bool(err.max() <= 2e-2 and err.mean() <= 2e-3)}
-    return parity, {
+        parity = _parity(gpu_out, qo, rows, ref)
+    if gpu_out_scaled is not None:
+        ref_sq = oracle.extend_attention(pool, sub.prefix_lens, sub.extend_lens, sub.page_indptr, sub.page_ids,
+                                         q_rows, rows[:, 0], rows[:, 1], w.num_q_heads, w.sm_scale,
+                                         num_threads=cores, scaled_q=True)
+        parity_sq = _parity(gpu_out_scaled, qo, rows, ref_sq)
+    return parity, parity_sq, {
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
         "cores": used,
@@ -253,6 +284,9 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="oracle sample rows per request (0: sized to about 15 s of oracle work, at most 32)")
     ap.add_argument("--cpu-reqs", type=int, default=16)
+    ap.add_argument("--scaled-q-steps", type=int, default=-1,
+                    help="attention launches timed in the pool's scaled-Q mode after the exact steps "
+                         "(bf16 pools; -1: as many as --steps, 0: skip)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run only a plain 1 GiB device copy kernel (HBM counter calibration)")
     args = ap.parse_args()
@@ -280,7 +314,11 @@ def main():
         print(json.dumps({"calib_copy_bytes_read": 4 * n, "calib_copy_bytes_written": 4 * n, "launches": 3}))
         return
 
-    w, ms_step, store_t, attn_t, gpu_out = run_gpu(args.config, args.steps, args.warmup, args.rope)
+    sq_steps = args.steps if args.scaled_q_steps < 0 else args.scaled_q_steps
+    if is_decode(args.config):
+        sq_steps = 0  # decode steps are always exact
+    w, ms_step, store_t, attn_t, gpu_out, scaled = run_gpu(args.config, args.steps, args.warmup, args.rope,
+                                                           sq_steps)
     # the roofline entry takes the kernel's average launch time; medians are reported beside it
     store_ms, attn_ms = float(store_t.mean()), float(attn_t.mean())
     store_med, attn_med = float(np.median(store_t)), float(np.median(attn_t))
@@ -352,10 +390,24 @@ def main():
     if traffic is not None:
         result["roofline"]["traffic_GBps"] = round(traffic / (attn_ms * 1e-3) / 1e9, 1)
         result["roofline"]["traffic_over_algorithmic"] = round(traffic / attn_alg_bytes, 2)
+    if scaled is not None:
+        sq_t, _ = scaled
+        sq_med = float(np.median(sq_t))
+        result["scaled_q_mode"] = {
+            "what": "kv_pool_set_scaled_q: Q times the softmax scale rounded to bf16, no FMA per score "
+                    "(a precision option, not the headline)",
+            "attn_ms_median": round(sq_med, 4),
+            "attn_ms_min_max": [round(float(sq_t.min()), 4), round(float(sq_t.max()), 4)],
+            "attn_tflops_median": round(flops / (sq_med * 1e-3) / 1e12, 2),
+            "pct_bf16_peak_attn_median": round(100.0 * flops / (sq_med * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+        }
     if not args.no_cpu_baseline:
-        parity, cb = run_cpu_baseline(args.config, args.cpu_rows, args.cpu_reqs, gpu_out)
+        parity, parity_sq, cb = run_cpu_baseline(args.config, args.cpu_rows, args.cpu_reqs, gpu_out,
+                                                 scaled[1] if scaled is not None else None)
         result["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v) for k, v in cb.items()}
         result["parity"] = parity
+        if parity_sq is not None:
+            result["scaled_q_mode"]["parity"] = parity_sq
     print(json.dumps(result), flush=True)
 
 

@@ -316,6 +316,23 @@ int extend_attention_plan(const kvx_batch *batch, int32_t num_q_heads, int32_t n
  */
 int kv_pool_set_split_keys(kvx_pool *pool, int32_t keys);
 
+/*
+ * Scaled-Q softmax of extend_attention's prefill launches on a bf16 pool (0 =
+ * off, the default; 1 = on).  When on, each query is multiplied by
+ * c = float32(sm_scale * float32(log2 e)) in float32 and rounded to bf16 (round to
+ * nearest even) when it is loaded, and the scores of those queries are taken in
+ * base 2: o = softmax_j(ln 2 * bf16(q * c) . k_j) v_j.  This removes one VALU
+ * instruction per (query, key) pair, about 4% of the kernel time on long key
+ * ranges, and adds one more bf16 rounding of q (2^-9 relative per element): the
+ * error against the exact attention grows where scores are large (about twice
+ * the default's at query scale 4).  The prefill kernel of an fp8 pool always takes
+ * this form (its e4m3 keys dominate the error), and decode steps are always
+ * exact.  The softmax itself (Section 2's prefill over the uncached suffix) is
+ * unchanged.  A setting of the pool: takes effect for calls queued after it, from
+ * the pool's one host thread.  Errors: EINVAL (pool NULL, enable not 0 or 1).
+ */
+int kv_pool_set_scaled_q(kvx_pool *pool, int32_t enable);
+
 /* Message describing the last non-OK status on this thread ("" if none). */
 const char *kvx_last_error(void);
 

@@ -201,14 +201,34 @@ def store_kv_values(pool: OraclePool, prefix_lens, extend_lens, page_indptr, pag
         raise ValueError(f"oracle_store_kv_f64 failed ({rc}): page id outside the pool")
 
 
+LOG2E_F32 = np.float32(1.4426950408889634)
+
+
+def scaled_queries(q_rows, sm_scale) -> np.ndarray:
+    """bf16 bits of the queries of the scaled-Q mode: each query times
+    c = float32(float32(sm_scale) * float32(log2 e)) as a float32 product, rounded
+    to bf16 (nearest, ties to even).  Attention of these queries with softmax scale
+    ln 2 is the mode's result: exp2(bf16(q c) . k) = exp(ln 2 * bf16(q c) . k)."""
+    c = np.float32(np.float32(sm_scale) * LOG2E_F32)
+    q = bf16_value(q_rows).astype(np.float32)
+    y = (q * c).astype(np.float32)  # one float32 product per element
+    return bf16_round(y.astype(np.float64))
+
+
 def extend_attention(pool: OraclePool, prefix_lens, extend_lens, page_indptr, page_ids, q_rows,
                      row_req, row_pos, num_q_heads, sm_scale, mutant="none", num_threads=0,
-                     want_lse=False):
+                     want_lse=False, scaled_q=False):
     """Attention outputs (float64 [n, Hq, d]) of the listed suffix rows.
 
     q_rows: bf16 [n, Hq, d] (torch bf16 or uint16 bits) -- the queries of those rows.
     row_req / row_pos: request index and suffix position of each row.
+    scaled_q: the scaled-Q mode's definition instead (the queries of
+    ``scaled_queries`` with softmax scale ln 2); the LSE is then in natural units of
+    those scores.
     """
+    if scaled_q:
+        q_rows = scaled_queries(q_rows, sm_scale)
+        sm_scale = float(np.log(2.0))
     p = _c(prefix_lens, np.int32)
     e = _c(extend_lens, np.int32)
     pi = _indptr64(page_indptr)

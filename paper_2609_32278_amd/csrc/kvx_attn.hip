@@ -26,11 +26,13 @@
 //   * online softmax in base 2: p = exp2(s * scale - m) (one FMA + one exp per
 //     score).  The running maximum m moves only when a row's maximum grows by
 //     more than 2^8, so O is rarely rescaled (the final division cancels the
-//     reference point).  On an fp8 pool the FMA goes away: Q is multiplied by
-//     scale * k_scale when it is loaded (one more bf16 rounding, 2^-9 relative,
-//     far below the pool's own e4m3 rounding of K), and the first MFMA of every
-//     score tile takes -m (a 16-register block) as its accumulator input, so the
-//     tile comes out as s * scale - m and p is exp2 of it directly;
+//     reference point).  Folded form (always on an fp8 pool; on a bf16 pool when
+//     the pool's scaled-Q setting asks for it): the FMA goes away.  Q is
+//     multiplied by scale (times k_scale on an fp8 pool) when it is loaded and
+//     rounded once more to bf16 (2^-9 relative; on an fp8 pool far below the
+//     e4m3 rounding of K), and the first MFMA of every score tile takes -m (a
+//     16-register block) as its accumulator input, so the tile comes out as
+//     s * scale - m and p is exp2 of it directly;
 //   * O^T += V^T(t) P^T(t): V^T from LDS is the A operand, P stays in registers
 //     as bf16 pairs, and the row sums are taken over those bf16 values (v_dot2).
 // Software pipeline: the MFMAs of S(t+1) are issued among the exp / pack of tile
@@ -328,6 +330,40 @@ __device__ __forceinline__ void pv_tile(f32x16 (&o)[Geom<D>::DB], const uint8_t*
 
 // ---------------------------------------------------------------- shared by both kernels
 
+// Folded online softmax state of a lane's row, in log2 units of the scaled scores:
+// the reference point m, the row sum l relative to it, -m as a 16-register
+// accumulator input of every score tile's first k-step, and mx, the maximum of the
+// newest tile relative to m.
+
+// After the first tile: m = its row maximum (finite, because the unit's first key is
+// visible to every row of the unit), and that tile is moved to it.
+__device__ __forceinline__ void set_reference(f32x16 (&s)[kKB], float& mx, float& m_run, f32x16& cneg) {
+  m_run = mx;
+#pragma unroll
+  for (int kb = 0; kb < kKB; kb++) s[kb] -= mx;
+  cneg = -mx;
+  mx = 0.0f;
+}
+
+// Lazy rescale before the tile st (maximum mx) is exponentiated: m moves only when a
+// row outgrows it by 2^8 (kRescaleThreshold), and O, l and st move with it.
+template <int D>
+__device__ __forceinline__ void folded_rescale(f32x16 (&st)[kKB], f32x16 (&o)[Geom<D>::DB], float& mx, float& m_run,
+                                               float& l_run, f32x16& cneg) {
+  if (__any(mx > kRescaleThreshold)) {
+    const float d = fmaxf(mx, 0.0f);
+    const float alpha = __builtin_amdgcn_exp2f(-d);
+    l_run *= alpha;
+#pragma unroll
+    for (int b = 0; b < Geom<D>::DB; b++) o[b] *= alpha;
+#pragma unroll
+    for (int kb = 0; kb < kKB; kb++) st[kb] -= d;
+    m_run += d;
+    mx -= d;
+    cneg = -m_run;
+  }
+}
+
 // The work item of this workgroup (scalar loads: every index derived from it stays
 // uniform) and the lane's query row within it.
 struct Rows {
@@ -445,7 +481,8 @@ __device__ __forceinline__ void write_result(const AttnParams& p, const Rows& r,
 
 // ---------------------------------------------------------------- bf16 pool
 
-template <int D>
+// SQ: folded softmax (Q scaled and rounded once more to bf16, see the file header).
+template <int D, bool SQ>
 __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams p) {
   using G = Geom<D>;
   __shared__ __attribute__((aligned(1024))) uint8_t k_lds[G::NSTAGE][G::TILE_BYTES];
@@ -460,7 +497,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   const float scale = p.scale_log2;  // softmax scale of the scores in log2 units
 
   bf16x8 qf[G::KSTEPS];
-  load_q<D, false>(qf, p, r, scale);
+  load_q<D, SQ>(qf, p, r, scale);
   int koff[G::KSTEPS];
   k_offsets<D>(koff, r.n, h);
   const int vbase = v_offset(r.n, h);
@@ -471,8 +508,10 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   f32x16 o[G::DB];
 #pragma unroll
   for (int b = 0; b < G::DB; b++) o[b] = f32x16{};
-  float m_run = -1e30f, l_run = 0.0f, mx;  // running maximum (log2 units) and sum of the lane's row
-  const f32x16 zero = f32x16{};
+  // running maximum (log2 units) and sum of the lane's row; folded: m relative to the
+  // first tile's row maximum, and -m as the score tiles' accumulator input
+  float m_run = SQ ? 0.0f : -1e30f, l_run = 0.0f, mx;
+  f32x16 c0 = f32x16{};
 
   const int kb0 = u.key_begin;
   const int n_tiles = (u.key_end - kb0 + kBN - 1) / kBN;
@@ -537,14 +576,17 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
 
   f32x16 sa[kKB], sb[kKB];
   bf16x8 pb[2 * kKB];
-  qk_tile<D>(sa, k_lds[0], koff, qf, zero);
+  qk_tile<D>(sa, k_lds[0], koff, qf, c0);
   mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
+  if constexpr (SQ) set_reference(sa, mx, m_run, c0);
   __syncthreads();  // every wave has read K(0) before iteration 0 refills its slot with K(4)
 
   // lazy rescale before the scores of the tile whose maximum is mx are exponentiated:
   // the reference maximum moves only when a row outgrows it by 2^8
-  auto rescale = [&]() {
-    if (__any(mx * scale > m_run + kRescaleThreshold)) {
+  auto rescale = [&](f32x16 (&st)[kKB]) {
+    if constexpr (SQ) {
+      folded_rescale<D>(st, o, mx, m_run, l_run, c0);
+    } else if (__any(mx * scale > m_run + kRescaleThreshold)) {
       const float m_new = fmaxf(m_run, mx * scale);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
@@ -584,25 +626,25 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       issued = issue(tk, tv);
     }
 
-    rescale();
+    rescale(s_cur);
 
     if constexpr (MASKED) {
-      if (has_next) qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, zero);
-      l_run = exp_pack<false>(s_cur, pb, l_run, m_run, scale);
+      if (has_next) qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0);
+      l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
       pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
       if (has_next) mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
     } else if constexpr (SPREAD) {
-      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, zero, [&](int i) {
+      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0, [&](int i) {
         const int it = G::PER_WAVE - 1 - i;
         const bool is_v = it >= G::K_SLOTS;
         issue_direct<D>(slot[it], blk[it], is_v ? v_lds[ring(3)] : k_lds[ring(4)]);  // V(t+3), K(t+4)
       });
-      l_run = exp_pack<false>(s_cur, pb, l_run, m_run, scale);
+      l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
       pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
       mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     } else {
-      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, zero);
-      l_run = exp_pack<false>(s_cur, pb, l_run, m_run, scale);
+      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0);
+      l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
       pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
       mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
     }
@@ -869,31 +911,9 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_fp8_kernel(AttnPa
   bf16x8 pb[2 * kKB];
   qk_tile<D>(sa, k_lds[0], koff, qf, cneg);
   mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
-  // the reference point: the first tile's row maximum (finite: the tile's first key
-  // is visible to every row of the unit)
-  m_run = mx;
-#pragma unroll
-  for (int kb = 0; kb < kKB; kb++) sa[kb] -= mx;
-  cneg = -mx;
-  mx = 0.0f;
+  set_reference(sa, mx, m_run, cneg);
   __syncthreads();  // every wave has read K(0) before iteration 0 converts K(2) into its buffer
 
-  // lazy rescale before the tile st (its row maximum mx, both relative to m) is
-  // exponentiated: m moves only when a row outgrows it by 2^8, and st moves with it
-  auto rescale = [&](f32x16 (&st)[kKB]) {
-    if (__any(mx > kRescaleThreshold)) {
-      const float d = fmaxf(mx, 0.0f);
-      const float alpha = __builtin_amdgcn_exp2f(-d);
-      l_run *= alpha;
-#pragma unroll
-      for (int b = 0; b < G::DB; b++) o[b] *= alpha;
-#pragma unroll
-      for (int kb = 0; kb < kKB; kb++) st[kb] -= d;
-      m_run += d;
-      mx -= d;
-      cneg = -m_run;
-    }
-  };
 
   // One pipelined iteration: consumes S(t), produces S(t+1) from bf16 K(t+1) with its
   // maximum, accumulates P(t) V(t), loads pair t+3 and converts pair t+1.  Before the
@@ -921,7 +941,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_fp8_kernel(AttnPa
     } else {
       issued = issue(t + 3);
     }
-    rescale(s_cur);
+    folded_rescale<D>(s_cur, o, mx, m_run, l_run, cneg);
     if constexpr (SPREAD) {
       qk_tile<D>(s_nxt, k_lds[buf(1)], koff, qf, cneg, [&](int i) {
         if (i < G8::NDMA) dma(i, stg[slot_of(3)], blk[i]);
@@ -1018,16 +1038,18 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams p) {
 
 }  // namespace
 
-hipError_t launch_extend_attention(const AttnParams& p, int64_t n_units, int head_dim, bool fp8,
+hipError_t launch_extend_attention(const AttnParams& p, int64_t n_units, int head_dim, bool fp8, bool scaled_q,
                                    hipStream_t stream) {
   if (n_units <= 0) return hipSuccess;
   dim3 grid((unsigned)n_units), block(kAttnThreads);
   if (head_dim == 128) {
     if (fp8) hipLaunchKernelGGL((extend_attn_fp8_kernel<128>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((extend_attn_kernel<128>), grid, block, 0, stream, p);
+    else if (scaled_q) hipLaunchKernelGGL((extend_attn_kernel<128, true>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((extend_attn_kernel<128, false>), grid, block, 0, stream, p);
   } else {
     if (fp8) hipLaunchKernelGGL((extend_attn_fp8_kernel<64>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((extend_attn_kernel<64>), grid, block, 0, stream, p);
+    else if (scaled_q) hipLaunchKernelGGL((extend_attn_kernel<64, true>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((extend_attn_kernel<64, false>), grid, block, 0, stream, p);
   }
   return hipGetLastError();
 }

@@ -187,6 +187,7 @@ struct kvx_pool {
   Staging st_store, st_attn, st_io, st_move;
   Workspace parts;
   int32_t split_keys = 0;  // key-range split length of extend_attention; 0 = automatic
+  int32_t scaled_q = 0;    // 1: prefill attention on a bf16 pool takes the folded softmax
 };
 
 namespace {
@@ -663,6 +664,14 @@ int kv_pool_set_split_keys(kvx_pool* pool, int32_t keys) {
   return KVX_OK;
 }
 
+int kv_pool_set_scaled_q(kvx_pool* pool, int32_t enable) {
+  g_last_error.clear();
+  if (int rc = check_pool(pool)) return rc;
+  if (enable != 0 && enable != 1) return fail(KVX_EINVAL, "scaled_q %d: must be 0 or 1", enable);
+  pool->scaled_q = enable;
+  return KVX_OK;
+}
+
 int kv_pool_create(int64_t num_pages, int32_t page_size, int32_t num_kv_heads, int32_t head_dim,
                    int32_t kv_dtype, const float* k_scale, const float* v_scale, kvx_pool** out) {
   g_last_error.clear();
@@ -1110,7 +1119,8 @@ int kvx::attention_call(kvx_pool* pool, const kvx_batch* batch, const void* q, i
   p.group = num_q_heads / pool->num_kv_heads;
   p.tile_tok = kvx::kTileRows / p.group;
   p.scale_log2 = sm_scale * 1.4426950408889634f;
-  hipError_t e = kvx::launch_extend_attention(p, (int64_t)plan.units.size(), D, pool->kv_dtype == KVX_KV_FP8_E4M3, s);
+  hipError_t e = kvx::launch_extend_attention(p, (int64_t)plan.units.size(), D, pool->kv_dtype == KVX_KV_FP8_E4M3,
+                                              pool->scaled_q != 0, s);
   if (e != hipSuccess) return hip_fail(e, "extend_attention kernel launch");
   if (!plan.merges.empty()) {
     kvx::MergeParams m;

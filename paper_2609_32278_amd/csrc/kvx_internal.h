@@ -229,7 +229,7 @@ struct FixedScratch {
 int attention_call(kvx_pool* pool, const kvx_batch* batch, const void* q, int32_t num_q_heads, float sm_scale,
                    void* out, float* lse, kvx_stream_t stream, const FixedScratch* fixed);
 
-hipError_t launch_extend_attention(const AttnParams& p, int64_t n_units, int head_dim, bool fp8,
+hipError_t launch_extend_attention(const AttnParams& p, int64_t n_units, int head_dim, bool fp8, bool scaled_q,
                                    hipStream_t stream);
 hipError_t launch_merge(const MergeParams& p, int64_t n_merges, int head_dim, hipStream_t stream);
 hipError_t launch_store_kv(const StoreParams& p, int64_t n_units, int head_dim, bool fp8,

@@ -30,7 +30,7 @@ NOALLOC_PLAN_BYTES, NOALLOC_PARTS_BYTES = 8 << 20, 56 << 20  # KVX_NOALLOC_* in 
 # Every symbol include/kvx.h and include/kvx_cache.h declare.
 EXPORTS = ["kv_pool_create", "kv_pool_destroy", "kv_pool_layout", "kv_pool_write_pages",
            "kv_pool_read_pages", "kv_pool_record_bytes", "kv_pool_spill", "kv_pool_reload", "store_kv", "store_kv_rope", "extend_attention", "extend_attention_noalloc", "extend_attention_plan",
-           "kv_pool_set_split_keys", "kvx_last_error",
+           "kv_pool_set_split_keys", "kv_pool_set_scaled_q", "kvx_last_error",
            "kvx_cache_create", "kvx_cache_create_tiered", "kvx_cache_set_recency_tiers", "kvx_cache_destroy", "kvx_cache_begin_turn",
            "kvx_cache_begin_turn_tiered", "kvx_cache_end_turn", "kvx_cache_complete", "kvx_cache_agent",
            "kvx_cache_agent_host", "kvx_cache_join", "kvx_cache_group", "kvx_cache_stats",
@@ -125,6 +125,7 @@ def lib():
             "extend_attention_noalloc": [P, ctypes.POINTER(kvx_batch), P, i32, f32, P, P, P],
             "extend_attention_plan": [ctypes.POINTER(kvx_batch), i32, i32, i32, i32, P, i64, ctypes.POINTER(i64)],
             "kv_pool_set_split_keys": [P, i32],
+            "kv_pool_set_scaled_q": [P, i32],
             "kvx_cache_create": [i64, i32, i32, i32, ctypes.POINTER(P)],
             "kvx_cache_create_tiered": [i64, i64, i32, i32, i32, ctypes.POINTER(P)],
             "kvx_cache_set_recency_tiers": [P, i64],
@@ -375,6 +376,10 @@ def extend_attention_plan(batch: Batch, num_q_heads: int, num_kv_heads: int, hea
 
 def kv_pool_set_split_keys(pool, keys: int) -> None:
     _check(lib().kv_pool_set_split_keys(pool, int(keys)), "kv_pool_set_split_keys")
+
+
+def kv_pool_set_scaled_q(pool, enable: bool) -> None:
+    _check(lib().kv_pool_set_scaled_q(pool, 1 if enable else 0), "kv_pool_set_scaled_q")
 
 
 # ------------------------------------------------------------------ prefix cache (include/kvx_cache.h)

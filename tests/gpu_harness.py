@@ -31,12 +31,15 @@ class GpuRun:
     """Pool + batch of one workload on the GPU; the cached prefixes are written by
     store_kv of the history turn, request by request."""
 
-    def __init__(self, w: wl.Workload, fill_bits: int | None = None, overrides=None, split_keys: int = 0):
+    def __init__(self, w: wl.Workload, fill_bits: int | None = None, overrides=None, split_keys: int = 0,
+                 scaled_q: bool = False):
         self.w = w
         self.pool = kvx.kv_pool_create(w.num_pages, w.page_size, w.num_kv_heads, w.head_dim, w.kv_dtype,
                                        w.k_scale, w.v_scale)
         if split_keys:
             kvx.kv_pool_set_split_keys(self.pool, split_keys)
+        if scaled_q:
+            kvx.kv_pool_set_scaled_q(self.pool, True)
         if fill_bits is not None:
             self.fill_pool(fill_bits)
         self.batch, self._ids = fresh_batch(w, w.page_ids, w.prefix_lens, w.extend_lens, w.page_indptr)
@@ -105,9 +108,10 @@ class GpuRun:
 
 
 def oracle_rows(w: wl.Workload, q_dev: torch.Tensor, rows: np.ndarray | None, fill=None, want_lse=False,
-                kv_override=None):
+                kv_override=None, scaled_q=False):
     """Oracle outputs of the listed rows ((r, i) pairs; None = every row), built from
-    the generator's values for just the requests involved (compact pool)."""
+    the generator's values for just the requests involved (compact pool); scaled_q:
+    the scaled-Q mode's definition."""
     if rows is None:
         rr, rp = oracle.all_rows(w.extend_lens)
         rows = np.stack([rr, rp], 1)
@@ -132,7 +136,8 @@ def oracle_rows(w: wl.Workload, q_dev: torch.Tensor, rows: np.ndarray | None, fi
     q_rows = q_dev[torch.from_numpy(gidx).to(q_dev.device)].cpu()
     rr = np.array([remap[int(r)] for r in rows[:, 0]], np.int32)
     res = oracle.extend_attention(pool, sub.prefix_lens, sub.extend_lens, sub.page_indptr, sub.page_ids, q_rows,
-                                  rr, rows[:, 1].astype(np.int32), w.num_q_heads, w.sm_scale, want_lse=want_lse)
+                                  rr, rows[:, 1].astype(np.int32), w.num_q_heads, w.sm_scale, want_lse=want_lse,
+                                  scaled_q=scaled_q)
     return res, gidx
 
 

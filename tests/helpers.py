@@ -56,11 +56,11 @@ def oracle_pool_for(w: wl.Workload, t: dict, fill=None) -> oracle.OraclePool:
 
 
 def oracle_all_rows(w: wl.Workload, pool: oracle.OraclePool, q: torch.Tensor, mutant="none",
-                    want_lse=False, num_threads=0):
+                    want_lse=False, num_threads=0, scaled_q=False):
     rr, rp = oracle.all_rows(w.extend_lens)
     return oracle.extend_attention(pool, w.prefix_lens, w.extend_lens, w.page_indptr, w.page_ids,
                                    q, rr, rp, w.num_q_heads, w.sm_scale, mutant=mutant,
-                                   want_lse=want_lse, num_threads=num_threads)
+                                   want_lse=want_lse, num_threads=num_threads, scaled_q=scaled_q)
 
 
 def brute_force_all(w: wl.Workload, dequant=None):

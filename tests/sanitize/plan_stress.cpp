@@ -28,7 +28,7 @@ namespace kvx {
   }
 KVX_STUB(launch_decode, const DecodeParams&, int64_t, int, bool, hipStream_t)
 KVX_STUB(launch_decode_merge, const DecodeMergeParams&, int64_t, int, hipStream_t)
-KVX_STUB(launch_extend_attention, const AttnParams&, int64_t, int, bool, hipStream_t)
+KVX_STUB(launch_extend_attention, const AttnParams&, int64_t, int, bool, bool, hipStream_t)
 KVX_STUB(launch_merge, const MergeParams&, int64_t, int, hipStream_t)
 KVX_STUB(launch_store_kv, const StoreParams&, int64_t, int, bool, hipStream_t)
 KVX_STUB(launch_store_kv_rope, const RopeParams&, int64_t, int, bool, bool, hipStream_t)

@@ -58,6 +58,7 @@ def test_pool_argument_errors():
     assert _err(kvx.kv_pool_create, 10, 16, 2, 64, kvx.KVX_KV_FP8_E4M3, [1.0, 0.0], [1.0, 1.0]) == kvx.KVX_EINVAL
     assert _err(kvx.kv_pool_create, 10, 16, 2, 64, 7) == kvx.KVX_EINVAL
     assert _err(kvx.kv_pool_set_split_keys, None, 64) == kvx.KVX_EINVAL
+    assert _err(kvx.kv_pool_set_scaled_q, None, True) == kvx.KVX_EINVAL
     assert _err(kvx.kv_pool_layout, None) == kvx.KVX_EINVAL
 
 

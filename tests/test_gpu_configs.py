@@ -39,8 +39,8 @@ def _sample_requests(w, k, seed=0):
     return sorted(must | set(int(x) for x in extra))
 
 
-@pytest.mark.parametrize("name", list(SAMPLING))
-def test_full_config_parity(name):
+@pytest.mark.parametrize("name,scaled_q", [(n, False) for n in SAMPLING] + [("wide70b", True)])
+def test_full_config_parity(name, scaled_q):
     w = wl.make_workload(name)
     k, per = SAMPLING[name]
     reqs = _sample_requests(w, k)
@@ -51,15 +51,15 @@ def test_full_config_parity(name):
         extra = np.stack([np.zeros(32, np.int32), np.linspace(0, e0 - 1, 32).astype(np.int32)], 1)
         rows = np.unique(np.concatenate([rows, extra]), axis=0)
     print(f"[config] {name}: R={w.num_reqs} T={w.total_extend} pages={w.num_pages} sampled reqs={reqs} "
-          f"rows={len(rows)}", flush=True)
-    run = GpuRun(w)
+          f"rows={len(rows)} scaled_q={int(scaled_q)}", flush=True)
+    run = GpuRun(w, scaled_q=scaled_q)
     try:
         run.store()
         out = run.attend()
         assert not torch.isnan(out).any(), "some output rows were not written"
         assert torch.isfinite(out.float()).all()
         print(f"[config] {name}: GPU done, running the oracle", flush=True)
-        ref, gidx = oracle_rows(w, run.q, rows)
+        ref, gidx = oracle_rows(w, run.q, rows, scaled_q=scaled_q)
         got = out[torch.from_numpy(gidx).to(out.device)].float().cpu().numpy().astype(np.float64)
         compare(got, ref, name)
         # KV store: the sampled requests' pages, bit for bit

@@ -18,15 +18,17 @@ def _f64(t):
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
-def _run_and_compare(w, tag, want_lse=False, fill=None, split_keys=0):
+def _run_and_compare(w, tag, want_lse=False, fill=None, split_keys=0, scaled_q=False):
     print(f"[extend] {tag}: R={w.num_reqs} T={w.total_extend} Hq={w.num_q_heads} Hkv={w.num_kv_heads} "
-          f"d={w.head_dim} fp8={w.kv_dtype} split={split_keys}", flush=True)
-    run = GpuRun(w, fill_bits=fill, split_keys=split_keys)
+          f"d={w.head_dim} fp8={w.kv_dtype} split={split_keys} scaled_q={int(scaled_q)}", flush=True)
+    run = GpuRun(w, fill_bits=fill, split_keys=split_keys, scaled_q=scaled_q)
     try:
         run.store()
         res = run.attend(want_lse=want_lse)
         out, lse = (res if want_lse else (res, None))
-        ref, gidx = oracle_rows(w, run.q, None, want_lse=want_lse)
+        # an fp8 pool's prefill kernel always scales Q; its reference stays the exact
+        # attention over the dequantised pool
+        ref, gidx = oracle_rows(w, run.q, None, want_lse=want_lse, scaled_q=scaled_q and w.kv_dtype == wl.KV_BF16)
         if want_lse:
             ref, ref_lse = ref
         got = _f64(out)[gidx]
@@ -80,6 +82,49 @@ def test_edge_cases_every_row(name):
 def test_sharpened_queries():
     w = wl.make_custom([40, 300, 0], [90, 33, 77], 8, 2, 128, q_sigma=4.0, seed=9)
     _run_and_compare(w, "sharpened")
+
+
+# The scaled-Q mode (kv_pool_set_scaled_q): the folded softmax on bf16 pools,
+# every row against the oracle's definition of the mode (queries rounded to bf16
+# after scaling, scores in base 2) at the same gate.
+SCALED = ["ragged_g4_d128", "g1_d64", "g6_d128", "g16_d64", "long_causal", "g32_d128", "g256_d64", "hkv16_d64"]
+
+
+@pytest.mark.parametrize("name", SCALED)
+def test_scaled_q_mode_every_row(name):
+    p, e, hq, hkv, d, dt = CASES[name]
+    w = wl.make_custom(p, e, hq, hkv, d, kv_dtype=dt, seed=len(name))
+    _run_and_compare(w, f"scaled_{name}", want_lse=True, scaled_q=True)
+
+
+@pytest.mark.parametrize("q_sigma", [1.0, 4.0])
+def test_scaled_q_mode_sharpened_queries(q_sigma):
+    w = wl.make_custom([40, 300, 0], [90, 33, 77], 8, 2, 128, q_sigma=q_sigma, seed=9)
+    _run_and_compare(w, f"scaled_sharp{q_sigma:g}", want_lse=True, scaled_q=True)
+
+
+def test_scaled_q_mode_with_forced_splits():
+    w = wl.make_custom([1000, 77], [130, 64], 8, 2, 128, seed=21)
+    _run_and_compare(w, "scaled_split", want_lse=True, split_keys=128, scaled_q=True)
+
+
+def test_scaled_q_setting_leaves_fp8_prefill_and_decode_steps_unchanged():
+    """An fp8 pool's prefill kernel always takes the folded form, and decode steps
+    are always exact: the setting changes no bit of their outputs.  A value other
+    than 0 or 1 is rejected."""
+    for name in ["g8_fp8_d128", "decode_like"]:
+        p, e, hq, hkv, d, dt = CASES[name]
+        w = wl.make_custom(p, e, hq, hkv, d, kv_dtype=dt, seed=len(name))
+        run = GpuRun(w)
+        try:
+            run.store()
+            a = run.attend()
+            kvx.kv_pool_set_scaled_q(run.pool, True)
+            b = run.attend()
+            assert kvx.lib().kv_pool_set_scaled_q(run.pool, 2) == kvx.KVX_EINVAL
+        finally:
+            run.close()
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16)), name
 
 
 @pytest.mark.parametrize("split", [64, 128, 1024])

@@ -12,7 +12,11 @@ oracle is pinned by mathematics and library routines:
   (e) a single key returns its value exactly; constant V returns the constant;
       Q = 0 averages the visible values; a planted needle key dominates;
   plus the fp8 codec against torch's float8_e4m3fn cast, store round trips, and
-  planted mistakes that must each fail a pin and the parity gate.
+  planted mistakes that must each fail a pin and the parity gate;
+  (f) the scaled-Q mode of the kernels (queries times the softmax scale in log2
+      units, rounded to bf16, scores in base 2): its rounding step against torch's
+      float32 product and bf16 cast, the brute force on the rounded queries, and
+      exact attention wherever that product is exact.
 """
 
 import math
@@ -336,3 +340,63 @@ def test_each_planted_mistake_fails_the_parity_gate_and_a_pin(mutant):
         pin_fails |= not (np.abs(bad - ref).max() <= TOL)
     assert gate_fails, f"mutant {mutant} passes the parity gate"
     assert pin_fails, f"mutant {mutant} passes the brute-force pin"
+
+
+# ------------------------------------------------- (f) the scaled-Q mode (kernel option)
+
+@pytest.mark.parametrize("sm_scale", [1 / math.sqrt(64), 1 / math.sqrt(128), 0.3])
+def test_scaled_queries_match_torch_float32_product_and_bf16_cast(sm_scale):
+    g = torch.Generator().manual_seed(3)
+    q = (torch.randn(7, 5, 64, generator=g) * 3).to(torch.bfloat16)
+    q[0, 0, :4] = torch.tensor([0.0, -0.0, 3.0e38, -1.0e-38]).to(torch.bfloat16)
+    c = torch.tensor(sm_scale, dtype=torch.float32) * torch.tensor(math.log2(math.e), dtype=torch.float32)
+    want = (q.float() * c).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(oracle.scaled_queries(q, sm_scale), want)
+
+
+@pytest.mark.parametrize("q_sigma", [1.0, 4.0])
+def test_scaled_mode_is_base_two_attention_of_the_rounded_queries(q_sigma):
+    """The mode's output is the brute force over the logical sequence with the
+    rounded queries bf16(q c) and scores ln 2 * q'.k (exp2 of the base-2 scores)."""
+    w = wl.make_custom([48, 13, 0], [20, 35, 9], 4, 2, 32, q_sigma=q_sigma, seed=11)
+    t = wl.batch_tensors(w)
+    pool = oracle_pool_for(w, t)
+    out, lse = oracle_all_rows(w, pool, t["q"], want_lse=True, scaled_q=True)
+    outs, lses = [], []
+    for r in range(w.num_reqs):
+        q = oracle.bf16_value(oracle.scaled_queries(wl.request_q(w, r), w.sm_scale))
+        k, v = wl.request_kv(w, r)
+        o, l = brute_force(q, to_f64(k), to_f64(v), int(w.prefix_lens[r]), math.log(2.0))
+        outs.append(o)
+        lses.append(l)
+    assert np.abs(out - np.concatenate(outs)).max() <= TOL
+    assert np.abs(lse - np.concatenate(lses)).max() <= TOL
+    # and it differs from the exact attention by the rounding of q only
+    exact = oracle_all_rows(w, pool, t["q"])
+    assert 0 < np.abs(out - exact).max() < 0.05
+
+
+def test_scaled_mode_reduces_to_exact_attention_when_the_product_is_exact():
+    """With a float32 scale whose product with float32(log2 e) is exactly 1/8, every
+    bf16(q / 8) is q / 8, and the mode is exact attention with softmax scale
+    ln 2 / 8 (a relative 2^-24 from the scale passed)."""
+    l2e = np.float32(math.log2(math.e))
+    sm = np.float32(0.125 / float(l2e))
+    for _ in range(8):
+        prod = np.float32(sm * l2e)
+        if prod == np.float32(0.125):
+            break
+        sm = np.nextafter(sm, np.float32(np.inf) if prod < 0.125 else np.float32(0), dtype=np.float32)
+    assert np.float32(sm * l2e) == np.float32(0.125)
+    w = wl.make_custom([40, 7], [25, 30], 4, 2, 32, seed=12)
+    t = wl.batch_tensors(w)
+    pool = oracle_pool_for(w, t)
+    rr, rp = oracle.all_rows(w.extend_lens)
+
+    def run(scale, scaled_q):
+        return oracle.extend_attention(pool, w.prefix_lens, w.extend_lens, w.page_indptr, w.page_ids, t["q"],
+                                       rr, rp, w.num_q_heads, scale, scaled_q=scaled_q)
+
+    assert np.abs(run(float(sm), True) - run(math.log(2.0) / 8.0, False)).max() <= TOL
+    # a scale whose product is not exact does change the result
+    assert np.abs(run(0.3, True) - run(0.3, False)).max() > 1e-6
