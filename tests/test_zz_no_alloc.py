@@ -4,7 +4,7 @@ Two calls in a row through the C ABI, the second on a smaller batch (so it runs
 on what the first left in the shared per-GPU scratch), each compared with
 extend_attention on the same pool and inputs: bit for bit (both take the same
 plan here, split parts included) and against the fp64 oracle with the parity
-gate.  A batch whose plan does not fit the scratch is refused on the host.
+gate, also with the pool's scaled-Q setting on.  A batch whose plan does not fit the scratch is refused on the host.
 """
 
 import numpy as np
@@ -18,8 +18,8 @@ from paper_2609_32278_amd import workloads as wl
 pytestmark = pytest.mark.gpu
 
 
-def _both(w, split_keys=0):
-    run = GpuRun(w, split_keys=split_keys)
+def _both(w, split_keys=0, scaled_q=False):
+    run = GpuRun(w, split_keys=split_keys, scaled_q=scaled_q)
     try:
         run.store()
         ref, ref_lse = run.attend(want_lse=True)
@@ -33,9 +33,10 @@ def _both(w, split_keys=0):
         run.close()
 
 
-@pytest.mark.parametrize("case", ["prefill", "decode"])
+@pytest.mark.parametrize("case", ["prefill", "prefill_scaled_q", "decode"])
 def test_noalloc_matches_extend_attention_on_two_calls_in_a_row(case):
-    if case == "prefill":
+    scaled_q = case == "prefill_scaled_q"  # the pool's scaled-Q setting holds for both entry points
+    if case.startswith("prefill"):
         # split key ranges (partial results in the scratch), then a smaller batch
         first = wl.make_custom([4000, 129, 0, 2500], [70, 200, 300, 33], 8, 2, 128, seed=41)
         second = wl.make_custom([300, 17], [40, 9], 8, 2, 128, seed=42)
@@ -48,13 +49,13 @@ def test_noalloc_matches_extend_attention_on_two_calls_in_a_row(case):
     for k, (w, split) in enumerate(zip((first, second), splits)):
         print(f"[noalloc] {case} call {k}: P={w.prefix_lens.tolist()} E={w.extend_lens.tolist()} split={split}",
               flush=True)
-        q, ref, ref_lse, out, lse, items = _both(w, split)
+        q, ref, ref_lse, out, lse, items = _both(w, split, scaled_q)
         parts = int((items["part"] >= 0).sum())
         if k == 0:
             assert parts > 0, "the first call should exercise the partial-result region"
         assert torch.equal(out.view(torch.int16), ref.view(torch.int16)), f"{case} call {k}: outputs differ"
         assert torch.equal(lse, ref_lse), f"{case} call {k}: LSE differs"
-        want, gidx = oracle_rows(w, q, None)
+        want, gidx = oracle_rows(w, q, None, scaled_q=scaled_q)
         got = out.float().cpu().numpy().astype(np.float64)[gidx]
         compare(got, want, f"noalloc {case} call {k}")
 
