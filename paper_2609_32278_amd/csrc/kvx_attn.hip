@@ -722,13 +722,10 @@ struct Geom8 {
   static constexpr int PAIR = 2 * TILE_CODES;             // a staging slot: K codes, then V codes
   static constexpr int KINSTR = TILE_CODES / 1024;        // 1 KiB direct loads per tile
   static constexpr int NDMA = 2 * KINSTR / kWaves;        // direct loads per wave and pair
-  static constexpr int CONV = PAIR / 16 / kAttnThreads;   // 16-code chunks converted per lane and pair
-  static constexpr int KCHUNKS = TILE_CODES / 16;         // 16-code chunks of a K tile
   static constexpr int CPR16 = D / 16;                    // 16-code chunks per K row
   static constexpr int NSTG = 4;                          // staging slots
   static constexpr int NBUF = 2;                          // bf16 buffers of K and of V^T
   static_assert(NDMA >= 1 && (2 * KINSTR) % kWaves == 0, "direct loads must spread evenly over waves");
-  static_assert(CONV >= 1 && PAIR % (16 * kAttnThreads) == 0, "conversion must spread evenly over lanes");
 };
 
 // One wave's direct load of a pair: load g = wave + 8 * it is K load g (g < KINSTR)
@@ -759,23 +756,34 @@ struct CodeLoad {
   }
 };
 
-// One lane's conversion of a pair: chunk q = i * 512 + wave * 64 + lane of the
-// staging slot (K chunks first), at staging byte 16 q, becomes two bf16 chunks at
-// dst and dst ^ 16 of its tile (the two 16-byte halves of a 32-byte-aligned pair
-// of chunks, in the order the swizzle gives).
-//   K chunk (key, c16), 16 dims from 16 c16: bf16 chunks 2 c16, 2 c16 + 1 of row key.
-//   V chunk (page pg, dim d), 16 slots: slots 0..7 and 8..15 of dim row d of page pg.
+// Conversion of a pair by lane L = wave * 64 + lane of the workgroup: for k < NCONV
+// it writes bf16 chunk Q = L + 512 k (16 bytes at 16 Q) of the K tile and of the
+// V^T tile, so that the 8 lanes of each group write one 128-byte half of a row
+// (LDS writes free of bank conflicts), and reads the 8 codes that chunk holds from
+// where the tile's swizzle puts them:
+//   K: chunk p = Q % CPR of row r = Q / CPR holds dims 8 c .. 8 c + 7, c = p ^ (r % CPR):
+//      codes at byte r D + 8 c of the K codes;
+//   V^T: half h = Q & 1 of dim row d = Q / 2 (page d / D) holds slots 8 s .. 8 s + 7,
+//      s = h ^ ((d >> 3) & 1): codes at byte 16 d + 8 s of the V codes.
+// Chunk Q + 512 sits 4096 code bytes further in both (the row swizzle repeats), and
+// its V slots 4096 / D keys later.
 template <int D>
-__device__ __forceinline__ int conv_dst(int q) {
-  using G8 = Geom8<D>;
-  using G = Geom<D>;
-  if (q >= G8::KCHUNKS) {
-    const int qv = q - G8::KCHUNKS, pg = qv / D, d = qv % D;
-    return pg * (D * 32) + d * 32 + ((d >> 3) & 1) * 16;
+struct ConvLane {
+  static constexpr int NCONV = Geom<D>::TILE_BYTES / 16 / kAttnThreads;  // chunks per lane and tile
+  static_assert(NCONV >= 1 && Geom<D>::TILE_BYTES % (16 * kAttnThreads) == 0, "conversion must spread evenly");
+  static_assert(NCONV == 1 || (kAttnThreads / Geom<D>::CPR) % Geom<D>::CPR == 0, "swizzle repeats every 512 chunks");
+  int ksrc;  // byte offset of the lane's K codes in the K codes of a staging slot
+  int vsrc;  // byte offset of the lane's V codes in the V codes
+  int vkey;  // key offset of the lane's first V slot in the tile
+  __device__ __forceinline__ void init(int L) {
+    using G = Geom<D>;
+    const int r = L / G::CPR, pch = L % G::CPR;
+    ksrc = r * D + ((pch ^ (r % G::CPR)) * 8);
+    const int d = L / 2, hs = (L & 1) ^ ((d >> 3) & 1);
+    vsrc = d * 16 + 8 * hs;
+    vkey = (d / D) * kPageSize + 8 * hs;
   }
-  const int key = q / G8::CPR16, c16 = q % G8::CPR16;
-  return key * (D * 2) + ((2 * c16) ^ (key % G::CPR)) * 16;
-}
+};
 
 // Zero the bf16 values of V^T slots at or past key_end (8 slots starting at key).
 __device__ __forceinline__ uint4 zero_past(uint4 x, int key, int key_end) {
@@ -840,10 +848,10 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_fp8_kernel(AttnPa
     ld[it].init(wave + kWaves * it, lane);
     head_base[it] = (const char*)(ld[it].is_v ? p.v_pool : p.k_pool) + (size_t)r.kv_head * (kPageSize * D);
   }
-  // conversion chunks of this lane: q = i * 512 + wave * 64 + lane
-  int cdst[G8::CONV];
-#pragma unroll
-  for (int i = 0; i < G8::CONV; i++) cdst[i] = conv_dst<D>(i * kAttnThreads + wave * 64 + lane);
+  // the bf16 chunks this lane converts: 16 L (+ 8192 k) of each tile
+  const int L = wave * 64 + lane;
+  ConvLane<D> cv;
+  cv.init(L);
   const int lp0 = (int)((uint32_t)kb0 / kPageSize);
   // tile of pair s that load `it` fetches: K(s+1) or V(s)
   auto tile_of = [&](int it, int s) { return ld[it].is_v ? s : s + 1; };
@@ -872,24 +880,20 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_fp8_kernel(AttnPa
   // vdst (V(s))
   auto convert = [&](int s, auto whole, const uint8_t* src, uint8_t* kdst, uint8_t* vdst) {
     constexpr bool WHOLE = decltype(whole)::value;
+    const bool k_in = WHOLE || (s + 1 >= 0 && s + 1 < n_tiles);  // K(s+1) exists
+    const bool v_in = WHOLE || (s >= 0 && s < n_tiles);          // V(s) exists
 #pragma unroll
-    for (int i = 0; i < G8::CONV; i++) {
-      const int q0 = i * kAttnThreads + wave * 64;  // uniform
-      const bool is_v = q0 >= G8::KCHUNKS;
-      const int tt = is_v ? s : s + 1;
-      if (!WHOLE && (tt < 0 || tt >= n_tiles)) continue;
-      const uint4 x = *(const uint4*)(src + (q0 + lane) * 16);
-      uint4 lo = fp8x8_to_bf16x8(make_uint2(x.x, x.y));
-      uint4 hi = fp8x8_to_bf16x8(make_uint2(x.z, x.w));
-      if (!WHOLE && is_v && tt >= last_whole) {
-        // first key of the chunk's 16 slots: page (q - KCHUNKS) / D of tile tt
-        const int key = kb0 + tt * kBN + ((q0 + lane - G8::KCHUNKS) / D) * kPageSize;
-        lo = zero_past(lo, key, u.key_end);
-        hi = zero_past(hi, key + 8, u.key_end);
+    for (int k = 0; k < ConvLane<D>::NCONV; k++) {
+      if (k_in) {
+        const uint2 c = *(const uint2*)(src + cv.ksrc + 4096 * k);
+        *(uint4*)(kdst + 16 * L + 8192 * k) = fp8x8_to_bf16x8(c);
       }
-      uint8_t* dst = is_v ? vdst : kdst;
-      *(uint4*)(dst + cdst[i]) = lo;
-      *(uint4*)(dst + (cdst[i] ^ 16)) = hi;
+      if (v_in) {
+        const uint2 c = *(const uint2*)(src + G8::TILE_CODES + cv.vsrc + 4096 * k);
+        uint4 x = fp8x8_to_bf16x8(c);
+        if (!WHOLE && s >= last_whole) x = zero_past(x, kb0 + s * kBN + cv.vkey + (4096 / D) * k, u.key_end);
+        *(uint4*)(vdst + 16 * L + 8192 * k) = x;
+      }
     }
   };
 
