@@ -24,9 +24,14 @@
 //     In the result each lane owns one query row and 16 keys of it, so softmax
 //     statistics are per lane plus one v_permlane32_swap;
 //   * online softmax in base 2: p = exp2(s * scale - m) (one FMA + one exp per
-//     score).  The running maximum m moves only when a row's maximum grows by
-//     more than 2^8, so O is rarely rescaled (the final division cancels the
-//     reference point).  Folded form (always on an fp8 pool; on a bf16 pool when
+//     score) against a reference point m that stays at the row maximum of the
+//     unit's first tile: no per-tile maximum and no rescale in the loop (the
+//     final division cancels m).  bf16 P and fp32 O and l keep their relative
+//     precision for p far above 1, so this is exact unless a later score beats
+//     the first tile's maximum by so much that an exponential or a sum overflows
+//     fp32.  A workgroup whose results are not all finite therefore runs the
+//     unit a second time with a moving reference (a row's maximum moves when it
+//     grows by more than 2^8, with O and l rescaled).  Folded form (always on an fp8 pool; on a bf16 pool when
 //     the pool's scaled-Q setting asks for it): the FMA goes away.  Q is
 //     multiplied by scale (times k_scale on an fp8 pool) when it is loaded and
 //     rounded once more to bf16 (2^-9 relative; on an fp8 pool far below the
@@ -36,7 +41,8 @@
 //   * O^T += V^T(t) P^T(t): V^T from LDS is the A operand, P stays in registers
 //     as bf16 pairs, and the row sums are taken over those bf16 values (v_dot2).
 // Software pipeline: the MFMAs of S(t+1) are issued among the exp / pack of tile
-// t, and the MFMAs of O += P(t) V(t) among the row maximum of tile t+1.
+// t; in the second pass the MFMAs of O += P(t) V(t) overlap the row maximum of
+// tile t+1.
 // MFMA row m of the S^T product is assigned key perm(m) (bits 2 and 3 of m
 // swapped), which makes the keys a lane holds in the S^T accumulators exactly
 // the 8 consecutive keys its B operand slot needs in the V^T P^T product.
@@ -289,6 +295,30 @@ __device__ __forceinline__ float row_max(f32x16 (&s)[kKB], int k0, int qpos, int
   return pair_max(m);
 }
 
+// Causal mask of a tile in place (keys past the row's position become -inf).
+__device__ __forceinline__ void causal_mask(f32x16 (&s)[kKB], int k0, int qpos, int h) {
+#pragma unroll
+  for (int kb = 0; kb < kKB; kb++) {
+#pragma unroll
+    for (int i = 0; i < 16; i++) {
+      const int key = k0 + 32 * kb + 16 * (i / 8) + 8 * h + (i % 8);
+      s[kb][i] = key > qpos ? -INFINITY : s[kb][i];
+    }
+  }
+}
+
+// Whether a lane's results are finite (inf and NaN propagate through the sum; an
+// overflow of the sum itself only reports a false alarm).
+template <int D>
+__device__ __forceinline__ bool all_finite(const f32x16 (&o)[Geom<D>::DB], float l) {
+  float acc = l;
+#pragma unroll
+  for (int b = 0; b < Geom<D>::DB; b++)
+#pragma unroll
+    for (int i = 0; i < 16; i++) acc += o[b][i];
+  return __builtin_isfinite(acc);
+}
+
 // p = exp2(s * scale - m) as bf16 pairs (the P^T B operands, one per page of the
 // tile); returns the row sum over those bf16 values added to l.
 // FOLDED: the tile is already s * scale - m, and p = exp2 of it.
@@ -506,12 +536,10 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
   for (int it = 0; it < G::PER_WAVE; it++) slot[it].init(it * kWaves + wave, lane);
 
   f32x16 o[G::DB];
-#pragma unroll
-  for (int b = 0; b < G::DB; b++) o[b] = f32x16{};
   // running maximum (log2 units) and sum of the lane's row; folded: m relative to the
   // first tile's row maximum, and -m as the score tiles' accumulator input
-  float m_run = SQ ? 0.0f : -1e30f, l_run = 0.0f, mx;
-  f32x16 c0 = f32x16{};
+  float m_run, l_run, mx;
+  f32x16 c0;
 
   const int kb0 = u.key_begin;
   const int n_tiles = (u.key_end - kb0 + kBN - 1) / kBN;
@@ -547,7 +575,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       const char* block = page_block(head_base[it], pid[it], page_bytes);
       uint8_t* tile = is_v ? v_lds[t % G::NSTAGE] : k_lds[t % G::NSTAGE];
       if (is_v && t >= last_whole) {
-        *(uint4*)(tile + s.j * 1024 + lane * 16) = mask_v_tail<D>(*(const uint4*)(block + s.off), s, kb0 + t * kBN, u.key_end);
+        *(uint4*)(tile + s.j * 1024 + lane * 16) =
+            mask_v_tail<D>(*(const uint4*)(block + s.off), s, kb0 + t * kBN, u.key_end);
       } else {
         issue_direct<D>(s, block, tile);
         direct++;
@@ -557,145 +586,176 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
     return direct;
   };
 
-  // ---- prologue: K(0), K(1), V(0) resident; K(2), V(1) and then K(3), V(2) in flight
-  // (they play the loads of iterations -2 and -1)
-  auto tile_or_none = [&](int t) { return t < n_tiles ? t : -1; };
-  int issued_prev = 0;
+  // One pass over the unit.  FIXED: the reference point stays at the first tile's
+  // row maximum (no per-tile maximum, no rescale); otherwise it moves lazily.
+  auto run = [&](auto fixed) {
+    constexpr bool FIXED = decltype(fixed)::value;
 #pragma unroll
-  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 0);
-  issue(0, 0);
+    for (int b = 0; b < G::DB; b++) o[b] = f32x16{};
+    m_run = SQ ? 0.0f : -1e30f;
+    l_run = 0.0f;
+    c0 = f32x16{};
+    // ---- prologue: K(0), K(1), V(0) resident; K(2), V(1) and then K(3), V(2) in flight
+    // (they play the loads of iterations -2 and -1)
+    auto tile_or_none = [&](int t) { return t < n_tiles ? t : -1; };
+    int issued_prev = 0;
 #pragma unroll
-  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 1);
-  issue(tile_or_none(1), -1);
-  wait_vmcnt<0>();
+    for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 0);
+    issue(0, 0);
 #pragma unroll
-  for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, it >= G::K_SLOTS ? 1 : 2);
-  issue(tile_or_none(2), tile_or_none(1));
-  issued_prev = issue(tile_or_none(3), tile_or_none(2));  // pid already advanced to K(3), V(2)
-  __syncthreads();
-
-  f32x16 sa[kKB], sb[kKB];
-  bf16x8 pb[2 * kKB];
-  qk_tile<D>(sa, k_lds[0], koff, qf, c0);
-  mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
-  if constexpr (SQ) set_reference(sa, mx, m_run, c0);
-  __syncthreads();  // every wave has read K(0) before iteration 0 refills its slot with K(4)
-
-  // lazy rescale before the scores of the tile whose maximum is mx are exponentiated:
-  // the reference maximum moves only when a row outgrows it by 2^8
-  auto rescale = [&](f32x16 (&st)[kKB]) {
-    if constexpr (SQ) {
-      folded_rescale<D>(st, o, mx, m_run, l_run, c0);
-    } else if (__any(mx * scale > m_run + kRescaleThreshold)) {
-      const float m_new = fmaxf(m_run, mx * scale);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
+    for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, 1);
+    issue(tile_or_none(1), -1);
+    wait_vmcnt<0>();
 #pragma unroll
-      for (int b = 0; b < G::DB; b++) o[b] *= alpha;
-      m_run = m_new;
-    }
-  };
-
-  // One pipelined iteration: consumes S(t) (scores in s_cur, maximum in mx), produces
-  // S(t+1) into s_nxt with its maximum, accumulates P(t) V(t).  Issues K(t+4) and
-  // V(t+3) into the ring and, before its barrier, waits for K(t+2) and V(t+1),
-  // which were issued two iterations earlier.
-  // In the unmasked variant tile t+1 exists and needs no mask, so the compute part
-  // is one branch-free block in which MFMA and the softmax VALU work interleave.
-  auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole, auto stage) {
-    constexpr bool MASKED = decltype(masked)::value;
-    constexpr bool WHOLE = decltype(whole)::value;
-    constexpr int ST = decltype(stage)::value;
-    // ring slot of tile t + d: a constant when the caller knows t's slot, so every
-    // LDS operand address is a register plus an immediate offset
-    auto ring = [&](int d) -> int {
-      if constexpr (ST >= 0) return (ST + d) % G::NSTAGE;
-      else return (t + d) % G::NSTAGE;
-    };
-    const int k0 = kb0 + t * kBN;
-    const bool has_next = MASKED ? t + 1 < n_tiles : true;
-    const int tk = WHOLE || t + 4 < n_tiles ? t + 4 : -1;
-    const int tv = WHOLE || t + 3 < n_tiles ? t + 3 : -1;
-    int issued = G::PER_WAVE;
-    constexpr bool SPREAD = WHOLE && !MASKED;  // steady state
-    const char* blk[G::PER_WAVE];
-    if constexpr (SPREAD) {
-#pragma unroll
-      for (int it = 0; it < G::PER_WAVE; it++) blk[it] = page_block(head_base[it], pid[it], page_bytes);
-    } else {
-      issued = issue(tk, tv);
-    }
-
-    rescale(s_cur);
-
-    if constexpr (MASKED) {
-      if (has_next) qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0);
-      l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
-      pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
-      if (has_next) mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
-    } else if constexpr (SPREAD) {
-      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0, [&](int i) {
-        const int it = G::PER_WAVE - 1 - i;
-        const bool is_v = it >= G::K_SLOTS;
-        issue_direct<D>(slot[it], blk[it], is_v ? v_lds[ring(3)] : k_lds[ring(4)]);  // V(t+3), K(t+4)
-      });
-      l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
-      pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
-      mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
-    } else {
-      qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0);
-      l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
-      pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
-      mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
-    }
-
-    if constexpr (SPREAD) {
-      // next page ids, read after this iteration's last LDS operand read so that no
-      // operand wait has to cover an outstanding scalar load
-#pragma unroll
-      for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, (it >= G::K_SLOTS ? tv : tk) + 1);
-    }
-    // K(t+2), V(t+1) (issued two iterations ago) must be in LDS before the barrier
-    if constexpr (WHOLE) wait_vmcnt<2 * G::PER_WAVE>();
-    else wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
-    issued_prev = issued;
+    for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, it >= G::K_SLOTS ? 1 : 2);
+    issue(tile_or_none(2), tile_or_none(1));
+    issued_prev = issue(tile_or_none(3), tile_or_none(2));  // pid already advanced to K(3), V(2)
     __syncthreads();
+
+    f32x16 sa[kKB], sb[kKB];
+    bf16x8 pb[2 * kKB];
+    qk_tile<D>(sa, k_lds[0], koff, qf, c0);
+    mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
+    if constexpr (SQ) set_reference(sa, mx, m_run, c0);
+    else if constexpr (FIXED) m_run = mx * scale;
+    __syncthreads();  // every wave has read K(0) before iteration 0 refills its slot with K(4)
+
+    // lazy rescale before the scores of the tile whose maximum is mx are exponentiated:
+    // the reference maximum moves only when a row outgrows it by 2^8
+    auto rescale = [&](f32x16 (&st)[kKB]) {
+      if constexpr (SQ) {
+        folded_rescale<D>(st, o, mx, m_run, l_run, c0);
+      } else if (__any(mx * scale > m_run + kRescaleThreshold)) {
+        const float m_new = fmaxf(m_run, mx * scale);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int b = 0; b < G::DB; b++) o[b] *= alpha;
+        m_run = m_new;
+      }
+    };
+
+    // One pipelined iteration: consumes S(t) (scores in s_cur, maximum in mx), produces
+    // S(t+1) into s_nxt with its maximum, accumulates P(t) V(t).  Issues K(t+4) and
+    // V(t+3) into the ring and, before its barrier, waits for K(t+2) and V(t+1),
+    // which were issued two iterations earlier.
+    // In the unmasked variant tile t+1 exists and needs no mask, so the compute part
+    // is one branch-free block in which MFMA and the softmax VALU work interleave.
+    auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole, auto stage) {
+      constexpr bool MASKED = decltype(masked)::value;
+      constexpr bool WHOLE = decltype(whole)::value;
+      constexpr int ST = decltype(stage)::value;
+      // ring slot of tile t + d: a constant when the caller knows t's slot, so every
+      // LDS operand address is a register plus an immediate offset
+      auto ring = [&](int d) -> int {
+        if constexpr (ST >= 0) return (ST + d) % G::NSTAGE;
+        else return (t + d) % G::NSTAGE;
+      };
+      const int k0 = kb0 + t * kBN;
+      const bool has_next = MASKED ? t + 1 < n_tiles : true;
+      const int tk = WHOLE || t + 4 < n_tiles ? t + 4 : -1;
+      const int tv = WHOLE || t + 3 < n_tiles ? t + 3 : -1;
+      int issued = G::PER_WAVE;
+      constexpr bool SPREAD = WHOLE && !MASKED;  // steady state
+      const char* blk[G::PER_WAVE];
+      if constexpr (SPREAD) {
+#pragma unroll
+        for (int it = 0; it < G::PER_WAVE; it++) blk[it] = page_block(head_base[it], pid[it], page_bytes);
+      } else {
+        issued = issue(tk, tv);
+      }
+
+      if constexpr (!FIXED) rescale(s_cur);
+
+      if constexpr (MASKED) {
+        if (has_next) qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0);
+        l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
+        pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
+        if (has_next) {
+          if constexpr (FIXED) causal_mask(s_nxt, k0 + kBN, qpos, h);
+          else mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
+        }
+      } else if constexpr (SPREAD) {
+        qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0, [&](int i) {
+          const int it = G::PER_WAVE - 1 - i;
+          const bool is_v = it >= G::K_SLOTS;
+          issue_direct<D>(slot[it], blk[it], is_v ? v_lds[ring(3)] : k_lds[ring(4)]);  // V(t+3), K(t+4)
+        });
+        l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
+        pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
+        if constexpr (!FIXED) mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
+      } else {
+        qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0);
+        l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
+        pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
+        if constexpr (!FIXED) mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
+      }
+
+      if constexpr (SPREAD) {
+        // next page ids, read after this iteration's last LDS operand read so that no
+        // operand wait has to cover an outstanding scalar load
+#pragma unroll
+        for (int it = 0; it < G::PER_WAVE; it++) pid[it] = page_for(it, (it >= G::K_SLOTS ? tv : tk) + 1);
+      }
+      // K(t+2), V(t+1) (issued two iterations ago) must be in LDS before the barrier
+      if constexpr (WHOLE) wait_vmcnt<2 * G::PER_WAVE>();
+      else wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
+      issued_prev = issued;
+      __syncthreads();
+    };
+
+    int t = 0;
+    // unmasked part: S(t+1) needs no mask while t + 1 < n_full.  While the tiles an
+    // iteration issues (K(t+4), V(t+3)) are whole, the loads are unconditional; the
+    // prologue issued K(3) and V(2) in full whenever that holds for t = 0.
+    {
+      const int whole_end = (last_whole - 3 < n_tiles - 4 ? last_whole - 3 : n_tiles - 4);
+      // four tiles per trip (t % 4 == 0 at its top): every ring slot is a constant
+      for (; t + 4 < n_full && t + 3 < whole_end; t += 4) {
+        iteration(sa, sb, t, False{}, True{}, Stage<0>{});
+        iteration(sb, sa, t + 1, False{}, True{}, Stage<1>{});
+        iteration(sa, sb, t + 2, False{}, True{}, Stage<2>{});
+        iteration(sb, sa, t + 3, False{}, True{}, Stage<3>{});
+      }
+      for (; t + 2 < n_full && t + 1 < whole_end; t += 2) {
+        iteration(sa, sb, t, False{}, True{}, AnyStage{});
+        iteration(sb, sa, t + 1, False{}, True{}, AnyStage{});
+      }
+    }
+    for (; t + 2 < n_full; t += 2) {
+      iteration(sa, sb, t, False{}, False{}, AnyStage{});
+      iteration(sb, sa, t + 1, False{}, False{}, AnyStage{});
+    }
+    if (t + 1 < n_full) {
+      iteration(sa, sb, t, False{}, False{}, AnyStage{});
+      t++;
+#pragma unroll
+      for (int kb = 0; kb < kKB; kb++) sa[kb] = sb[kb];
+    }
+    for (; t < n_tiles; t += 2) {
+      iteration(sa, sb, t, True{}, False{}, AnyStage{});
+      if (t + 1 < n_tiles) iteration(sb, sa, t + 1, True{}, False{}, AnyStage{});
+    }
+
+    wait_vmcnt<0>();  // no load into this workgroup's LDS may outlive it
   };
 
-  int t = 0;
-  // unmasked part: S(t+1) needs no mask while t + 1 < n_full.  While the tiles an
-  // iteration issues (K(t+4), V(t+3)) are whole, the loads are unconditional; the
-  // prologue issued K(3) and V(2) in full whenever that holds for t = 0.
-  {
-    const int whole_end = (last_whole - 3 < n_tiles - 4 ? last_whole - 3 : n_tiles - 4);
-    // four tiles per trip (t % 4 == 0 at its top): every ring slot is a constant
-    for (; t + 4 < n_full && t + 3 < whole_end; t += 4) {
-      iteration(sa, sb, t, False{}, True{}, Stage<0>{});
-      iteration(sb, sa, t + 1, False{}, True{}, Stage<1>{});
-      iteration(sa, sb, t + 2, False{}, True{}, Stage<2>{});
-      iteration(sb, sa, t + 3, False{}, True{}, Stage<3>{});
-    }
-    for (; t + 2 < n_full && t + 1 < whole_end; t += 2) {
-      iteration(sa, sb, t, False{}, True{}, AnyStage{});
-      iteration(sb, sa, t + 1, False{}, True{}, AnyStage{});
-    }
-  }
-  for (; t + 2 < n_full; t += 2) {
-    iteration(sa, sb, t, False{}, False{}, AnyStage{});
-    iteration(sb, sa, t + 1, False{}, False{}, AnyStage{});
-  }
-  if (t + 1 < n_full) {
-    iteration(sa, sb, t, False{}, False{}, AnyStage{});
-    t++;
+  // Against a fixed reference the sums are exact unless a later score outgrew the
+  // first tile's maximum far enough to overflow; then the whole workgroup runs the
+  // unit again with the moving reference.
+  run(True{});
+  const bool bad = __any(r.valid && !all_finite<D>(o, l_run));
+  __syncthreads();  // the ring is free
+  int* vote = (int*)&k_lds[0][0];
+  if (lane == 0) vote[wave] = bad ? 1 : 0;
+  __syncthreads();
+  int again = 0;
 #pragma unroll
-    for (int kb = 0; kb < kKB; kb++) sa[kb] = sb[kb];
+  for (int w = 0; w < kWaves; w++) again |= vote[w];
+  if (again) {
+    __syncthreads();  // every wave has read the votes before the ring refills
+    run(False{});
   }
-  for (; t < n_tiles; t += 2) {
-    iteration(sa, sb, t, True{}, False{}, AnyStage{});
-    if (t + 1 < n_tiles) iteration(sb, sa, t + 1, True{}, False{}, AnyStage{});
-  }
-
-  wait_vmcnt<0>();  // no load into this workgroup's LDS may outlive it
   write_result<D>(p, r, o, l_run, m_run, 1.0f);
 }
 
@@ -824,12 +884,10 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_fp8_kernel(AttnPa
   const int vbase = v_offset(r.n, h);
 
   f32x16 o[G::DB];
-#pragma unroll
-  for (int b = 0; b < G::DB; b++) o[b] = f32x16{};
   // running maximum m of the lane's row (log2 units), -m as the score tiles'
   // accumulator input; m starts at the first tile's row maximum
-  float m_run = 0.0f, l_run = 0.0f, mx;
-  f32x16 cneg = f32x16{};
+  float m_run, l_run, mx;
+  f32x16 cneg;
 
   const int kb0 = u.key_begin;
   const int n_tiles = (u.key_end - kb0 + kBN - 1) / kBN;
@@ -897,112 +955,141 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_fp8_kernel(AttnPa
     }
   };
 
-  // ---- prologue: pairs -1 = {K(0)}, 0, 1, 2 loaded; -1 and 0 converted (K(0), K(1),
-  // V(0) in bf16), 1 resident, 2 in flight
+  // One pass over the unit.  FIXED: the reference point stays at the first tile's
+  // row maximum (no per-tile maximum, no rescale); otherwise it moves lazily.
+  auto run = [&](auto fixed) {
+    constexpr bool FIXED = decltype(fixed)::value;
 #pragma unroll
-  for (int it = 0; it < G8::NDMA; it++) pid[it] = page_for(it, 0);
-  issue(-1);
-  issue(0);
-  issue(1);
-  const int in_flight = issue(2);
-  wait_issued<G8::NDMA>(in_flight);
-  __syncthreads();
-  convert(-1, False{}, stg[3], k_lds[0], v_lds[1]);
-  convert(0, False{}, stg[0], k_lds[1], v_lds[0]);
-  __syncthreads();
-
-  f32x16 sa[kKB], sb[kKB];
-  bf16x8 pb[2 * kKB];
-  qk_tile<D>(sa, k_lds[0], koff, qf, cneg);
-  mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
-  set_reference(sa, mx, m_run, cneg);
-  __syncthreads();  // every wave has read K(0) before iteration 0 converts K(2) into its buffer
-
-
-  // One pipelined iteration: consumes S(t), produces S(t+1) from bf16 K(t+1) with its
-  // maximum, accumulates P(t) V(t), loads pair t+3 and converts pair t+1.  Before the
-  // barrier only this iteration's loads may still be in flight.
-  auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole, auto stage) {
-    constexpr bool MASKED = decltype(masked)::value;
-    constexpr bool WHOLE = decltype(whole)::value;
-    constexpr int ST = decltype(stage)::value;
-    auto buf = [&](int d) -> int {  // bf16 buffer of tile t + d
-      if constexpr (ST >= 0) return (ST + d) % G8::NBUF;
-      else return (t + d) % G8::NBUF;
-    };
-    auto slot_of = [&](int d) -> int {  // staging slot of pair t + d
-      if constexpr (ST >= 0) return (ST + d) % G8::NSTG;
-      else return (t + d) % G8::NSTG;
-    };
-    const int k0 = kb0 + t * kBN;
-    const bool has_next = MASKED ? t + 1 < n_tiles : true;
-    constexpr bool SPREAD = WHOLE && !MASKED;
-    int issued = G8::NDMA;
-    const char* blk[G8::NDMA];
-    if constexpr (SPREAD) {
+    for (int b = 0; b < G::DB; b++) o[b] = f32x16{};
+    m_run = 0.0f;
+    l_run = 0.0f;
+    cneg = f32x16{};
+    // ---- prologue: pairs -1 = {K(0)}, 0, 1, 2 loaded; -1 and 0 converted (K(0), K(1),
+    // V(0) in bf16), 1 resident, 2 in flight
 #pragma unroll
-      for (int it = 0; it < G8::NDMA; it++) blk[it] = page_block(head_base[it], pid[it], page_bytes);
-    } else {
-      issued = issue(t + 3);
-    }
-    folded_rescale<D>(s_cur, o, mx, m_run, l_run, cneg);
-    if constexpr (SPREAD) {
-      qk_tile<D>(s_nxt, k_lds[buf(1)], koff, qf, cneg, [&](int i) {
-        if (i < G8::NDMA) dma(i, stg[slot_of(3)], blk[i]);
-      });
-    } else {
-      if (!MASKED || has_next) qk_tile<D>(s_nxt, k_lds[buf(1)], koff, qf, cneg);
-    }
-    convert(t + 1, whole, stg[slot_of(1)], k_lds[buf(2)], v_lds[buf(1)]);
-    l_run = exp_pack<true>(s_cur, pb, l_run, m_run, 0.0f);
-    pv_tile<D>(o, v_lds[buf(0)], vbase, pb);
-    if constexpr (MASKED) {
-      if (has_next) mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
-    } else {
-      mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
-    }
-    if constexpr (SPREAD) {
-#pragma unroll
-      for (int it = 0; it < G8::NDMA; it++) pid[it] = page_for(it, tile_of(it, t + 4));
-    }
-    // pair t+2 (loaded one iteration ago) is converted in the next iteration
-    if constexpr (WHOLE) wait_vmcnt<G8::NDMA>();
-    else wait_issued<G8::NDMA>(issued);
+    for (int it = 0; it < G8::NDMA; it++) pid[it] = page_for(it, 0);
+    issue(-1);
+    issue(0);
+    issue(1);
+    const int in_flight = issue(2);
+    wait_issued<G8::NDMA>(in_flight);
     __syncthreads();
+    convert(-1, False{}, stg[3], k_lds[0], v_lds[1]);
+    convert(0, False{}, stg[0], k_lds[1], v_lds[0]);
+    __syncthreads();
+
+    f32x16 sa[kKB], sb[kKB];
+    bf16x8 pb[2 * kKB];
+    qk_tile<D>(sa, k_lds[0], koff, qf, cneg);
+    mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
+    set_reference(sa, mx, m_run, cneg);
+    __syncthreads();  // every wave has read K(0) before iteration 0 converts K(2) into its buffer
+
+
+    // One pipelined iteration: consumes S(t), produces S(t+1) from bf16 K(t+1) with its
+    // maximum, accumulates P(t) V(t), loads pair t+3 and converts pair t+1.  Before the
+    // barrier only this iteration's loads may still be in flight.
+    auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole, auto stage) {
+      constexpr bool MASKED = decltype(masked)::value;
+      constexpr bool WHOLE = decltype(whole)::value;
+      constexpr int ST = decltype(stage)::value;
+      auto buf = [&](int d) -> int {  // bf16 buffer of tile t + d
+        if constexpr (ST >= 0) return (ST + d) % G8::NBUF;
+        else return (t + d) % G8::NBUF;
+      };
+      auto slot_of = [&](int d) -> int {  // staging slot of pair t + d
+        if constexpr (ST >= 0) return (ST + d) % G8::NSTG;
+        else return (t + d) % G8::NSTG;
+      };
+      const int k0 = kb0 + t * kBN;
+      const bool has_next = MASKED ? t + 1 < n_tiles : true;
+      constexpr bool SPREAD = WHOLE && !MASKED;
+      int issued = G8::NDMA;
+      const char* blk[G8::NDMA];
+      if constexpr (SPREAD) {
+#pragma unroll
+        for (int it = 0; it < G8::NDMA; it++) blk[it] = page_block(head_base[it], pid[it], page_bytes);
+      } else {
+        issued = issue(t + 3);
+      }
+      if constexpr (!FIXED) folded_rescale<D>(s_cur, o, mx, m_run, l_run, cneg);
+      if constexpr (SPREAD) {
+        qk_tile<D>(s_nxt, k_lds[buf(1)], koff, qf, cneg, [&](int i) {
+          if (i < G8::NDMA) dma(i, stg[slot_of(3)], blk[i]);
+        });
+      } else {
+        if (!MASKED || has_next) qk_tile<D>(s_nxt, k_lds[buf(1)], koff, qf, cneg);
+      }
+      convert(t + 1, whole, stg[slot_of(1)], k_lds[buf(2)], v_lds[buf(1)]);
+      l_run = exp_pack<true>(s_cur, pb, l_run, m_run, 0.0f);
+      pv_tile<D>(o, v_lds[buf(0)], vbase, pb);
+      if constexpr (MASKED) {
+        if (has_next) {
+          if constexpr (FIXED) causal_mask(s_nxt, k0 + kBN, qpos, h);
+          else mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
+        }
+      } else if constexpr (!FIXED) {
+        mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
+      }
+      if constexpr (SPREAD) {
+#pragma unroll
+        for (int it = 0; it < G8::NDMA; it++) pid[it] = page_for(it, tile_of(it, t + 4));
+      }
+      // pair t+2 (loaded one iteration ago) is converted in the next iteration
+      if constexpr (WHOLE) wait_vmcnt<G8::NDMA>();
+      else wait_issued<G8::NDMA>(issued);
+      __syncthreads();
+    };
+
+    int t = 0;
+    {
+      // steady state: the pair loaded (t+3: K(t+4), V(t+3)) exists and the pair
+      // converted (t+1: K(t+2), V(t+1)) needs no zeroing
+      const int whole_end = (n_tiles - 4 < last_whole - 1 ? n_tiles - 4 : last_whole - 1);
+      for (; t + 4 < n_full && t + 3 < whole_end; t += 4) {
+        iteration(sa, sb, t, False{}, True{}, Stage<0>{});
+        iteration(sb, sa, t + 1, False{}, True{}, Stage<1>{});
+        iteration(sa, sb, t + 2, False{}, True{}, Stage<2>{});
+        iteration(sb, sa, t + 3, False{}, True{}, Stage<3>{});
+      }
+      for (; t + 2 < n_full && t + 1 < whole_end; t += 2) {
+        iteration(sa, sb, t, False{}, True{}, AnyStage{});
+        iteration(sb, sa, t + 1, False{}, True{}, AnyStage{});
+      }
+    }
+    for (; t + 2 < n_full; t += 2) {
+      iteration(sa, sb, t, False{}, False{}, AnyStage{});
+      iteration(sb, sa, t + 1, False{}, False{}, AnyStage{});
+    }
+    if (t + 1 < n_full) {
+      iteration(sa, sb, t, False{}, False{}, AnyStage{});
+      t++;
+#pragma unroll
+      for (int kb = 0; kb < kKB; kb++) sa[kb] = sb[kb];
+    }
+    for (; t < n_tiles; t += 2) {
+      iteration(sa, sb, t, True{}, False{}, AnyStage{});
+      if (t + 1 < n_tiles) iteration(sb, sa, t + 1, True{}, False{}, AnyStage{});
+    }
+
+    wait_vmcnt<0>();  // no load into this workgroup's LDS may outlive it
   };
 
-  int t = 0;
-  {
-    // steady state: the pair loaded (t+3: K(t+4), V(t+3)) exists and the pair
-    // converted (t+1: K(t+2), V(t+1)) needs no zeroing
-    const int whole_end = (n_tiles - 4 < last_whole - 1 ? n_tiles - 4 : last_whole - 1);
-    for (; t + 4 < n_full && t + 3 < whole_end; t += 4) {
-      iteration(sa, sb, t, False{}, True{}, Stage<0>{});
-      iteration(sb, sa, t + 1, False{}, True{}, Stage<1>{});
-      iteration(sa, sb, t + 2, False{}, True{}, Stage<2>{});
-      iteration(sb, sa, t + 3, False{}, True{}, Stage<3>{});
-    }
-    for (; t + 2 < n_full && t + 1 < whole_end; t += 2) {
-      iteration(sa, sb, t, False{}, True{}, AnyStage{});
-      iteration(sb, sa, t + 1, False{}, True{}, AnyStage{});
-    }
-  }
-  for (; t + 2 < n_full; t += 2) {
-    iteration(sa, sb, t, False{}, False{}, AnyStage{});
-    iteration(sb, sa, t + 1, False{}, False{}, AnyStage{});
-  }
-  if (t + 1 < n_full) {
-    iteration(sa, sb, t, False{}, False{}, AnyStage{});
-    t++;
+  // as in the bf16 kernel: a fixed reference, and a second pass with the moving one
+  // if anything overflowed
+  run(True{});
+  const bool bad = __any(r.valid && !all_finite<D>(o, l_run));
+  __syncthreads();  // the staging ring and the bf16 buffers are free
+  int* vote = (int*)&stg[0][0];
+  if (lane == 0) vote[wave] = bad ? 1 : 0;
+  __syncthreads();
+  int again = 0;
 #pragma unroll
-    for (int kb = 0; kb < kKB; kb++) sa[kb] = sb[kb];
+  for (int w = 0; w < kWaves; w++) again |= vote[w];
+  if (again) {
+    __syncthreads();  // every wave has read the votes before the ring refills
+    run(False{});
   }
-  for (; t < n_tiles; t += 2) {
-    iteration(sa, sb, t, True{}, False{}, AnyStage{});
-    if (t + 1 < n_tiles) iteration(sb, sa, t + 1, True{}, False{}, AnyStage{});
-  }
-
-  wait_vmcnt<0>();  // no load into this workgroup's LDS may outlive it
   write_result<D>(p, r, o, l_run, m_run, vscale);
 }
 

@@ -227,6 +227,59 @@ def test_needle_key_dominates(where):
         run.close()
 
 
+# A few query rows are aimed at one key far past the unit's first tile, with a
+# logit margin of about 200 (natural units) over every other key: exponentials
+# against the first tile's maximum overflow fp32 there, and the rows must still
+# come out as the oracle's (nearly one-hot) softmax of that key.
+FAR_ABOVE = {
+    "bf16_tile3": (wl.KV_BF16, False, 128, "tile3", 0),
+    "bf16_diagonal": (wl.KV_BF16, False, 128, "diagonal", 0),
+    "bf16_d64_tile3": (wl.KV_BF16, False, 64, "tile3", 0),
+    "scaled_q_tile3": (wl.KV_BF16, True, 128, "tile3", 0),
+    "scaled_q_diagonal": (wl.KV_BF16, True, 128, "diagonal", 0),
+    "fp8_tile3": (wl.KV_FP8_E4M3, False, 128, "tile3", 0),
+    "fp8_diagonal": (wl.KV_FP8_E4M3, False, 128, "diagonal", 0),
+    "bf16_split": (wl.KV_BF16, False, 128, "tile3", 128),
+}
+
+
+@pytest.mark.parametrize("name", sorted(FAR_ABOVE))
+def test_scores_far_above_the_first_tile(name):
+    kv_dtype, scaled_q, d, where, split = FAR_ABOVE[name]
+    P, E, B = 200, 60, 12.0
+    w = wl.make_custom([P, 90], [E, 50], 8, 2, d, kv_dtype=kv_dtype, seed=31)
+    g = torch.Generator().manual_seed(5)
+    u = torch.randn(d, generator=g, dtype=torch.float64)
+    u /= u.norm()
+    a = 200.0 * math.sqrt(d) / B  # logit A B / sqrt(d) = 200
+    hot = [10, 33, E - 1]
+    q0 = wl.request_q(w, 0, DEV).clone()
+    k0, v0 = (t.clone() for t in wl.request_kv(w, 0, DEV))
+    for i in hot:
+        j = {"tile3": 3 * 64 + 5, "diagonal": P + i}[where]
+        q0[i, 0] = (a * u).to(torch.bfloat16).to(DEV)
+        k0[j, 0] = (B * u).to(torch.bfloat16).to(DEV)
+        v0[j, 0] = 3.0
+    kv = lambda r: (k0, v0) if r == 0 else wl.request_kv(w, r, DEV)
+    qq = lambda r: q0 if r == 0 else wl.request_q(w, r, DEV)
+    print(f"[extend] far_above {name}: d={d} fp8={kv_dtype} scaled_q={int(scaled_q)} split={split}", flush=True)
+    run = GpuRun(w, overrides={"kv": kv, "q": qq}, split_keys=split, scaled_q=scaled_q)
+    try:
+        run.store()
+        out, lse = run.attend(want_lse=True)
+        ref, gidx = oracle_rows(w, run.q, None, want_lse=True, kv_override=kv,
+                                scaled_q=scaled_q and kv_dtype == wl.KV_BF16)
+        ref, ref_lse = ref
+        compare(_f64(out)[gidx], ref, f"far_above_{name}")
+        lerr = np.abs(lse.cpu().numpy()[gidx] - ref_lse).max()
+        print(f"[parity] far_above_{name}: lse max err {lerr:.3e}", flush=True)
+        assert lerr <= 2e-3 * max(1.0, float(np.abs(ref_lse).max()))
+        # the aimed rows really are dominated by the key they aim at
+        assert float(ref_lse[hot, 0].min()) > 150.0
+    finally:
+        run.close()
+
+
 @pytest.mark.parametrize("kv_dtype", [wl.KV_BF16, wl.KV_FP8_E4M3])
 def test_split_invariance_across_page_boundaries(kv_dtype):
     """One logical sequence, cut into cached prefix + suffix at several page
