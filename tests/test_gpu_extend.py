@@ -240,6 +240,8 @@ FAR_ABOVE = {
     "fp8_tile3": (wl.KV_FP8_E4M3, False, 128, "tile3", 0),
     "fp8_diagonal": (wl.KV_FP8_E4M3, False, 128, "diagonal", 0),
     "bf16_split": (wl.KV_BF16, False, 128, "tile3", 128),
+    "fp8_split": (wl.KV_FP8_E4M3, False, 128, "diagonal", 128),
+    "fp8_d64_tile3": (wl.KV_FP8_E4M3, False, 64, "tile3", 0),
 }
 
 
