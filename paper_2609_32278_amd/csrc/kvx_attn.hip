@@ -701,7 +701,14 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       if constexpr (WHOLE) wait_vmcnt<2 * G::PER_WAVE>();
       else wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
       issued_prev = issued;
+      // Folded form: nothing crosses the barrier in the schedule.  Left free, the
+      // compiler moves a tile's register-only exponentials into the next
+      // iteration, which then carries twice the VALU work beside its products
+      // while the one before has none; the exact form, an FMA per score heavier,
+      // schedules better without the fence.
+      if constexpr (SQ) __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
+      if constexpr (SQ) __builtin_amdgcn_sched_barrier(0);
     };
 
     int t = 0;
@@ -1038,7 +1045,10 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_fp8_kernel(AttnPa
       // pair t+2 (loaded one iteration ago) is converted in the next iteration
       if constexpr (WHOLE) wait_vmcnt<G8::NDMA>();
       else wait_issued<G8::NDMA>(issued);
+      // each iteration keeps its own softmax work (as in the bf16 kernel's folded form)
+      __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
     };
 
     int t = 0;
