@@ -130,7 +130,10 @@ def _check_plan(w, split=0):
                 assert rng[0][0] == 0 and rng[-1][1] == P + t0 + ntok
                 for (a, b_, pa, _), (c, _, pc, _) in zip(rng, rng[1:]):
                     assert b_ == c and b_ % 64 == 0
-                    assert b_ <= P + t0  # earlier parts hold keys every row of the tile sees
+                    # earlier parts hold keys every row of the tile sees, so each part's first
+                    # key is visible to all its rows (the attention kernel takes that key's
+                    # tile maximum as its softmax reference)
+                    assert b_ <= P + t0
                 assert (len(rng) == 1) == (rng[0][2] == -1)
             assert (covered == 1).all()
     assert not seen
