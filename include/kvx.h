@@ -322,7 +322,7 @@ int kv_pool_set_split_keys(kvx_pool *pool, int32_t keys);
  * c = float32(sm_scale * float32(log2 e)) in float32 and rounded to bf16 (round to
  * nearest even) when it is loaded, and the scores of those queries are taken in
  * base 2: o = softmax_j(ln 2 * bf16(q * c) . k_j) v_j.  This removes one VALU
- * instruction per (query, key) pair, about 4% of the kernel time on long key
+ * instruction per (query, key) pair, about 5% of the kernel time on long key
  * ranges, and adds one more bf16 rounding of q (2^-9 relative per element): the
  * error against the exact attention grows where scores are large (about twice
  * the default's at query scale 4).  The prefill kernel of an fp8 pool always takes
