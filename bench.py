@@ -61,10 +61,49 @@ def is_decode(config: str) -> bool:
     return config.startswith("decode")
 
 
+def code_only(text: str) -> str:
+    """C/C++ source text without its comments and blank lines, each line stripped:
+    an edit of comments or layout alone leaves it unchanged."""
+    out, i, n, quote = [], 0, len(text), None
+    while i < n:
+        c = text[i]
+        if quote:
+            out.append(c)
+            if c == "\\" and i + 1 < n:
+                out.append(text[i + 1])
+                i += 2
+                continue
+            if c == quote:
+                quote = None
+            i += 1
+        elif c in "\"'":
+            quote = c
+            out.append(c)
+            i += 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    lines = (ln.strip() for ln in "".join(out).splitlines())
+    return "\n".join(ln for ln in lines if ln)
+
+
+def code_hash(path: str) -> str:
+    """sha256[:16] of a source file's code (comments and blank lines removed)."""
+    return hashlib.sha256(code_only(open(path, encoding="utf-8").read()).encode()).hexdigest()[:16]
+
+
 def attn_source_hash(config: str = "llama8b") -> str:
+    """Code hash of the attention (or decode) kernel source: committed counter
+    summaries carry it, and their traffic is used only while it matches."""
     name = "kvx_decode.hip" if is_decode(config) else "kvx_attn.hip"
-    path = os.path.join(ROOT, "paper_2609_32278_amd", "csrc", name)
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    return code_hash(os.path.join(ROOT, "paper_2609_32278_amd", "csrc", name))
 
 
 def traffic_from_profiles(config: str):
@@ -75,7 +114,7 @@ def traffic_from_profiles(config: str):
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    m_hash = re.search(r"kernel source sha256\[:16\]:\s*`?([0-9a-f]{16})", text)
+    m_hash = re.search(r"kernel code sha256\[:16\][^:`]*:\s*`?([0-9a-f]{16})", text)
     m_bytes = re.search(r"HBM bytes per launch \(scaled\):\s*`?([0-9.eE+]+)", text)
     if not (m_hash and m_bytes) or m_hash.group(1) != attn_source_hash(config):
         return None
@@ -293,8 +332,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); this build "
-              f"has no multi-GPU path", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): kvx has no "
+              f"multi-GPU path", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -31,13 +31,13 @@
 //     the first tile's maximum by so much that an exponential or a sum overflows
 //     fp32.  A workgroup whose results are not all finite therefore runs the
 //     unit a second time with a moving reference (a row's maximum moves when it
-//     grows by more than 2^8, with O and l rescaled).  Folded form (always on an fp8 pool; on a bf16 pool when
-//     the pool's scaled-Q setting asks for it): the FMA goes away.  Q is
-//     multiplied by scale (times k_scale on an fp8 pool) when it is loaded and
-//     rounded once more to bf16 (2^-9 relative; on an fp8 pool far below the
-//     e4m3 rounding of K), and the first MFMA of every score tile takes -m (a
-//     16-register block) as its accumulator input, so the tile comes out as
-//     s * scale - m and p is exp2 of it directly;
+//     grows by more than 2^8, with O and l rescaled).  Folded form (always on an
+//     fp8 pool; on a bf16 pool when the pool's scaled-Q setting asks for it): the
+//     FMA goes away.  Q is multiplied by scale (times k_scale on an fp8 pool)
+//     when it is loaded and rounded once more to bf16 (2^-9 relative; on an fp8
+//     pool far below the e4m3 rounding of K), and the first MFMA of every score
+//     tile takes -m (a 16-register block) as its accumulator input, so the tile
+//     comes out as s * scale - m and p is exp2 of it directly;
 //   * O^T += V^T(t) P^T(t): V^T from LDS is the A operand, P stays in registers
 //     as bf16 pairs, and the row sums are taken over those bf16 values (v_dot2).
 // Software pipeline: the MFMAs of S(t+1) are issued among the exp / pack of tile
@@ -635,10 +635,10 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       }
     };
 
-    // One pipelined iteration: consumes S(t) (scores in s_cur, maximum in mx), produces
-    // S(t+1) into s_nxt with its maximum, accumulates P(t) V(t).  Issues K(t+4) and
-    // V(t+3) into the ring and, before its barrier, waits for K(t+2) and V(t+1),
-    // which were issued two iterations earlier.
+    // One pipelined iteration: consumes S(t) (scores in s_cur; in the second pass its
+    // maximum in mx), produces S(t+1) into s_nxt (and its maximum), accumulates
+    // P(t) V(t).  Issues K(t+4) and V(t+3) into the ring and, before its barrier,
+    // waits for K(t+2) and V(t+1), which were issued two iterations earlier.
     // In the unmasked variant tile t+1 exists and needs no mask, so the compute part
     // is one branch-free block in which MFMA and the softmax VALU work interleave.
     auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole, auto stage) {
@@ -993,9 +993,10 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_fp8_kernel(AttnPa
     __syncthreads();  // every wave has read K(0) before iteration 0 converts K(2) into its buffer
 
 
-    // One pipelined iteration: consumes S(t), produces S(t+1) from bf16 K(t+1) with its
-    // maximum, accumulates P(t) V(t), loads pair t+3 and converts pair t+1.  Before the
-    // barrier only this iteration's loads may still be in flight.
+    // One pipelined iteration: consumes S(t), produces S(t+1) from bf16 K(t+1) (in the
+    // second pass with its maximum), accumulates P(t) V(t), loads pair t+3 and
+    // converts pair t+1.  Before the barrier only this iteration's loads may still be
+    // in flight.
     auto iteration = [&](f32x16 (&s_cur)[kKB], f32x16 (&s_nxt)[kKB], int t, auto masked, auto whole, auto stage) {
       constexpr bool MASKED = decltype(masked)::value;
       constexpr bool WHOLE = decltype(whole)::value;
