@@ -41,8 +41,9 @@
 //   * O^T += V^T(t) P^T(t): V^T from LDS is the A operand, P stays in registers
 //     as bf16 pairs, and the row sums are taken over those bf16 values (v_dot2).
 // Software pipeline: the MFMAs of S(t+1) are issued among the exp / pack of tile
-// t; in the second pass the MFMAs of O += P(t) V(t) overlap the row maximum of
-// tile t+1.
+// t; the MFMAs of O += P(t) V(t) overlap, in the exact form's fixed-reference
+// pass, the FMAs that turn S(t+1) into exponents, and in the second pass the row
+// maximum of tile t+1.
 // MFMA row m of the S^T product is assigned key perm(m) (bits 2 and 3 of m
 // swapped), which makes the keys a lane holds in the S^T accumulators exactly
 // the 8 consecutive keys its B operand slot needs in the V^T P^T product.
@@ -317,6 +318,15 @@ __device__ __forceinline__ bool all_finite(const f32x16 (&o)[Geom<D>::DB], float
 #pragma unroll
     for (int i = 0; i < 16; i++) acc += o[b][i];
   return __builtin_isfinite(acc);
+}
+
+// s * scale - m in place (the exponent of the exact form), exactly as exp_pack forms it.
+__device__ __forceinline__ void prescale(f32x16 (&s)[kKB], float scale, float m_run) {
+  const float neg = -m_run;
+#pragma unroll
+  for (int kb = 0; kb < kKB; kb++)
+#pragma unroll
+    for (int i = 0; i < 16; i++) s[kb][i] = __builtin_fmaf(s[kb][i], scale, neg);
 }
 
 // p = exp2(s * scale - m) as bf16 pairs (the P^T B operands, one per page of the
@@ -618,6 +628,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
     mx = n_full > 0 ? row_max<false>(sa, kb0, qpos, h) : row_max<true>(sa, kb0, qpos, h);
     if constexpr (SQ) set_reference(sa, mx, m_run, c0);
     else if constexpr (FIXED) m_run = mx * scale;
+    if constexpr (FIXED && !SQ) prescale(sa, scale, m_run);
     __syncthreads();  // every wave has read K(0) before iteration 0 refills its slot with K(4)
 
     // lazy rescale before the scores of the tile whose maximum is mx are exponentiated:
@@ -666,14 +677,19 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       }
 
       if constexpr (!FIXED) rescale(s_cur);
+      // Exact form with the fixed reference: S(t) already holds s * scale - m, formed
+      // one iteration earlier beside the PV products (which have no other VALU
+      // work) by the same FMA exp_pack would use.
+      constexpr bool PRE = FIXED && !SQ;
 
       if constexpr (MASKED) {
         if (has_next) qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0);
-        l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
+        l_run = exp_pack<SQ || PRE>(s_cur, pb, l_run, m_run, scale);
         pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
         if (has_next) {
           if constexpr (FIXED) causal_mask(s_nxt, k0 + kBN, qpos, h);
           else mx = row_max<true>(s_nxt, k0 + kBN, qpos, h);
+          if constexpr (PRE) prescale(s_nxt, scale, m_run);
         }
       } else if constexpr (SPREAD) {
         qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0, [&](int i) {
@@ -681,14 +697,16 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
           const bool is_v = it >= G::K_SLOTS;
           issue_direct<D>(slot[it], blk[it], is_v ? v_lds[ring(3)] : k_lds[ring(4)]);  // V(t+3), K(t+4)
         });
-        l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
+        l_run = exp_pack<SQ || PRE>(s_cur, pb, l_run, m_run, scale);
         pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
         if constexpr (!FIXED) mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
+        if constexpr (PRE) prescale(s_nxt, scale, m_run);
       } else {
         qk_tile<D>(s_nxt, k_lds[ring(1)], koff, qf, c0);
-        l_run = exp_pack<SQ>(s_cur, pb, l_run, m_run, scale);
+        l_run = exp_pack<SQ || PRE>(s_cur, pb, l_run, m_run, scale);
         pv_tile<D>(o, v_lds[ring(0)], vbase, pb);
         if constexpr (!FIXED) mx = row_max<false>(s_nxt, k0 + kBN, qpos, h);
+        if constexpr (PRE) prescale(s_nxt, scale, m_run);
       }
 
       if constexpr (SPREAD) {
@@ -701,14 +719,13 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_kernel(AttnParams
       if constexpr (WHOLE) wait_vmcnt<2 * G::PER_WAVE>();
       else wait_issued<2 * G::PER_WAVE>(issued + issued_prev);
       issued_prev = issued;
-      // Folded form: nothing crosses the barrier in the schedule.  Left free, the
-      // compiler moves a tile's register-only exponentials into the next
-      // iteration, which then carries twice the VALU work beside its products
-      // while the one before has none; the exact form, an FMA per score heavier,
-      // schedules better without the fence.
-      if constexpr (SQ) __builtin_amdgcn_sched_barrier(0);
+      // Nothing crosses the barrier in the schedule (folded form, and the exact
+      // form's fixed-reference pass).  Left free, the compiler moves a tile's
+      // register-only exponentials into the next iteration, which then carries
+      // twice the VALU work beside its products while the one before has none.
+      if constexpr (SQ || FIXED) __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
-      if constexpr (SQ) __builtin_amdgcn_sched_barrier(0);
+      if constexpr (SQ || FIXED) __builtin_amdgcn_sched_barrier(0);
     };
 
     int t = 0;
