@@ -252,8 +252,10 @@ int extend_attention(kvx_pool *pool, const kvx_batch *batch, const void *q, int3
 
 /*
  * extend_attention for callers that cannot allocate device memory during the
- * call: code under HIP graph capture, tight serving loops, harnesses that forbid
- * hipMalloc.  Same arguments, operation, kernels and result as extend_attention
+ * call: tight serving loops and harnesses that forbid hipMalloc.  It is still
+ * not capturable into a HIP graph: each call builds its plan on the host and
+ * copies it from a host vector that is freed when the call returns, so a
+ * captured copy would read freed memory on replay.  Same arguments, operation, kernels and result as extend_attention
  * (bit for bit when both split the key ranges alike), but the work plan and the
  * partial results of split key ranges go into one fixed device array of the
  * library instead of the pool's staging buffer and workspace; the call makes no

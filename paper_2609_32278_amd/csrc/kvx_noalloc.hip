@@ -1,6 +1,7 @@
 // extend_attention_noalloc: extend_attention for callers that cannot allocate
-// device memory during the call (code under HIP graph capture, tight serving
-// loops, harnesses that forbid hipMalloc).
+// device memory during the call (tight serving loops, harnesses that forbid
+// hipMalloc).  It is not capturable into a HIP graph: the plan is built on the
+// host per call and copied from a host vector freed when the call returns.
 //
 // The work plan and the partial results of split key ranges go into one fixed
 // device array, `scratch`, instead of the pool's staging buffer and growable
