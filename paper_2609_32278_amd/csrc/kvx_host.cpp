@@ -10,8 +10,10 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <map>
 #include <numeric>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "kvx_internal.h"
@@ -266,8 +268,11 @@ struct Plan {
 //     far longer than the average work per workgroup slot, the key range is split at
 //     multiples of the tile width into parts merged by log-sum-exp afterwards;
 //   * each (request, KV head) is bound to one XCD (KV head h -> XCD h % 8 when the
-//     head count is a multiple of 8, else greedy by cost), so the workgroups that
-//     stream the same K/V pages share one L2;
+//     head count is a multiple of 8), so the workgroups that stream the same K/V
+//     pages share one L2; for other head counts each (request, KV head, part of a
+//     split key range) is bound greedily by cost, so that a batch of few long
+//     requests still spreads its parts over all eight XCDs (the parts of one key
+//     range, read by every tile of the request, stay together);
 //   * within an XCD, requests go longest first and a request's tiles longest first.
 int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, int32_t Hkv, int32_t split_keys,
               int64_t max_parts, Plan& plan) {
@@ -314,23 +319,43 @@ int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, in
     }
   }
 
-  // (request, head) groups -> XCDs
-  std::vector<int64_t> group_cost((size_t)b->num_reqs * Hkv, 0);
-  for (const Tile& t : tiles) group_cost[(size_t)t.r * Hkv + t.h] += t.cost;
-  std::vector<int> group_xcd(group_cost.size(), 0);
-  if (Hkv % kvx::kNumXcd == 0) {
-    for (size_t g = 0; g < group_cost.size(); g++) group_xcd[g] = (int)(g % Hkv) % kvx::kNumXcd;
-  } else {
-    std::vector<size_t> order(group_cost.size());
-    std::iota(order.begin(), order.end(), 0);
-    std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t c) { return group_cost[a] > group_cost[c]; });
+  // Key ranges of a tile: [0, split), [split, 2 split), ... up to the last boundary
+  // <= qpos0, then the rest to kend; one range when unsplit.
+  auto ranges_of = [&](const Tile& t) {
+    std::vector<std::pair<int64_t, int64_t>> rg;
+    if (split > 0 && t.qpos0 / split > 0) {
+      int64_t kb = 0;
+      for (int64_t bnd = split; bnd <= t.qpos0; bnd += split) {
+        rg.push_back({kb, bnd});
+        kb = bnd;
+      }
+      rg.push_back({kb, t.kend});
+    } else {
+      rg.push_back({0, t.kend});
+    }
+    return rg;
+  };
+  // XCD of (request, head, part index).  Multiples of 8 heads: head h -> XCD h % 8
+  // for every part.  Otherwise greedy by cost over (request, head, part) keys,
+  // costliest first, each to the least loaded XCD.
+  const bool by_head = Hkv % kvx::kNumXcd == 0;
+  std::map<std::tuple<int, int, int64_t>, int> bind_xcd;
+  if (!by_head) {
+    std::map<std::tuple<int, int, int64_t>, int64_t> bind_cost;
+    for (const Tile& t : tiles) {
+      const auto rg = ranges_of(t);
+      for (size_t i = 0; i < rg.size(); i++)
+        bind_cost[{t.r, t.h, (int64_t)i}] += ceil_div(rg[i].second - rg[i].first, BN);
+    }
+    std::vector<std::pair<std::tuple<int, int, int64_t>, int64_t>> order(bind_cost.begin(), bind_cost.end());
+    std::stable_sort(order.begin(), order.end(), [](const auto& a, const auto& c) { return a.second > c.second; });
     int64_t load[kvx::kNumXcd] = {0};
-    for (size_t g : order) {
+    for (const auto& kc : order) {
       int best = 0;
       for (int x = 1; x < kvx::kNumXcd; x++)
         if (load[x] < load[best]) best = x;
-      group_xcd[g] = best;
-      load[best] += group_cost[g];
+      bind_xcd[kc.first] = best;
+      load[best] += kc.second;
     }
   }
   // request order: total cost, longest first
@@ -354,24 +379,13 @@ int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, in
   plan.merges.clear();
   plan.n_parts = 0;
   for (const Tile& t : tiles) {
-    const int x = group_xcd[(size_t)t.r * Hkv + t.h];
     AttnUnit u;
     u.qo_row0 = (int32_t)(qo[(size_t)t.r] + t.tok0);
     u.q_pos0 = (int32_t)t.qpos0;
     u.page_base = b->page_indptr[t.r];
     u.head_ntok = (t.h << 16) | t.ntok;
     u.req = t.r;
-    std::vector<std::pair<int64_t, int64_t>> ranges;
-    if (split > 0 && t.qpos0 / split > 0) {
-      int64_t kb = 0;
-      for (int64_t bnd = split; bnd <= t.qpos0; bnd += split) {
-        ranges.push_back({kb, bnd});
-        kb = bnd;
-      }
-      ranges.push_back({kb, t.kend});
-    } else {
-      ranges.push_back({0, t.kend});
-    }
+    const std::vector<std::pair<int64_t, int64_t>> ranges = ranges_of(t);
     const bool is_split = ranges.size() > 1;
     if (is_split) {
       MergeUnit m;
@@ -381,7 +395,9 @@ int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, in
       m.nparts = (int32_t)ranges.size();
       plan.merges.push_back(m);
     }
-    for (const auto& rg : ranges) {
+    for (size_t i = 0; i < ranges.size(); i++) {
+      const auto& rg = ranges[i];
+      const int x = by_head ? t.h % kvx::kNumXcd : bind_xcd.at({t.r, t.h, (int64_t)i});
       u.key_begin = (int32_t)rg.first;
       u.key_end = (int32_t)rg.second;
       u.part = is_split ? (int32_t)plan.n_parts++ : -1;

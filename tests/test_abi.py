@@ -203,6 +203,26 @@ def test_plan_balances_xcds_for_eight_kv_heads():
     assert cost.max() / cost.min() < 1.0001
 
 
+@pytest.mark.parametrize("hkv,extend", [(1, [53, 200]), (2, [53, 200]), (1, [1, 1])])
+def test_plan_spreads_few_long_requests_over_all_xcds(hkv, extend):
+    """Two requests with 4M- and 1M-token prefixes and 1-2 KV heads: the planner
+    splits their key ranges, and binds each (request, KV head, part) rather than
+    each (request, KV head), so all eight XCDs carry work; units that read the same
+    key range of one (request, KV head) stay on one XCD."""
+    w = wl.make_custom([4194319, 1048577], extend, 8 * hkv, hkv, 128, seed=41)
+    items = _check_plan(w)
+    real = items[items["req"] >= 0]
+    assert (real["part"] >= 0).all()
+    cost = np.zeros(8)
+    np.add.at(cost, real["xcd"], (real["key_end"] - real["key_begin"]).astype(np.float64))
+    assert cost.max() / cost.mean() < 1.15, cost
+    if extend[0] > 1:
+        xcd_of = {}
+        for it in real:
+            key = (int(it["req"]), int(it["kv_head"]), int(it["key_begin"]))
+            assert xcd_of.setdefault(key, int(it["xcd"])) == int(it["xcd"])
+
+
 def test_headers_compile_as_c99_and_work_from_c(tmp_path):
     """A C99 program (tests/c_abi/consumer.c) includes both public headers with
     -pedantic -Werror, links libkvx.so and calls the host-only entry points."""
