@@ -266,7 +266,8 @@ struct Plan {
 //     = 256 rows) per KV head; a tile covers keys [0, P + last token of the tile];
 //   * when the batch has too little work to fill the chip, or a tile's key range is
 //     far longer than the average work per workgroup slot, the key range is split at
-//     multiples of the tile width into parts merged by log-sum-exp afterwards;
+//     multiples of the tile width into parts merged by log-sum-exp afterwards (the
+//     parts lengthened slightly when that saves a nearly empty last round of units);
 //   * each (request, KV head) is bound to one XCD (KV head h -> XCD h % 8 when the
 //     head count is a multiple of 8), so the workgroups that stream the same K/V
 //     pages share one L2; for other head counts each (request, KV head, part of a
@@ -316,6 +317,36 @@ int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, in
       }
       if (parts <= max_parts) break;
       split *= 2;
+    }
+    if (split_keys <= 0) {
+      // Whole rounds: a unit count a little past a multiple of the 256 slots leaves a
+      // nearly empty last round.  Lengthen the parts (in whole tiles) when that
+      // removes it for less than the round costs: the smallest split below
+      // split * (k + 1) / k that yields at most k rounds of units (the count never
+      // grows with the split, so a bisection finds it).
+      std::vector<std::pair<int64_t, int64_t>> starts;  // (first query position, tiles)
+      for (const Tile& t : tiles) {
+        if (!starts.empty() && starts.back().first == t.qpos0) starts.back().second++;
+        else starts.push_back({t.qpos0, 1});
+      }
+      auto units_at = [&](int64_t s) {
+        int64_t n = 0;
+        for (const auto& q : starts) n += (q.first / s + 1) * q.second;
+        return n;
+      };
+      const int64_t k = (units_at(split) - 1) / kPlanSlots;
+      if (k >= 1) {
+        const int64_t target = k * kPlanSlots;
+        int64_t lo = split / BN + 1, hi = (split * (k + 1) / k - 1) / BN;  // split lengths in tiles
+        if (lo <= hi && units_at(hi * BN) <= target) {
+          while (lo < hi) {
+            const int64_t mid = lo + (hi - lo) / 2;
+            if (units_at(mid * BN) <= target) hi = mid;
+            else lo = mid + 1;
+          }
+          split = lo * BN;
+        }
+      }
     }
   }
 

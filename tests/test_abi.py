@@ -189,7 +189,9 @@ def test_plan_splits_decode_like_batches_automatically():
     w = wl.make_custom([32768], [64], 32, 8, 128)
     items = _check_plan(w)
     real = items[items["req"] >= 0]
-    assert len(real) >= 256 and (real["part"] >= 0).all()
+    # one round that fills at least 90% of the 256 workgroup slots (not 264 units,
+    # whose last 8 would run as a second round)
+    assert 0.9 * 256 <= len(real) <= 256 and (real["part"] >= 0).all()
 
 
 def test_plan_balances_xcds_for_eight_kv_heads():
@@ -221,6 +223,31 @@ def test_plan_spreads_few_long_requests_over_all_xcds(hkv, extend):
         for it in real:
             key = (int(it["req"]), int(it["kv_head"]), int(it["key_begin"]))
             assert xcd_of.setdefault(key, int(it["xcd"])) == int(it["xcd"])
+
+
+@pytest.mark.parametrize("prefix,extend,hq,hkv", [
+    ([131072], [512], 32, 8),                    # one returning agent
+    ([200000], [300], 64, 8),
+    ([4194319, 1048577], [53, 200], 8, 1),
+    ([4194319, 1048577], [53, 200], 16, 2),
+])
+def test_split_parts_fill_whole_rounds(prefix, extend, hq, hkv):
+    """A few tiles with long key ranges: the automatic split would leave a unit count
+    a little past two rounds of the 256 workgroup slots (519-576 units); the planner
+    lengthens the parts just enough to fit two rounds, and every visible pair is
+    still covered once."""
+    w = wl.make_custom(prefix, extend, hq, hkv, 128, seed=41)
+    items = _check_plan(w)
+    real = items[items["req"] >= 0]
+    assert (real["part"] >= 0).any()
+    assert 256 < len(real) <= 512, len(real)
+    # a forced split length is kept as given: parts start at its multiples, and every
+    # part but a tile's last is exactly that long
+    f = 30720
+    forced = _check_plan(w, f)
+    fr = forced[(forced["req"] >= 0) & (forced["part"] >= 0)]
+    lens = fr["key_end"] - fr["key_begin"]
+    assert (fr["key_begin"] % f == 0).all() and (lens == f).any() and (lens <= f + 256).all()
 
 
 def test_headers_compile_as_c99_and_work_from_c(tmp_path):
