@@ -321,9 +321,10 @@ int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, in
     if (split_keys <= 0) {
       // Whole rounds: a unit count a little past a multiple of the 256 slots leaves a
       // nearly empty last round.  Lengthen the parts (in whole tiles) when that
-      // removes it for less than the round costs: the smallest split below
-      // split * (k + 1) / k that yields at most k rounds of units (the count never
-      // grows with the split, so a bisection finds it).
+      // removes it for less than half a round (the units spilling into it are often
+      // a tile's short last parts): the smallest split below split * (1 + 1 / 2k)
+      // that yields at most k rounds of units (the count never grows with the
+      // split, so a bisection finds it).
       std::vector<std::pair<int64_t, int64_t>> starts;  // (first query position, tiles)
       for (const Tile& t : tiles) {
         if (!starts.empty() && starts.back().first == t.qpos0) starts.back().second++;
@@ -337,7 +338,7 @@ int make_plan(const kvx_batch* b, const std::vector<int64_t>& qo, int32_t Hq, in
       const int64_t k = (units_at(split) - 1) / kPlanSlots;
       if (k >= 1) {
         const int64_t target = k * kPlanSlots;
-        int64_t lo = split / BN + 1, hi = (split * (k + 1) / k - 1) / BN;  // split lengths in tiles
+        int64_t lo = split / BN + 1, hi = (split + split / (2 * k) - 1) / BN;  // split lengths in tiles
         if (lo <= hi && units_at(hi * BN) <= target) {
           while (lo < hi) {
             const int64_t mid = lo + (hi - lo) / 2;
