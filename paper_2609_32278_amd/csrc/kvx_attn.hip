@@ -1122,37 +1122,42 @@ __global__ __launch_bounds__(kAttnThreads, 1) void extend_attn_fp8_kernel(AttnPa
 }
 
 // Combine the parts of split tiles: o = sum_p e^{lse_p - M} o_p / sum_p e^{lse_p - M}.
+// Rows of a tile per merge workgroup (256 lanes, one 16-byte column group each).
+template <int D>
+constexpr int kMergeRows = 256 / (D / 4);
+static_assert(kTileRows % kMergeRows<128> == 0 && kTileRows % kMergeRows<64> == 0, "whole row blocks");
+
 template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(MergeParams p) {
+  // workgroup (merge, row block): kMergeRows rows of the tile, one 16-byte column
+  // group of one row per lane, so that a merge of few tiles still spreads over the CUs
   const MergeUnit mu = p.merges[blockIdx.x];
   const int kv_head = mu.head_ntok >> 16;
   const int ntok = mu.head_ntok & 0xFFFF;
   constexpr int C4 = D / 4;
-  for (int idx = threadIdx.x; idx < kTileRows * C4; idx += blockDim.x) {
-    const int rho = idx / C4;
-    const int c = (idx % C4) * 4;
-    const int tok = rho / p.group;
-    if (tok >= ntok) continue;
-    const int hq = kv_head * p.group + (rho - tok * p.group);
-    float mx = -INFINITY;
-    for (int q = 0; q < mu.nparts; q++) mx = fmaxf(mx, p.lse_part[(size_t)(mu.part0 + q) * kTileRows + rho]);
-    float wsum = 0.0f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int q = 0; q < mu.nparts; q++) {
-      const float l = p.lse_part[(size_t)(mu.part0 + q) * kTileRows + rho];
-      const float w = (l == -INFINITY) ? 0.0f : __expf(l - mx);
-      const f32x4 v = *(const f32x4*)(p.o_part + ((size_t)(mu.part0 + q) * kTileRows + rho) * D + c);
-      acc += v * w;
-      wsum += w;
-    }
-    const float inv = wsum > 0.0f ? 1.0f / wsum : 0.0f;
-    const size_t row = (size_t)(mu.qo_row0 + tok) * p.num_q_heads + hq;
-    uint2 w2;
-    w2.x = pack_bf16(acc[0] * inv, acc[1] * inv);
-    w2.y = pack_bf16(acc[2] * inv, acc[3] * inv);
-    *(uint2*)(p.out + row * D + c) = w2;
-    if (p.lse != nullptr && c == 0) p.lse[row] = mx + __logf(wsum);
+  const int rho = (int)blockIdx.y * kMergeRows<D> + (int)threadIdx.x / C4;
+  const int c = ((int)threadIdx.x % C4) * 4;
+  const int tok = rho / p.group;
+  if (tok >= ntok) return;
+  const int hq = kv_head * p.group + (rho - tok * p.group);
+  float mx = -INFINITY;
+  for (int q = 0; q < mu.nparts; q++) mx = fmaxf(mx, p.lse_part[(size_t)(mu.part0 + q) * kTileRows + rho]);
+  float wsum = 0.0f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int q = 0; q < mu.nparts; q++) {
+    const float l = p.lse_part[(size_t)(mu.part0 + q) * kTileRows + rho];
+    const float w = (l == -INFINITY) ? 0.0f : __expf(l - mx);
+    const f32x4 v = *(const f32x4*)(p.o_part + ((size_t)(mu.part0 + q) * kTileRows + rho) * D + c);
+    acc += v * w;
+    wsum += w;
   }
+  const float inv = wsum > 0.0f ? 1.0f / wsum : 0.0f;
+  const size_t row = (size_t)(mu.qo_row0 + tok) * p.num_q_heads + hq;
+  uint2 w2;
+  w2.x = pack_bf16(acc[0] * inv, acc[1] * inv);
+  w2.y = pack_bf16(acc[2] * inv, acc[3] * inv);
+  *(uint2*)(p.out + row * D + c) = w2;
+  if (p.lse != nullptr && c == 0) p.lse[row] = mx + __logf(wsum);
 }
 
 }  // namespace
@@ -1175,9 +1180,11 @@ hipError_t launch_extend_attention(const AttnParams& p, int64_t n_units, int hea
 
 hipError_t launch_merge(const MergeParams& p, int64_t n_merges, int head_dim, hipStream_t stream) {
   if (n_merges <= 0) return hipSuccess;
-  dim3 grid((unsigned)n_merges), block(256);
-  if (head_dim == 128) hipLaunchKernelGGL((merge_kernel<128>), grid, block, 0, stream, p);
-  else hipLaunchKernelGGL((merge_kernel<64>), grid, block, 0, stream, p);
+  const dim3 block(256);
+  if (head_dim == 128)
+    hipLaunchKernelGGL((merge_kernel<128>), dim3((unsigned)n_merges, kTileRows / kMergeRows<128>), block, 0, stream, p);
+  else
+    hipLaunchKernelGGL((merge_kernel<64>), dim3((unsigned)n_merges, kTileRows / kMergeRows<64>), block, 0, stream, p);
   return hipGetLastError();
 }
 
